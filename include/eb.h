@@ -1,0 +1,172 @@
+/*
+ * eb.h — C ABI of libeb: the jagged, pooled EmbeddingBag forward on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation.  The paper's DLRM study (Sec. IV-A.2, icicle view) splits a
+ * recommendation model into sparse_arch, which looks rows up in embedding
+ * tables and produces one output embedding per example and categorical
+ * feature, and the dense, interaction and over modules that consume them.  The
+ * inputs of sparse_arch are jagged categorical features (Abstract; Sec. IV-A.3
+ * names embedding-bag lookups over jagged inputs as what sets these models
+ * apart from a GEMM-bound LLM), and the stage is bound by memory bandwidth
+ * (Sec. IV-A.2).  This library computes exactly that stage:
+ *
+ *   T tables; table t has R_t rows of D_t elements.  The batch has B examples.
+ *   Bag g = t*B + b (table-major) holds the index positions
+ *   I_g = [offsets[g], offsets[g+1]).  With x(t,r,d) the fp32 value of element
+ *   d of row r of table t (see eb_table_dtype) and w_i the per-sample weight
+ *   (1 when no weights are given):
+ *
+ *     S[d]                      = sum_{i in I_g} w_i * x(t, indices[i], d)
+ *     out[b, Doff[t] + d]       = S[d]                   (EB_POOL_SUM)
+ *                               = S[d] / |I_g|           (EB_POOL_MEAN)
+ *     an empty bag (|I_g| = 0) yields +0.0 in every mode,
+ *
+ *   where Doff[t] = D_0 + ... + D_{t-1}, so out is [B, sum_t D_t] with the
+ *   tables' pooled vectors concatenated in table order.  Sums accumulate in
+ *   fp32 starting from +0.0; a bag of one row returns that row's value
+ *   (times its weight) rounded once, bit for bit.
+ *
+ * Memory and ownership.  Every data pointer passed to this library (table
+ * rows, indices, offsets, weights, out) is DEVICE memory owned by the caller
+ * and must stay valid until the work that uses it has finished on the
+ * handle's stream.  The handle copies the table descriptors (not the rows)
+ * into a small device array that it owns.
+ *
+ * Streams and synchronisation.  The HIP stream is fixed when the handle is
+ * created.  eb_forward only enqueues one kernel on it and returns; `out` is
+ * valid once that stream has been synchronised.  A handle is immutable after
+ * creation, so forwards from several host threads may share it.
+ *
+ * Errors.  Every error the host can detect from the arguments is returned
+ * before anything is enqueued, and `out` is left untouched.  The kernel never
+ * reads outside the tables, indices, offsets or weights, whatever their
+ * contents: an index outside [0, R_t) contributes nothing, and offsets are
+ * clamped into [0, numel(indices)] and made non-decreasing.  Such inputs
+ * break the contract, so the output for the affected bags is unspecified,
+ * unless checked mode is on: with the environment variable EB_CHECK=1 set
+ * when the handle is created, eb_forward synchronises the stream after the
+ * kernel and returns EB_ERR_INDEX_OOB or EB_ERR_OFFSETS if the kernel met
+ * such data (offsets[0] != 0 and offsets[T*B] != numel(indices) included).
+ * Checked mode is for debugging; it blocks the calling thread.
+ */
+#ifndef EB_H_
+#define EB_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  EB_OK = 0,
+  EB_ERR_INVALID_ARG = -1, /* null pointer, bad count, weights with MEAN ... */
+  EB_ERR_DTYPE = -2,       /* unknown table dtype or element type, or a mismatch */
+  EB_ERR_SHAPE = -3,       /* sizes that do not fit together */
+  EB_ERR_UNSUPPORTED = -4, /* valid request outside what the kernels handle */
+  EB_ERR_INDEX_OOB = -5,   /* checked mode: an index outside its table */
+  EB_ERR_OFFSETS = -6,     /* checked mode: offsets not a valid partition */
+  EB_ERR_OOM = -7,         /* device allocation failed in eb_create_tables */
+  EB_ERR_HIP = -8          /* any other HIP runtime error (no device, launch) */
+} eb_status;
+
+/*
+ * Storage format of one table's rows (row r starts at data + r*row_stride_bytes).
+ *   EB_F32:          D fp32 values; x = the value.
+ *   EB_F16:          D IEEE binary16 values; x = the value widened to fp32
+ *                    (exact).
+ *   EB_INT8_ROWWISE: D unsigned 8-bit codes q[0..D), then an fp16 scale s at
+ *                    byte D and an fp16 bias c at byte D+2 (little endian);
+ *                    x[d] = fp32(s*q[d] + c) rounded once (s*q is exact in
+ *                    fp32, so this equals fmaf(s, q, c)).
+ */
+typedef enum { EB_F32 = 0, EB_F16 = 1, EB_INT8_ROWWISE = 2 } eb_table_dtype;
+
+/* Element type of an eb_tensor. */
+typedef enum { EB_I32 = 0, EB_I64 = 1, EB_T_F32 = 2 } eb_elem_type;
+
+/* Pooling mode.  A weighted sum is EB_POOL_SUM with per_sample_weights. */
+typedef enum { EB_POOL_SUM = 0, EB_POOL_MEAN = 1 } eb_pooling;
+
+/*
+ * One embedding table.  Requirements, checked by eb_create_tables:
+ *   data != NULL; num_rows in [1, 2^31-1]; dim >= 1;
+ *   EB_F32:          dim % 4 == 0,  row_stride_bytes >= 4*dim,  data and
+ *                    row_stride_bytes multiples of 16;
+ *   EB_F16:          dim % 8 == 0,  row_stride_bytes >= 2*dim,  data and
+ *                    row_stride_bytes multiples of 16;
+ *   EB_INT8_ROWWISE: dim % 16 == 0, row_stride_bytes >= dim+4, data and
+ *                    row_stride_bytes multiples of 4 (dim=128 packs rows at
+ *                    132 bytes).
+ *   dim <= 8192.  Any other value gives EB_ERR_INVALID_ARG, an unknown dtype
+ *   EB_ERR_DTYPE, a dim or alignment the kernels cannot take
+ *   EB_ERR_UNSUPPORTED.
+ */
+typedef struct {
+  const void *data;         /* device pointer to row 0 */
+  int64_t num_rows;         /* R_t */
+  int32_t dim;              /* D_t */
+  int32_t dtype;            /* eb_table_dtype */
+  int64_t row_stride_bytes; /* bytes from row r to row r+1 */
+} eb_table_desc;
+
+/* A flat device array: `numel` elements of type `elem_type` at `data`. */
+typedef struct {
+  const void *data;
+  int64_t numel;
+  int32_t elem_type; /* eb_elem_type */
+} eb_tensor;
+
+/* Opaque handle: the table set, its device descriptor array and its stream. */
+typedef struct eb_tables eb_tables;
+
+/*
+ * Create a handle for `num_tables` (1 .. 65535) tables described by `descs`
+ * (host array, copied).  `hip_stream` is the hipStream_t every eb_forward on
+ * this handle enqueues on (NULL = the device's null stream); the current HIP
+ * device at this call is the handle's device.  On success *out receives the
+ * handle, which the caller releases with eb_destroy.  Synchronous: allocates
+ * one small device array (EB_ERR_OOM if that fails) and copies the
+ * descriptors into it.  On error *out is set to NULL.
+ * Paper: Sec. IV-A.2 (sparse_arch's embedding tables) and Sec. III-B.1
+ * (tables too large for one GPU are shrunk to fit it, so the handle takes
+ * tables of any row count that fits in device memory).
+ */
+eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables,
+                           void *hip_stream, eb_tables **out);
+
+/*
+ * Pooled lookup of one batch of jagged categorical features (the jagged
+ * features of the Abstract and Sec. IV-A.3 in, sparse_arch's output
+ * embeddings of Sec. IV-A.2 out).
+ *   indices: EB_I32 or EB_I64, [N]; table-major (all bags of table 0, then
+ *            table 1, ...), each value a row number local to its table.
+ *   offsets: same element type as indices, [T*B + 1]; offsets[0] = 0,
+ *            non-decreasing, offsets[T*B] = N.  B = (numel - 1) / T must be
+ *            an integer >= 1 (else EB_ERR_SHAPE); B <= 2^31-1.
+ *   per_sample_weights: data == NULL for none; else EB_T_F32 [N]
+ *            (EB_ERR_SHAPE if numel != N); not allowed with EB_POOL_MEAN
+ *            (EB_ERR_INVALID_ARG).
+ *   pooling: EB_POOL_SUM or EB_POOL_MEAN (mean divides by |I_g|).
+ *   out:     EB_T_F32 [B * sum_t D_t], row-major [B, sum_t D_t], 16-byte
+ *            aligned (EB_ERR_SHAPE if numel differs, EB_ERR_UNSUPPORTED if
+ *            misaligned).  Every element is written.
+ * Asynchronous on the handle's stream (see checked mode above); allocates
+ * nothing.  N = 0 is valid (all bags empty, out is zero-filled).
+ */
+eb_status eb_forward(const eb_tables *tables, eb_tensor indices,
+                     eb_tensor offsets, eb_tensor per_sample_weights,
+                     eb_pooling pooling, eb_tensor out);
+
+/* Release a handle (synchronises its stream first).  NULL is a no-op. */
+eb_status eb_destroy(eb_tables *tables);
+
+/* Static, never-NULL English description of a status code. */
+const char *eb_status_string(eb_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EB_H_ */

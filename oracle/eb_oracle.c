@@ -1,0 +1,240 @@
+/*
+ * eb_oracle.c — plain, slow CPU oracle for the pooled EmbeddingBag forward.
+ *
+ * TEST INFRASTRUCTURE.  Only the tests, the smoke check and the benchmark's
+ * CPU-baseline leg load this library.  The product path (libeb and its Python
+ * binding) never does, and this file shares no code, header, table or
+ * constant with it.
+ *
+ * What it computes (the plain definition).  The paper's DLRM study
+ * (Sec. IV-A.2) describes sparse_arch as lookups into embedding tables that
+ * produce one output embedding per example and categorical feature; its
+ * inputs are jagged categorical features (Abstract, Sec. IV-A.3: embedding-bag
+ * lookups over jagged inputs).  For T tables, batch B and bag g = t*B + b
+ * covering index positions [off[g], off[g+1]):
+ *
+ *   S[d] = sum_i w_i * x(t, idx[i], d)        (w_i = 1 without weights)
+ *   out  = fl32(S)            for sum pooling
+ *        = fl32(S / L)        for mean pooling, L = off[g+1] - off[g]
+ *        = +0.0               for an empty bag,
+ *
+ * written to out[b, Doff[t] .. Doff[t] + D_t).  S is accumulated in fp64
+ * (the product of two fp32 values is exact in fp64) in index order and
+ * rounded to fp32 once.  x is the fp32 value of a table element:
+ *   fp32 rows:     the stored value;
+ *   fp16 rows:     the binary16 value, decoded here from its bit fields
+ *                  (exact in fp32);
+ *   int8 row-wise: D unsigned codes q, then fp16 scale s and fp16 bias c;
+ *                  x = fp32(s*q + c) rounded once, i.e. fmaf(s, q, c).
+ * The paper fixes none of pooling mode, weights, row format or rounding; the
+ * readings taken here are the ones listed with the oracle's design notes.
+ *
+ * Besides `out`, the oracle can return absum = sum_i |w_i * x_i| (divided by
+ * L for mean) per output element, in fp64: the scale of the a-priori
+ * rounding-error bound that the GPU results are held to.
+ *
+ * Validation mirrors the checks a caller must satisfy: offsets start at 0,
+ * never decrease and end at N; every index lies in [0, R_t).
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define EBO_OK 0
+#define EBO_ERR_INVALID_ARG (-1)
+#define EBO_ERR_DTYPE (-2)
+#define EBO_ERR_SHAPE (-3)
+#define EBO_ERR_INDEX_OOB (-5)
+#define EBO_ERR_OFFSETS (-6)
+
+#define EBO_ROW_F32 0
+#define EBO_ROW_F16 1
+#define EBO_ROW_U8 2
+
+#define EBO_IDX_I32 0
+#define EBO_IDX_I64 1
+
+#define EBO_MODE_SUM 0
+#define EBO_MODE_MEAN 1
+
+typedef struct {
+  const void *data; /* host pointer to row 0, or NULL if no bag asked for reads it */
+  int64_t num_rows;
+  int32_t dim;
+  int32_t dtype;
+  int64_t row_stride_bytes;
+} ebo_table;
+
+/* IEEE 754 binary16 -> double, from the bit fields. */
+double ebo_half_to_double(uint16_t h) {
+  int sign = (h >> 15) & 1;
+  int expo = (h >> 10) & 0x1f;
+  int mant = h & 0x3ff;
+  double v;
+  if (expo == 0) {
+    v = ldexp((double)mant, -24); /* zero or subnormal: mant * 2^-24 */
+  } else if (expo == 31) {
+    v = mant ? NAN : INFINITY;
+  } else {
+    v = ldexp((double)(1024 + mant), expo - 25); /* (1 + mant/1024) * 2^(expo-15) */
+  }
+  return sign ? -v : v;
+}
+
+/* fp32 value of element d of row r (see the header comment). */
+static float ebo_element(const ebo_table *tb, int64_t r, int32_t d) {
+  const unsigned char *row =
+      (const unsigned char *)tb->data + (size_t)r * (size_t)tb->row_stride_bytes;
+  if (tb->dtype == EBO_ROW_F32) {
+    float v;
+    memcpy(&v, row + 4 * (size_t)d, 4);
+    return v;
+  }
+  if (tb->dtype == EBO_ROW_F16) {
+    uint16_t h;
+    memcpy(&h, row + 2 * (size_t)d, 2);
+    return (float)ebo_half_to_double(h);
+  }
+  /* int8 row-wise */
+  uint16_t hs, hc;
+  memcpy(&hs, row + tb->dim, 2);
+  memcpy(&hc, row + tb->dim + 2, 2);
+  float s = (float)ebo_half_to_double(hs);
+  float c = (float)ebo_half_to_double(hc);
+  return fmaf(s, (float)row[d], c);
+}
+
+static int64_t ebo_read_index(const void *p, int32_t type, int64_t i) {
+  if (type == EBO_IDX_I32) return (int64_t)((const int32_t *)p)[i];
+  return ((const int64_t *)p)[i];
+}
+
+/* Pool one bag g into dst[0 .. D_t) (and its error scale into asum, if set). */
+static void ebo_pool_bag(const ebo_table *tb, const void *indices, int32_t index_type,
+                         int64_t lo, int64_t hi, const float *weights, int32_t mode,
+                         float *dst, double *asum) {
+  int64_t L = hi - lo;
+  for (int32_t d = 0; d < tb->dim; ++d) {
+    double acc = 0.0, mag = 0.0;
+    for (int64_t i = lo; i < hi; ++i) {
+      int64_t r = ebo_read_index(indices, index_type, i);
+      double w = weights ? (double)weights[i] : 1.0;
+      double term = w * (double)ebo_element(tb, r, d);
+      acc += term;
+      mag += fabs(term);
+    }
+    if (mode == EBO_MODE_MEAN && L > 0) {
+      acc /= (double)L;
+      mag /= (double)L;
+    }
+    dst[d] = (float)acc;
+    if (asum) asum[d] = mag;
+  }
+}
+
+/*
+ * Forward over all bags (bags == NULL) or over the listed bag ids.
+ *
+ * tables[num_tables]; indices [num_indices]; offsets [num_offsets] with
+ * num_offsets = T*B + 1; weights [num_indices] or NULL.
+ * bags == NULL: out is [B, sum D] row-major (out_ld must be 0 or sum D).
+ * bags != NULL: the k-th listed bag is written to out[k*out_ld .. + D_t);
+ *               out_ld >= max D_t over the listed bags' tables.
+ * asum (optional) has out's layout.  num_threads <= 0 lets OpenMP choose.
+ * Returns 0 or a negative error code; out is not written on error.
+ */
+int ebo_forward(const ebo_table *tables, int32_t num_tables, const void *indices,
+                const void *offsets, int32_t index_type, int64_t num_indices,
+                int64_t num_offsets, const float *weights, int32_t mode,
+                const int64_t *bags, int64_t num_bags, float *out, int64_t out_ld,
+                double *asum, int32_t num_threads) {
+  if (!tables || num_tables < 1 || !offsets || !out) return EBO_ERR_INVALID_ARG;
+  if (num_indices < 0 || (num_indices > 0 && !indices)) return EBO_ERR_INVALID_ARG;
+  if (index_type != EBO_IDX_I32 && index_type != EBO_IDX_I64) return EBO_ERR_DTYPE;
+  if (mode != EBO_MODE_SUM && mode != EBO_MODE_MEAN) return EBO_ERR_INVALID_ARG;
+  if (weights && mode == EBO_MODE_MEAN) return EBO_ERR_INVALID_ARG;
+  if (num_offsets < 2 || (num_offsets - 1) % num_tables != 0) return EBO_ERR_SHAPE;
+  const int64_t B = (num_offsets - 1) / num_tables;
+  const int64_t nbags = num_offsets - 1;
+
+  int64_t sum_d = 0;
+  for (int32_t t = 0; t < num_tables; ++t) {
+    const ebo_table *tb = &tables[t];
+    if (tb->dtype != EBO_ROW_F32 && tb->dtype != EBO_ROW_F16 && tb->dtype != EBO_ROW_U8)
+      return EBO_ERR_DTYPE;
+    if (tb->dim < 1 || tb->num_rows < 1) return EBO_ERR_INVALID_ARG;
+    sum_d += tb->dim;
+  }
+
+  /* offsets must partition [0, N) into T*B consecutive bags */
+  if (ebo_read_index(offsets, index_type, 0) != 0) return EBO_ERR_OFFSETS;
+  for (int64_t g = 0; g < nbags; ++g)
+    if (ebo_read_index(offsets, index_type, g + 1) < ebo_read_index(offsets, index_type, g))
+      return EBO_ERR_OFFSETS;
+  if (ebo_read_index(offsets, index_type, nbags) != num_indices) return EBO_ERR_OFFSETS;
+
+  /* every index must name a row of its bag's table */
+  for (int32_t t = 0; t < num_tables; ++t) {
+    int64_t lo = ebo_read_index(offsets, index_type, (int64_t)t * B);
+    int64_t hi = ebo_read_index(offsets, index_type, (int64_t)(t + 1) * B);
+    for (int64_t i = lo; i < hi; ++i) {
+      int64_t r = ebo_read_index(indices, index_type, i);
+      if (r < 0 || r >= tables[t].num_rows) return EBO_ERR_INDEX_OOB;
+    }
+  }
+
+  int64_t count = bags ? num_bags : nbags;
+  if (count < 0) return EBO_ERR_INVALID_ARG;
+  if (bags) {
+    for (int64_t k = 0; k < count; ++k) {
+      if (bags[k] < 0 || bags[k] >= nbags) return EBO_ERR_INVALID_ARG;
+      const ebo_table *tb = &tables[bags[k] / B];
+      if (out_ld < tb->dim) return EBO_ERR_SHAPE;
+      if (!tb->data && ebo_read_index(offsets, index_type, bags[k] + 1) >
+                           ebo_read_index(offsets, index_type, bags[k]))
+        return EBO_ERR_INVALID_ARG;
+    }
+  } else {
+    if (out_ld != 0 && out_ld != sum_d) return EBO_ERR_SHAPE;
+    out_ld = sum_d;
+    for (int32_t t = 0; t < num_tables; ++t)
+      if (!tables[t].data) return EBO_ERR_INVALID_ARG;
+  }
+
+  /* Doff[t]: first output column of table t */
+  int64_t *doff = (int64_t *)malloc(sizeof(int64_t) * (size_t)num_tables);
+  if (!doff) return EBO_ERR_INVALID_ARG;
+  doff[0] = 0;
+  for (int32_t t = 1; t < num_tables; ++t) doff[t] = doff[t - 1] + tables[t - 1].dim;
+
+  int nthreads = 1;
+#ifdef _OPENMP
+  nthreads = num_threads > 0 ? num_threads : omp_get_max_threads();
+#endif
+  (void)nthreads;
+#pragma omp parallel for schedule(dynamic, 16) num_threads(nthreads)
+  for (int64_t k = 0; k < count; ++k) {
+    int64_t g = bags ? bags[k] : k;
+    int64_t t = g / B, b = g % B;
+    int64_t pos = bags ? k * out_ld : b * out_ld + doff[t];
+    ebo_pool_bag(&tables[t], indices, index_type, ebo_read_index(offsets, index_type, g),
+                 ebo_read_index(offsets, index_type, g + 1), weights, mode, out + pos,
+                 asum ? asum + pos : NULL);
+  }
+  free(doff);
+  return EBO_OK;
+}
+
+/* Number of threads a parallel region would use when num_threads <= 0. */
+int ebo_max_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}

@@ -1,0 +1,168 @@
+"""ctypes marshalling for the plain-C oracle (test infrastructure only).
+
+The oracle computes, for every requested bag g = t*B + b, the fp64 sum
+S[d] = sum_i w_i * x(t, idx_i, d) rounded once to fp32 (divided by the bag
+length first for mean pooling; +0.0 for an empty bag) — the definition of the
+pooled embedding lookup of the paper's sparse_arch (Sec. IV-A.2) over jagged
+categorical features (Abstract, Sec. IV-A.3).  See eb_oracle.c.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "eb_oracle.c")
+_LIB_NAME = "libeb_oracle.so"
+
+_ROW_CODES = {"f32": 0, "f16": 1, "int8_rowwise": 2}
+_MODE_CODES = {"sum": 0, "mean": 1}
+_ERRORS = {-1: "invalid argument", -2: "dtype", -3: "shape", -5: "index out of range", -6: "bad offsets"}
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code: int):
+        super().__init__(f"oracle error {code}: {_ERRORS.get(code, 'unknown')}")
+        self.code = code
+
+
+def lib_path() -> str:
+    return os.path.join(_HERE, _LIB_NAME)
+
+
+def build() -> str:
+    """Compile eb_oracle.c with gcc (-O2, no fast-math, no FP contraction, OpenMP)."""
+    out = lib_path()
+    tmp = out + ".tmp"
+    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+           "-Wall", "-Wextra", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, out)
+    return out
+
+
+class _CTable(ctypes.Structure):
+    _fields_ = [
+        ("data", ctypes.c_void_p),
+        ("num_rows", ctypes.c_int64),
+        ("dim", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("row_stride_bytes", ctypes.c_int64),
+    ]
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        path = lib_path()
+        if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
+            build()
+        lib = ctypes.CDLL(path)
+        lib.ebo_forward.restype = ctypes.c_int
+        lib.ebo_forward.argtypes = [
+            ctypes.POINTER(_CTable), ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+            ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+            ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32,
+        ]
+        lib.ebo_half_to_double.restype = ctypes.c_double
+        lib.ebo_half_to_double.argtypes = [ctypes.c_uint16]
+        lib.ebo_max_threads.restype = ctypes.c_int
+        lib.ebo_max_threads.argtypes = []
+        _lib = lib
+    return _lib
+
+
+@dataclass
+class OracleTable:
+    """Host rows of one table: `rows` is a C-contiguous numpy array whose first
+    axis is the row (its byte stride is the row stride), or None when no bag
+    that is asked for reads this table (then num_rows must be given)."""
+
+    rows: Optional[np.ndarray]
+    dim: int
+    dtype: str
+    num_rows: Optional[int] = None
+
+
+def half_to_double(bits: int) -> float:
+    """The oracle's binary16 decoder (exposed so tests can pin it)."""
+    return float(_load().ebo_half_to_double(int(bits) & 0xFFFF))
+
+
+def max_threads() -> int:
+    return int(_load().ebo_max_threads())
+
+
+def ebo_forward(
+    tables: Sequence[OracleTable],
+    indices: np.ndarray,
+    offsets: np.ndarray,
+    weights: Optional[np.ndarray] = None,
+    pooling: str = "sum",
+    bags: Optional[np.ndarray] = None,
+    num_threads: int = 0,
+    with_absum: bool = False,
+):
+    """Run the oracle.  Returns out (fp32) or (out, absum) with absum fp64.
+
+    bags is None: out is [B, sum D].  Otherwise out is [len(bags), max D] and
+    row k holds bag bags[k] in its first D_t columns.
+    """
+    lib = _load()
+    offsets = np.ascontiguousarray(offsets)
+    indices = np.ascontiguousarray(indices)
+    if offsets.dtype == np.int64:
+        itype = 1
+    elif offsets.dtype == np.int32:
+        itype = 0
+    else:
+        raise TypeError("offsets must be int32 or int64")
+    if indices.dtype != offsets.dtype:
+        raise TypeError("indices and offsets must share a dtype")
+    ct = (_CTable * len(tables))()
+    for i, tb in enumerate(tables):
+        if tb.rows is not None:
+            if not tb.rows.flags["C_CONTIGUOUS"]:
+                raise ValueError("table rows must be C-contiguous")
+            ct[i].data = tb.rows.ctypes.data
+            ct[i].num_rows = tb.rows.shape[0]
+            ct[i].row_stride_bytes = tb.rows.strides[0]
+        else:
+            ct[i].data = None
+            ct[i].num_rows = int(tb.num_rows)
+            ct[i].row_stride_bytes = 0
+        ct[i].dim = int(tb.dim)
+        ct[i].dtype = _ROW_CODES[tb.dtype]
+    T = len(tables)
+    nbags = offsets.size - 1
+    B = nbags // T if T else 0
+    sum_d = sum(int(t.dim) for t in tables)
+    if weights is not None:
+        weights = np.ascontiguousarray(weights, dtype=np.float32)
+    if bags is None:
+        out = np.empty((B, sum_d), dtype=np.float32)
+        ld = sum_d
+        bag_ptr, nsel = None, 0
+    else:
+        bags = np.ascontiguousarray(bags, dtype=np.int64)
+        ld = max(int(t.dim) for t in tables)
+        out = np.empty((bags.size, ld), dtype=np.float32)
+        bag_ptr, nsel = bags.ctypes.data, bags.size
+    absum = np.empty(out.shape, dtype=np.float64) if with_absum else None
+    rc = lib.ebo_forward(
+        ct, T, indices.ctypes.data if indices.size else None, offsets.ctypes.data, itype, indices.size,
+        offsets.size, weights.ctypes.data if weights is not None else None, _MODE_CODES[pooling],
+        bag_ptr, nsel, out.ctypes.data, ld if bags is not None else 0,
+        absum.ctypes.data if absum is not None else None, int(num_threads),
+    )
+    if rc != 0:
+        raise OracleError(rc)
+    return (out, absum) if with_absum else out

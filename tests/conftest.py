@@ -1,0 +1,54 @@
+import os
+import sys
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (runs through the libeb C ABI)")
+
+
+# ----------------------------------------------------------------------------
+# shared helpers (plain numpy; no pooling arithmetic lives here)
+
+
+def ulp_distance(a, b):
+    """Distance in units in the last place between fp32 arrays (0 = same bits,
+    except +0 and -0 count as 0 apart)."""
+    a = np.ascontiguousarray(a, dtype=np.float32).view(np.int32).astype(np.int64)
+    b = np.ascontiguousarray(b, dtype=np.float32).view(np.int32).astype(np.int64)
+    # map the sign-magnitude bit patterns onto a monotone integer line
+    a = np.where(a < 0, -(a & 0x7FFFFFFF), a)
+    b = np.where(b < 0, -(b & 0x7FFFFFFF), b)
+    return np.abs(a - b)
+
+
+def oracle_tables(workload):
+    """Host copies of a workload's tables in the oracle's format."""
+    from oracle import OracleTable
+
+    return [OracleTable(t.rows.detach().cpu().numpy(), t.dim, t.dtype) for t in workload.tables]
+
+
+def oracle_forward(workload, tables=None, bags=None, with_absum=True, num_threads=0):
+    from oracle import ebo_forward
+
+    tables = oracle_tables(workload) if tables is None else tables
+    w = None if workload.weights is None else workload.weights.cpu().numpy()
+    return ebo_forward(tables, workload.indices.cpu().numpy(), workload.offsets.cpu().numpy(), w,
+                       workload.pooling, bags=bags, num_threads=num_threads, with_absum=with_absum)
+
+
+@pytest.fixture(scope="session", autouse=True)
+def _build_oracle_once():
+    from oracle import build, lib_path
+
+    src = os.path.join(ROOT, "oracle", "eb_oracle.c")
+    if not os.path.exists(lib_path()) or os.path.getmtime(lib_path()) < os.path.getmtime(src):
+        build()
+    yield

@@ -1,0 +1,398 @@
+"""Pins for the CPU oracle: it is checked here against things other than itself.
+
+The paper prints no worked example or value for the embedding lookups of its
+DLRM's sparse_arch (Sec. IV-A.2), so the oracle is pinned by
+  * hand-enumerated tiny cases whose results are exact in binary,
+  * the binary16 decoder against numpy's, over all 65536 bit patterns,
+  * invariants of the definition (empty bag, single row, mean = sum / L,
+    permutation, duplicates, unit weights, linearity, table concatenation),
+  * brute force: the dense count matrix A_t times the table in fp64,
+  * a library special case: torch's CPU embedding_bag in float64,
+  * the error codes for inputs that break the contract.
+A plausible slip in the oracle (a dropped term, a wrong index or sign, swapped
+scale and bias, swapped tables, the wrong mean divisor) fails at least one.
+"""
+import numpy as np
+import pytest
+import torch
+
+from conftest import oracle_forward, oracle_tables, ulp_distance
+from oracle import OracleError, OracleTable, ebo_forward, half_to_double
+from paper_2609_30656_amd.workload import make_workload
+
+# ----------------------------------------------------------------------------
+# hand-enumerated worked example (every value exact in binary)
+#   table W (4 x 2): rows [1,2], [3,4], [5,6], [7,8]
+#   indices [2, 0, 3, 3], offsets [0, 2, 2, 4]  ->  B = 3 bags {2,0}, {}, {3,3}
+
+W4 = np.array([[1, 2], [3, 4], [5, 6], [7, 8]], dtype=np.float32)
+IDX = np.array([2, 0, 3, 3], dtype=np.int64)
+OFF = np.array([0, 2, 2, 4], dtype=np.int64)
+
+
+def _tab(rows, dtype="f32", dim=None):
+    return OracleTable(np.ascontiguousarray(rows), rows.shape[1] if dim is None else dim, dtype)
+
+
+@pytest.mark.parametrize("itype", [np.int64, np.int32])
+def test_worked_sum(itype):
+    out = ebo_forward([_tab(W4)], IDX.astype(itype), OFF.astype(itype), pooling="sum")
+    # bag 0: [5,6] + [1,2] = [6,8]; bag 1 empty; bag 2: [7,8] + [7,8] = [14,16]
+    np.testing.assert_array_equal(out, [[6, 8], [0, 0], [14, 16]])
+
+
+def test_worked_mean():
+    out = ebo_forward([_tab(W4)], IDX, OFF, pooling="mean")
+    # [6,8]/2, empty -> 0 (no division), [14,16]/2
+    np.testing.assert_array_equal(out, [[3, 4], [0, 0], [7, 8]])
+
+
+def test_worked_weighted():
+    w = np.array([0.5, 2.0, 1.0, 0.25], dtype=np.float32)
+    out = ebo_forward([_tab(W4)], IDX, OFF, w, pooling="sum")
+    # bag 0: 0.5*[5,6] + 2*[1,2] = [4.5, 7]; bag 2: 1*[7,8] + 0.25*[7,8] = [8.75, 10]
+    np.testing.assert_array_equal(out, [[4.5, 7], [0, 0], [8.75, 10]])
+
+
+def test_worked_two_tables_column_placement():
+    # table 0 = W4 (D=2); table 1 (3 rows, D=3); B = 2; bags are table-major
+    W3 = np.array([[10, 20, 30], [40, 50, 60], [70, 80, 90]], dtype=np.float32)
+    idx = np.array([1, 3, 0, 2, 2, 1], dtype=np.int64)
+    # t0 b0: {1,3}; t0 b1: {}; t1 b0: {0}; t1 b1: {2,2,1}
+    off = np.array([0, 2, 2, 3, 6], dtype=np.int64)
+    out = ebo_forward([_tab(W4), _tab(W3)], idx, off)
+    # row b holds [table 0 (2 cols) | table 1 (3 cols)]
+    expect = [
+        [3 + 7, 4 + 8, 10, 20, 30],
+        [0, 0, 70 + 70 + 40, 80 + 80 + 50, 90 + 90 + 60],
+    ]
+    np.testing.assert_array_equal(out, expect)
+
+
+def test_worked_int8_rowwise_dequant():
+    # D = 2 codes, then fp16 scale 0.5 (0x3800) and fp16 bias -1 (0xBC00)
+    rows = np.zeros((2, 6), dtype=np.uint8)
+    rows[0, :2] = [0, 255]
+    rows[0, 2:4] = np.frombuffer(np.float16(0.5).tobytes(), np.uint8)
+    rows[0, 4:6] = np.frombuffer(np.float16(-1.0).tobytes(), np.uint8)
+    rows[1, :2] = [2, 4]
+    rows[1, 2:4] = np.frombuffer(np.float16(0.25).tobytes(), np.uint8)
+    rows[1, 4:6] = np.frombuffer(np.float16(3.0).tobytes(), np.uint8)
+    t = OracleTable(rows, 2, "int8_rowwise")
+    out = ebo_forward([t], np.array([0, 0, 1], np.int64), np.array([0, 1, 3], np.int64))
+    # row 0: 0.5*[0,255] - 1 = [-1, 126.5]; row 1: 0.25*[2,4] + 3 = [3.5, 4]
+    np.testing.assert_array_equal(out, [[-1, 126.5], [-1 + 3.5, 126.5 + 4]])
+
+
+def test_worked_f16_rows():
+    bits = np.array([[0x3C00, 0xC000], [0x0001, 0x7BFF]], dtype=np.uint16)  # 1, -2, 2^-24, 65504
+    t = OracleTable(bits.view(np.float16), 2, "f16")
+    out = ebo_forward([t], np.array([0, 1, 1], np.int64), np.array([0, 1, 3], np.int64))
+    np.testing.assert_array_equal(out, np.array([[1, -2], [2 * 2.0**-24, 2 * 65504]], np.float32))
+
+
+# ----------------------------------------------------------------------------
+# binary16 decoder, exhaustively against numpy
+
+
+def test_half_decoder_exhaustive():
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    ref = bits.view(np.float16).astype(np.float64)
+    got = np.array([half_to_double(int(b)) for b in bits])
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))  # -0.0 keeps its sign
+
+
+# ----------------------------------------------------------------------------
+# invariants on random tables
+
+
+def _rand_table(rng, R, D, dtype):
+    if dtype == "f32":
+        return OracleTable(rng.uniform(-1, 1, (R, D)).astype(np.float32), D, "f32")
+    if dtype == "f16":
+        return OracleTable((rng.standard_normal((R, D)) * 0.01).astype(np.float16), D, "f16")
+    rows = np.zeros((R, D + 4), np.uint8)
+    rows[:, :D] = rng.integers(0, 256, (R, D))
+    rows[:, D:D + 2] = rng.uniform(1e-4, 4e-4, R).astype(np.float16).view(np.uint8).reshape(R, 2)
+    rows[:, D + 2:] = rng.uniform(-0.06, -0.02, R).astype(np.float16).view(np.uint8).reshape(R, 2)
+    return OracleTable(rows, D, "int8_rowwise")
+
+
+def _decode(t: OracleTable) -> np.ndarray:
+    """fp32 element values by an independent route (numpy), as float64."""
+    if t.dtype == "f32":
+        return t.rows.astype(np.float64)
+    if t.dtype == "f16":
+        return t.rows.astype(np.float64)
+    D = t.dim
+    q = t.rows[:, :D].astype(np.float64)
+    s = t.rows[:, D:D + 2].copy().view(np.float16).astype(np.float64)
+    c = t.rows[:, D + 2:D + 4].copy().view(np.float16).astype(np.float64)
+    # s*q + c is exact in fp64 for these magnitudes, so one rounding to fp32
+    return (s * q + c).astype(np.float32).astype(np.float64)
+
+
+DTYPES = ["f32", "f16", "int8_rowwise"]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_single_row_bag_is_the_row_bit_exact(dtype):
+    rng = np.random.default_rng(11)
+    t = _rand_table(rng, 50, 32, dtype)
+    idx = rng.integers(0, 50, 40).astype(np.int64)
+    off = np.arange(41, dtype=np.int64)
+    for mode in ("sum", "mean"):
+        out = ebo_forward([t], idx, off, pooling=mode)
+        expect = _decode(t)[idx].astype(np.float32)
+        expect = expect + np.float32(0)  # -0.0 -> +0.0: the sum starts at +0.0
+        assert np.array_equal(out.view(np.uint32), expect.view(np.uint32)), mode
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_empty_bags_are_positive_zero(dtype):
+    rng = np.random.default_rng(12)
+    t = _rand_table(rng, 20, 16, dtype)
+    off = np.array([0, 0, 3, 3, 3], np.int64)
+    idx = np.array([1, 2, 3], np.int64)
+    for mode in ("sum", "mean"):
+        out = ebo_forward([t], idx, off, pooling=mode)
+        for b in (0, 2, 3):
+            assert np.all(out[b].view(np.uint32) == 0), (mode, b)
+
+
+def test_negative_zero_element_pools_to_positive_zero():
+    t = OracleTable(np.array([[-0.0, 1.0]], np.float32), 2, "f32")
+    out = ebo_forward([t], np.array([0], np.int64), np.array([0, 1], np.int64))
+    assert out.view(np.uint32)[0, 0] == 0
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_mean_is_sum_over_length(dtype):
+    rng = np.random.default_rng(13)
+    t = _rand_table(rng, 100, 32, dtype)
+    lens = rng.integers(0, 30, 64)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    idx = rng.integers(0, 100, off[-1]).astype(np.int64)
+    s = ebo_forward([t], idx, off, pooling="sum")
+    m = ebo_forward([t], idx, off, pooling="mean")
+    ref = (s / np.maximum(lens, 1)[:, None]).astype(np.float32)
+    assert ulp_distance(m, ref).max() <= 1
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_permutation_within_bags(dtype):
+    rng = np.random.default_rng(14)
+    t = _rand_table(rng, 200, 16, dtype)
+    lens = rng.integers(0, 60, 32)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    idx = rng.integers(0, 200, off[-1]).astype(np.int64)
+    w = rng.uniform(0, 1, off[-1]).astype(np.float32)
+    perm = np.concatenate([off[b] + rng.permutation(lens[b]) for b in range(32)]).astype(np.int64)
+    a = ebo_forward([t], idx, off, w)
+    b = ebo_forward([t], idx[perm], off, w[perm])
+    assert ulp_distance(a, b).max() <= 1
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_duplicates_count_per_occurrence(dtype):
+    rng = np.random.default_rng(15)
+    t = _rand_table(rng, 10, 16, dtype)
+    x = _decode(t)
+    for k in (2, 3, 4, 7, 8):
+        out = ebo_forward([t], np.full(k, 5, np.int64), np.array([0, k], np.int64))
+        expect = (k * x[5]).astype(np.float32)  # k*x is exact in fp64; one rounding
+        assert np.array_equal(out[0], expect), k
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_unit_weights_equal_sum(dtype):
+    rng = np.random.default_rng(16)
+    t = _rand_table(rng, 64, 32, dtype)
+    lens = rng.integers(0, 40, 50)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    idx = rng.integers(0, 64, off[-1]).astype(np.int64)
+    a = ebo_forward([t], idx, off)
+    b = ebo_forward([t], idx, off, np.ones(off[-1], np.float32))
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_weights_scale_linearly():
+    rng = np.random.default_rng(17)
+    t = _rand_table(rng, 64, 16, "f32")
+    lens = rng.integers(1, 40, 50)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    idx = rng.integers(0, 64, off[-1]).astype(np.int64)
+    w = rng.uniform(0, 1, off[-1]).astype(np.float32)
+    a = ebo_forward([t], idx, off, w)
+    b = ebo_forward([t], idx, off, (w * 4).astype(np.float32))  # power of two: exact
+    assert np.array_equal((a * 4).view(np.uint32), b.view(np.uint32))
+
+
+def test_linear_in_table_values():
+    rng = np.random.default_rng(18)
+    W1 = rng.uniform(-1, 1, (80, 16)).astype(np.float32)
+    W2 = rng.uniform(-1, 1, (80, 16)).astype(np.float32)
+    lens = rng.integers(0, 30, 40)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    idx = rng.integers(0, 80, off[-1]).astype(np.int64)
+    a, sa = ebo_forward([_tab(W1)], idx, off, with_absum=True)
+    b, sb = ebo_forward([_tab(W2)], idx, off, with_absum=True)
+    c = ebo_forward([_tab((W1.astype(np.float64) + W2).astype(np.float32))], idx, off)
+    # W1 + W2 is rounded per element, so the sums agree to a few ulps of the scale
+    assert np.all(np.abs(c.astype(np.float64) - a - b) <= 4 * 2.0**-24 * (sa + sb) + 1e-30)
+
+
+def test_concat_equals_independent_tables():
+    w = make_workload("c4", "cpu", rows_cap=500, batch=16, num_tables=7)
+    full = oracle_forward(w, with_absum=False)
+    T, B = w.num_tables, w.batch
+    off = w.offsets.numpy()
+    idx = w.indices.numpy()
+    col = 0
+    for t, tab in enumerate(oracle_tables(w)):
+        lo, hi = off[t * B], off[(t + 1) * B]
+        part = ebo_forward([tab], idx[lo:hi], off[t * B:(t + 1) * B + 1] - lo)
+        assert np.array_equal(full[:, col:col + tab.dim].view(np.uint32), part.view(np.uint32))
+        col += tab.dim
+
+
+# ----------------------------------------------------------------------------
+# brute force: dense count matrix times table in fp64
+
+
+def _brute(tables, idx, off, w, pooling):
+    T = len(tables)
+    B = (off.size - 1) // T
+    cols = []
+    for t, tab in enumerate(tables):
+        X = _decode(tab)
+        A = np.zeros((B, X.shape[0]), np.float64)
+        for b in range(B):
+            g = t * B + b
+            for i in range(off[g], off[g + 1]):
+                A[b, idx[i]] += 1.0 if w is None else float(w[i])
+        S = A @ X
+        absS = np.abs(A) @ np.abs(X)
+        if pooling == "mean":
+            L = np.maximum(off[t * B + 1:(t + 1) * B + 1] - off[t * B:(t + 1) * B], 1)[:, None]
+            S, absS = S / L, absS / L
+        cols.append((S, absS))
+    return np.hstack([c[0] for c in cols]), np.hstack([c[1] for c in cols])
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3a", "c3b", "c4", "c5"])
+def test_brute_force_dense_product(name):
+    kw = dict(rows_cap=2000, batch=24)
+    if name in ("c4", "c5", "c2"):
+        kw["num_tables"] = 6
+    if name == "c1":
+        kw = {}
+    w = make_workload(name, "cpu", **kw)
+    tabs = oracle_tables(w)
+    idx, off = w.indices.numpy(), w.offsets.numpy()
+    wt = None if w.weights is None else w.weights.numpy()
+    out, asum = oracle_forward(w, tables=tabs)
+    S, absS = _brute(tabs, idx, off, wt, w.pooling)
+    # fp64 sums in two orders differ by far less than one fp32 ulp, so after one
+    # rounding the two agree except at near-ties (then by one ulp)
+    d = ulp_distance(out, S.astype(np.float32))
+    assert d.max() <= 1
+    assert (d == 0).mean() > 0.99
+    np.testing.assert_allclose(asum, absS, rtol=1e-12, atol=0)
+
+
+# ----------------------------------------------------------------------------
+# library special case: torch.nn.functional.embedding_bag on the CPU in float64
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3a", "c3b"])
+def test_torch_embedding_bag_float64(name):
+    kw = {} if name == "c1" else dict(rows_cap=3000, batch=40, num_tables=3)
+    w = make_workload(name, "cpu", **kw)
+    out = oracle_forward(w, with_absum=False)
+    B = w.batch
+    col = 0
+    for t, tab in enumerate(oracle_tables(w)):
+        X = torch.from_numpy(_decode(tab))
+        lo, hi = int(w.offsets[t * B]), int(w.offsets[(t + 1) * B])
+        off = w.offsets[t * B:(t + 1) * B + 1] - lo
+        idx = w.indices[lo:hi]
+        psw = None if w.weights is None else w.weights[lo:hi].double()
+        ref = torch.nn.functional.embedding_bag(idx, X, off, mode=w.pooling, per_sample_weights=psw,
+                                                include_last_offset=True)
+        d = ulp_distance(out[:, col:col + tab.dim], ref.numpy().astype(np.float32))
+        assert d.max() <= 1
+        col += tab.dim
+
+
+# ----------------------------------------------------------------------------
+# contract violations -> error codes
+
+
+def test_error_codes():
+    t = _tab(W4)
+    with pytest.raises(OracleError) as e:
+        ebo_forward([t], np.array([2, 0, 4, 3], np.int64), OFF)  # row 4 of a 4-row table
+    assert e.value.code == -5
+    with pytest.raises(OracleError) as e:
+        ebo_forward([t], np.array([2, 0, -1, 3], np.int64), OFF)
+    assert e.value.code == -5
+    with pytest.raises(OracleError) as e:
+        ebo_forward([t], IDX, np.array([1, 2, 2, 4], np.int64))  # offsets[0] != 0
+    assert e.value.code == -6
+    with pytest.raises(OracleError) as e:
+        ebo_forward([t], IDX, np.array([0, 3, 2, 4], np.int64))  # decreasing
+    assert e.value.code == -6
+    with pytest.raises(OracleError) as e:
+        ebo_forward([t], IDX, np.array([0, 2, 2, 3], np.int64))  # last != N
+    assert e.value.code == -6
+    with pytest.raises(OracleError) as e:
+        ebo_forward([t], IDX, OFF, np.ones(4, np.float32), pooling="mean")  # weights with mean
+    assert e.value.code == -1
+    with pytest.raises(OracleError) as e:
+        ebo_forward([t, t], IDX, OFF)  # 3 bags do not split over 2 tables
+    assert e.value.code == -3
+
+
+def test_bag_subset_matches_full():
+    w = make_workload("c3b", "cpu", rows_cap=1000, batch=32, num_tables=3)
+    full = oracle_forward(w, with_absum=False)
+    bags = np.array([0, 5, 31, 32, 63, 64, 95], np.int64)
+    sub = oracle_forward(w, bags=bags, with_absum=False)
+    B = w.batch
+    for k, g in enumerate(bags):
+        t, b = divmod(int(g), B)
+        assert np.array_equal(sub[k, :128], full[b, t * 128:(t + 1) * 128])
+
+
+def test_thread_count_does_not_change_results():
+    w = make_workload("c2", "cpu", rows_cap=5000, batch=64, num_tables=4)
+    a = oracle_forward(w, with_absum=False, num_threads=1)
+    b = oracle_forward(w, with_absum=False, num_threads=4)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+# ----------------------------------------------------------------------------
+# frozen record of the oracle (tests/golden/oracle_regression.json)
+
+
+def test_oracle_matches_frozen_record():
+    import json
+    import os
+
+    path = os.path.join(os.path.dirname(__file__), "golden", "oracle_regression.json")
+    with open(path) as f:
+        doc = json.load(f)
+    for case in doc["cases"]:
+        tabs = []
+        for k in ("f32", "f16", "int8_rowwise"):
+            raw = np.array(case["tables"][k], dtype=np.uint8)
+            arr = raw.view({"f32": np.float32, "f16": np.float16, "int8_rowwise": np.uint8}[k])
+            tabs.append(OracleTable(np.ascontiguousarray(arr), case["dim"], k))
+        w = None if case["weights"] is None else np.array(case["weights"], np.uint32).view(np.float32)
+        out = ebo_forward(tabs, np.array(case["indices"], np.int64), np.array(case["offsets"], np.int64), w,
+                          case["pooling"])
+        assert np.array_equal(out.view(np.uint32), np.array(case["out_bits"], np.uint32))
