@@ -1,0 +1,254 @@
+#!/usr/bin/env python3
+"""Benchmark: pooled EmbeddingBag forward on one MI355X.
+
+One step = one eb_forward over one batch of the workload (all tables, all
+bags).  Three independently seeded index batches over the same tables are
+rotated so consecutive steps do not replay identical lookups.  Tables,
+indices and offsets are resident in HBM before the timed region starts.
+
+Prints one JSON line:
+  value            algorithmic GB/s over the K timed steps (wall clock)
+  lookups_per_s    pooled lookups per second over the same steps
+  roofline         eb_pool_kernel's algorithmic bytes per launch / its mean
+                   launch time from HIP events on the library's stream,
+                   against 8 TB/s HBM3E; traffic from rocprofv3 counters
+  cpu_baseline     the CPU oracle on a bounded sample of the same workload
+
+Algorithmic bytes per step = gathered row bytes (every lookup, duplicates
+counted) + index bytes + offset bytes + weight bytes + output bytes.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "EmbeddingBag fwd achieved HBM GB/s (% of peak) + pooled lookups/sec, 1 GPU"
+KERNEL_NAME = "eb_pool_kernel"
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_30656_amd", "csrc", "eb.hip")
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def counter_traffic(config: str, index_law: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"eb_pool_kernel_{config}_{index_law}_pmc.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.split("=", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_cores() -> int:
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
+def run_cpu_baseline(w, budget_s: float, host_bytes_cap: float = 3e9):
+    """Time the oracle (as it stands) on the bags of the first tables of `w`
+    whose rows fit in `host_bytes_cap` bytes of host memory (all tables for the
+    smaller workloads), repeated until `budget_s` seconds have passed.
+    Returns (reps, seconds, threads, lookups per rep, algorithmic bytes per rep,
+    tables used)."""
+    import numpy as np
+
+    import oracle
+
+    threads = min(cpu_cores(), int(os.environ.get("OMP_NUM_THREADS", cpu_cores())))
+    use, acc = 0, 0
+    for t in w.tables:
+        nbytes = t.rows.numel() * t.rows.element_size()
+        if use and acc + nbytes > host_bytes_cap:
+            break
+        acc += nbytes
+        use += 1
+    tabs = [oracle.OracleTable(t.rows.cpu().numpy() if i < use else None, t.dim, t.dtype, t.num_rows)
+            for i, t in enumerate(w.tables)]
+    idx = w.indices.cpu().numpy()
+    off = w.offsets.cpu().numpy()
+    wt = None if w.weights is None else w.weights.cpu().numpy()
+    B = w.batch
+    bags = None if use == w.num_tables else np.arange(use * B, dtype=np.int64)
+    lens = w.lengths.view(w.num_tables, B).sum(dim=1).cpu().tolist()
+    look = int(sum(lens[:use]))
+    esz = w.indices.element_size()
+    nbytes = sum(int(lens[t]) * w.tables[t].row_bytes + B * w.tables[t].dim * 4 for t in range(use))
+    nbytes += look * (esz + (4 if wt is not None else 0)) + (use * B + 1) * esz
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.ebo_forward(tabs, idx, off, wt, w.pooling, bags=bags, num_threads=threads)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return reps, el, threads, look, nbytes, use
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="c2", help="workload: c1 c2 c3a c3b c4 c5")
+    ap.add_argument("--index-law", default="zipf", choices=["zipf", "uniform"],
+                    help="uniform = no-reuse control at the same shapes")
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing (0 = skip)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a 1 GiB device copy (to scale rocprofv3 byte counters)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the pooled lookup on one GPU is the per-GPU share of a table-wise sharded job)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_30656_amd import eb
+    from paper_2609_30656_amd.workload import CONFIGS, make_workload
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    lib = eb.load_library()
+    law = None if args.index_law == "zipf" else "uniform"
+
+    print(f"[bench] generating {args.config} ({CONFIGS[args.config].summary})", file=sys.stderr, flush=True)
+    batches = [make_workload(args.config, dev, batch_seed=0, index_law=law)]
+    for s in (1, 2):
+        batches.append(make_workload(args.config, dev, batch_seed=s, index_law=law, tables=batches[0].tables))
+    w0 = batches[0]
+    out = torch.empty((w0.batch, w0.sum_dim), dtype=torch.float32, device=dev)
+    algo = [b.algorithmic_bytes() for b in batches]
+    nlook = [b.num_indices for b in batches]
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.Stream(device=dev)  # default priority
+    h = eb.eb_create_tables(w0.tables, stream)
+    # marshal once; the loop only calls into the library
+    calls = [(eb._as_tensor(b.indices), eb._as_tensor(b.offsets), eb._as_tensor(b.weights),
+              eb.POOLING[b.pooling]) for b in batches]
+    o = eb._as_tensor(out)
+
+    def step(k):
+        i, f, wt, mode = calls[k % 3]
+        st = lib.eb_forward(h.ptr, i, f, wt, mode, o)
+        if st != eb.EB_OK:
+            raise eb.EBError(st, "eb_forward")
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record(stream)
+        step(k)
+        ends[k].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    kern_avg_s = sum(kern_ms) / len(kern_ms) / 1e3
+
+    bytes_total = sum(algo[k % 3] for k in range(args.steps))
+    look_total = sum(nlook[k % 3] for k in range(args.steps))
+    value = bytes_total / wall / 1e9
+    bytes_per_launch = bytes_total / args.steps
+    achieved = bytes_per_launch / kern_avg_s / 1e9
+    traffic = counter_traffic(args.config, args.index_law)
+
+    if args.copy_calibration:
+        n = 1 << 28  # 1 GiB of fp32
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    eb.eb_destroy(h)
+
+    cpu = None
+    if args.cpu_budget > 0:
+        print(f"[bench] CPU oracle baseline ({args.cpu_budget:.0f} s budget)", file=sys.stderr, flush=True)
+        reps, el, threads, look, nbytes, use = run_cpu_baseline(w0, args.cpu_budget)
+        what = "the whole batch" if use == w0.num_tables else f"the bags of tables 0..{use - 1} of {w0.num_tables}"
+        cpu = {
+            "value": round(nbytes * reps / el / 1e9, 4),
+            "unit": "GB/s",
+            "lookups_per_s": round(look * reps / el, 1),
+            "cores": threads,
+            "kind": "oracle",
+            "sample": f"{reps} pass(es) of the oracle over {what} of batch 0 of {args.config} "
+                      f"({look} lookups per pass) on the host, {el:.1f} s",
+        }
+
+    dtypes = sorted({t.dtype for t in w0.tables})
+    line = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "pct_of_peak_hbm": round(100.0 * value / PEAK_HBM_GBS, 2),
+        "lookups_per_s": round(look_total / wall, 1),
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.config}: {CONFIGS[args.config].summary}",
+            "index_law": args.index_law,
+            "tables": w0.num_tables,
+            "batch": w0.batch,
+            "bags": w0.num_bags,
+            "lookups_per_step": round(sum(nlook) / 3),
+            "algorithmic_bytes_per_step": round(sum(algo) / 3),
+            "index_dtype": str(w0.indices.dtype).replace("torch.", ""),
+            "table_storage": dtypes,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": KERNEL_NAME,
+            "achieved": round(achieved, 2),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": None if traffic is None else round(traffic),
+            "kernel_ms_avg": round(kern_avg_s * 1e3, 5),
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,489 @@
+// libeb — pooled EmbeddingBag forward for the AMD Instinct MI355X (gfx950).
+//
+// The operation is the embedding-table lookup stage (sparse_arch) of the
+// paper's DLRM study (Sec. IV-A.2): jagged categorical features in, one
+// pooled output embedding per (example, feature) out.  The paper finds that
+// stage bound by memory bandwidth with almost no arithmetic, so the kernel is
+// built around the HBM3E roofline: every byte of a gathered row is fetched
+// once with 128-bit loads, converted in registers and summed in fp32; there
+// is no matrix-core work because there is no dense contraction.
+//
+// Execution model (one wavefront of 64 lanes per bag):
+//   * a bag's row is split into 16-byte lane slices; LPR = lanes per row
+//     (the next power of two >= row bytes / 16, at most 64), so one wave-wide
+//     load instruction fetches RPL = 64 / LPR rows of the bag at once;
+//   * the bag's indices are read 64 at a time with one coalesced load and
+//     handed to the lanes of each row group by a cross-lane permute;
+//   * each lane accumulates its slice in fp32 registers; the RPL row groups
+//     are then combined by a butterfly over lanes and one group stores the
+//     pooled vector;
+//   * tables of every storage type and width are served by one launch: the
+//     (dtype, LPR) pair of the bag's table selects a specialised body, which
+//     is uniform across the wave.
+// Rows wider than 1 KiB take several 1 KiB column passes.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "eb.h"
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = 4;
+constexpr int kBlock = kWave * kWavesPerBlock;
+constexpr int kPassBytes = kWave * 16;  // one wave-wide 16-byte load covers 1 KiB
+constexpr uint32_t kBadRow = 0xFFFFFFFFu;
+constexpr int kMaxDim = 8192;
+
+// error bits raised by the kernel, reported in checked mode
+constexpr int kErrIndex = 1;
+constexpr int kErrOffsets = 2;
+
+enum : int32_t { kF32 = 0, kF16 = 1, kU8 = 2 };
+
+// Per-table descriptor as the kernel sees it (one scalar-cache line each).
+struct TableMeta {
+  const unsigned char *data;
+  uint32_t row_stride;  // bytes
+  int32_t num_rows;
+  int32_t dim;
+  int32_t code_bytes;   // element bytes per row: 4*dim, 2*dim or dim
+  int32_t out_col;      // first output column of this table
+  int32_t kind;         // dtype * 8 + log2(lanes per row)
+  int32_t passes;       // 1 KiB column passes per row
+  int32_t pad_;
+};
+
+struct FwdArgs {
+  const TableMeta *meta;
+  const void *indices;
+  const void *offsets;
+  const float *weights;
+  float *out;
+  int *err;
+  int64_t num_indices;
+  int64_t out_ld;
+  int32_t num_bags;
+  int32_t batch;
+  int32_t idx64;
+  int32_t mean;
+};
+
+// Table rows are plain device memory: address them in the global address
+// space so gathers compile to global (not flat) loads.
+#define EB_GLOBAL __attribute__((address_space(1)))
+typedef const EB_GLOBAL unsigned char gbyte;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// same vector, only 4-byte aligned: int8 rows of D+4 bytes start on any dword
+typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int DT>
+struct Vals {
+  static constexpr int n = DT == kF32 ? 4 : (DT == kF16 ? 8 : 16);  // values per 16 B
+  static constexpr int esize = DT == kF32 ? 4 : (DT == kF16 ? 2 : 1);
+};
+
+__device__ __forceinline__ float half_lo(uint32_t v) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(v & 0xFFFFu));
+}
+__device__ __forceinline__ float half_hi(uint32_t v) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(v >> 16));
+}
+
+// acc += x (or acc = w*x + acc) for the 16-byte slice v of one row.
+template <int DT, bool W>
+__device__ __forceinline__ void accumulate(float (&acc)[Vals<DT>::n], u32x4 v, uint32_t sb, float w) {
+  if constexpr (DT == kF32) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float x = __uint_as_float(v[i]);
+      acc[i] = W ? fmaf(w, x, acc[i]) : acc[i] + x;
+    }
+  } else if constexpr (DT == kF16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float x0 = half_lo(v[i]), x1 = half_hi(v[i]);
+      acc[2 * i] = W ? fmaf(w, x0, acc[2 * i]) : acc[2 * i] + x0;
+      acc[2 * i + 1] = W ? fmaf(w, x1, acc[2 * i + 1]) : acc[2 * i + 1] + x1;
+    }
+  } else {
+    // x = fp32(s*q + c): s*q is exact in fp32 (11-bit by 8-bit significands),
+    // so the fma rounds once, as the dequantisation is defined
+    const float s = half_lo(sb), c = half_hi(sb);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float q = (float)((v[i] >> (8 * j)) & 0xFFu);
+        const float x = fmaf(s, q, c);
+        acc[4 * i + j] = W ? fmaf(w, x, acc[4 * i + j]) : acc[4 * i + j] + x;
+      }
+    }
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ u32x4 load_slice(gbyte *p) {
+  if constexpr (DT == kU8) {
+    return *reinterpret_cast<const EB_GLOBAL u32x4_a4 *>(p);
+  } else {
+    return *reinterpret_cast<const EB_GLOBAL u32x4 *>(p);
+  }
+}
+
+// Loads in flight per lane before the first is consumed: enough rows per
+// wave to cover HBM latency, within a 64-VGPR budget.
+template <int RPL>
+struct Unroll {
+  static constexpr int u = RPL >= 16 ? 2 : (RPL >= 8 ? 4 : 8);
+};
+
+// Pool one bag over the 1 KiB column window starting at byte col_base.
+template <int DT, int LPR, bool W>
+__device__ __forceinline__ void pool_bag(const TableMeta &m, const FwdArgs &a, int64_t lo, int64_t hi,
+                                         float *dst, int col_base) {
+  constexpr int RPL = kWave / LPR;
+  constexpr int V = Vals<DT>::n;
+  constexpr int U = Unroll<RPL>::u;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int grp = lane / LPR;
+  const int colb = col_base + (lane % LPR) * 16;
+  const bool colok = colb < m.code_bytes;
+
+  float acc[V];
+#pragma unroll
+  for (int i = 0; i < V; ++i) acc[i] = 0.0f;
+
+  for (int64_t c = lo; c < hi; c += kWave) {
+    const int n = (int)((hi - c) < kWave ? (hi - c) : kWave);
+    uint32_t my_row = kBadRow;
+    float my_w = 0.0f;
+    if (lane < n) {
+      const int64_t r = a.idx64 ? static_cast<const int64_t *>(a.indices)[c + lane]
+                                : (int64_t) static_cast<const int32_t *>(a.indices)[c + lane];
+      if (r >= 0 && r < m.num_rows) my_row = (uint32_t)r;
+      if constexpr (W) my_w = a.weights[c + lane];
+    }
+    if (__ballot(lane < n && my_row == kBadRow)) {
+      if (lane == 0) atomicOr(a.err, kErrIndex);
+    }
+    const int steps = (n + RPL - 1) / RPL;
+    for (int s = 0; s < steps; s += U) {
+      u32x4 v[U];
+      uint32_t sb[U];
+      float w[U];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = (s + u) * RPL + grp;
+        uint32_t row;
+        if constexpr (RPL == 1) {
+          row = __builtin_amdgcn_readlane(my_row, (s + u) & (kWave - 1));
+          if constexpr (W) w[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                       __builtin_bit_cast(uint32_t, my_w), (s + u) & (kWave - 1)));
+        } else {
+          row = (uint32_t)__shfl((int)my_row, r & (kWave - 1));
+          if constexpr (W) w[u] = __shfl(my_w, r & (kWave - 1));
+        }
+        ok[u] = (r < n) && (row != kBadRow) && colok;
+        v[u] = u32x4{0u, 0u, 0u, 0u};
+        sb[u] = 0u;
+        if (ok[u]) {
+          gbyte *p = (gbyte *)m.data + (uint64_t)row * m.row_stride;
+          v[u] = load_slice<DT>(p + colb);
+          if constexpr (DT == kU8) sb[u] = *reinterpret_cast<const EB_GLOBAL uint32_t *>(p + m.dim);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (ok[u]) accumulate<DT, W>(acc, v[u], sb[u], W ? w[u] : 1.0f);
+      }
+    }
+  }
+
+  // combine the RPL row groups (fixed butterfly order: deterministic)
+#pragma unroll
+  for (int o = LPR; o < kWave; o <<= 1) {
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] += __shfl_xor(acc[i], o);
+  }
+
+  if (grp == 0 && colok) {
+    const int64_t L = hi - lo;
+    if (a.mean && L > 0) {
+      const float fl = (float)L;
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] = acc[i] / fl;
+    }
+    f32x4 *o4 = reinterpret_cast<f32x4 *>(dst + colb / Vals<DT>::esize);
+#pragma unroll
+    for (int i = 0; i < V / 4; ++i) o4[i] = f32x4{acc[4 * i], acc[4 * i + 1], acc[4 * i + 2], acc[4 * i + 3]};
+  }
+}
+
+template <int DT, int LPR, bool W>
+__device__ __forceinline__ void pool_all_passes(const TableMeta &m, const FwdArgs &a, int64_t lo, int64_t hi,
+                                                float *dst) {
+  if constexpr (LPR == kWave) {
+    for (int p = 0; p < m.passes; ++p) pool_bag<DT, LPR, W>(m, a, lo, hi, dst, p * kPassBytes);
+  } else {
+    pool_bag<DT, LPR, W>(m, a, lo, hi, dst, 0);
+  }
+}
+
+#define EB_KIND(DT, LOG2)                                                     \
+  case (DT)*8 + (LOG2):                                                       \
+    pool_all_passes<DT, (1 << (LOG2)), W>(m, a, lo, hi, dst);                 \
+    break;
+
+template <bool W>
+__global__ __launch_bounds__(kBlock) void eb_pool_kernel(FwdArgs a) {
+  const int32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int32_t g = (int32_t)blockIdx.x * kWavesPerBlock + wave;
+  if (g >= a.num_bags) return;
+  const int32_t t = g / a.batch;
+  const int32_t b = g - t * a.batch;
+  const TableMeta m = a.meta[t];
+
+  int64_t lo, hi;
+  if (a.idx64) {
+    lo = static_cast<const int64_t *>(a.offsets)[g];
+    hi = static_cast<const int64_t *>(a.offsets)[g + 1];
+  } else {
+    lo = static_cast<const int32_t *>(a.offsets)[g];
+    hi = static_cast<const int32_t *>(a.offsets)[g + 1];
+  }
+  // never read outside [0, N): clamp a broken partition and report it
+  bool bad = lo < 0 || hi < lo || hi > a.num_indices;
+  bad |= (g == 0 && lo != 0) || (g == a.num_bags - 1 && hi != a.num_indices);
+  if (bad) {
+    if ((threadIdx.x & (kWave - 1)) == 0) atomicOr(a.err, kErrOffsets);
+    lo = lo < 0 ? 0 : (lo > a.num_indices ? a.num_indices : lo);
+    hi = hi < lo ? lo : (hi > a.num_indices ? a.num_indices : hi);
+  }
+  float *dst = a.out + (int64_t)b * a.out_ld + m.out_col;
+
+  switch (m.kind) {
+    EB_KIND(kF32, 0) EB_KIND(kF32, 1) EB_KIND(kF32, 2) EB_KIND(kF32, 3)
+    EB_KIND(kF32, 4) EB_KIND(kF32, 5) EB_KIND(kF32, 6)
+    EB_KIND(kF16, 0) EB_KIND(kF16, 1) EB_KIND(kF16, 2) EB_KIND(kF16, 3)
+    EB_KIND(kF16, 4) EB_KIND(kF16, 5) EB_KIND(kF16, 6)
+    EB_KIND(kU8, 0) EB_KIND(kU8, 1) EB_KIND(kU8, 2) EB_KIND(kU8, 3)
+    EB_KIND(kU8, 4) EB_KIND(kU8, 5) EB_KIND(kU8, 6)
+    default:
+      break;
+  }
+}
+
+#undef EB_KIND
+
+int log2_lanes_per_row(int code_bytes) {
+  int slices = (code_bytes + 15) / 16;
+  int l = 0;
+  while ((1 << l) < slices && l < 6) ++l;
+  return l;
+}
+
+}  // namespace
+
+struct eb_tables {
+  int device;
+  hipStream_t stream;
+  int32_t num_tables;
+  int32_t checked;
+  int64_t sum_dim;
+  TableMeta *d_meta;  // device: num_tables descriptors followed by the error word
+  int *d_err;
+};
+
+extern "C" {
+
+const char *eb_status_string(eb_status s) {
+  switch (s) {
+    case EB_OK: return "ok";
+    case EB_ERR_INVALID_ARG: return "invalid argument";
+    case EB_ERR_DTYPE: return "unknown or mismatched data type";
+    case EB_ERR_SHAPE: return "sizes do not fit together";
+    case EB_ERR_UNSUPPORTED: return "unsupported dimension or alignment";
+    case EB_ERR_INDEX_OOB: return "index outside its table (checked mode)";
+    case EB_ERR_OFFSETS: return "offsets are not a partition of the indices (checked mode)";
+    case EB_ERR_OOM: return "device allocation failed";
+    case EB_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void *hip_stream, eb_tables **out) {
+  if (!out) return EB_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!descs || num_tables < 1 || num_tables > 65535) return EB_ERR_INVALID_ARG;
+
+  TableMeta *meta = static_cast<TableMeta *>(calloc((size_t)num_tables, sizeof(TableMeta)));
+  if (!meta) return EB_ERR_OOM;
+  int64_t col = 0;
+  eb_status st = EB_OK;
+  for (int32_t t = 0; t < num_tables && st == EB_OK; ++t) {
+    const eb_table_desc &d = descs[t];
+    int esize, align, dim_mult;
+    if (d.dtype == EB_F32) {
+      esize = 4; align = 16; dim_mult = 4;
+    } else if (d.dtype == EB_F16) {
+      esize = 2; align = 16; dim_mult = 8;
+    } else if (d.dtype == EB_INT8_ROWWISE) {
+      esize = 1; align = 4; dim_mult = 16;
+    } else {
+      st = EB_ERR_DTYPE;
+      break;
+    }
+    const int64_t code_bytes = (int64_t)d.dim * esize;
+    const int64_t row_bytes = code_bytes + (d.dtype == EB_INT8_ROWWISE ? 4 : 0);
+    if (!d.data || d.num_rows < 1 || d.num_rows > INT32_MAX || d.dim < 1 || d.dim > kMaxDim ||
+        d.row_stride_bytes < row_bytes) {
+      st = EB_ERR_INVALID_ARG;
+    } else if (d.dim % dim_mult != 0 || d.row_stride_bytes % align != 0 ||
+               reinterpret_cast<uintptr_t>(d.data) % align != 0 || d.row_stride_bytes > INT32_MAX) {
+      st = EB_ERR_UNSUPPORTED;
+    } else {
+      TableMeta &m = meta[t];
+      m.data = static_cast<const unsigned char *>(d.data);
+      m.row_stride = (uint32_t)d.row_stride_bytes;
+      m.num_rows = (int32_t)d.num_rows;
+      m.dim = d.dim;
+      m.code_bytes = (int32_t)code_bytes;
+      m.out_col = (int32_t)col;
+      m.kind = d.dtype * 8 + log2_lanes_per_row((int)code_bytes);
+      m.passes = (int32_t)((code_bytes + kPassBytes - 1) / kPassBytes);
+      col += d.dim;
+      if (col > INT32_MAX) st = EB_ERR_SHAPE;
+    }
+  }
+  if (st != EB_OK) {
+    free(meta);
+    return st;
+  }
+
+  eb_tables *h = static_cast<eb_tables *>(calloc(1, sizeof(eb_tables)));
+  if (!h) {
+    free(meta);
+    return EB_ERR_OOM;
+  }
+  if (hipGetDevice(&h->device) != hipSuccess) {
+    free(meta);
+    free(h);
+    return EB_ERR_HIP;
+  }
+  h->stream = static_cast<hipStream_t>(hip_stream);
+  h->num_tables = num_tables;
+  h->sum_dim = col;
+  const char *chk = getenv("EB_CHECK");
+  h->checked = (chk && chk[0] == '1') ? 1 : 0;
+
+  const size_t meta_bytes = sizeof(TableMeta) * (size_t)num_tables;
+  void *dev = nullptr;
+  hipError_t e = hipMalloc(&dev, meta_bytes + 256);
+  if (e != hipSuccess) {
+    free(meta);
+    free(h);
+    return e == hipErrorOutOfMemory ? EB_ERR_OOM : EB_ERR_HIP;
+  }
+  h->d_meta = static_cast<TableMeta *>(dev);
+  // the error word sits in the 256 bytes after the descriptors
+  h->d_err = reinterpret_cast<int *>(static_cast<char *>(dev) + meta_bytes);
+  e = hipMemcpy(h->d_meta, meta, meta_bytes, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemset(h->d_err, 0, sizeof(int));
+  free(meta);
+  if (e != hipSuccess) {
+    (void)hipFree(dev);
+    free(h);
+    return EB_ERR_HIP;
+  }
+  *out = h;
+  return EB_OK;
+}
+
+eb_status eb_forward(const eb_tables *h, eb_tensor indices, eb_tensor offsets, eb_tensor per_sample_weights,
+                     eb_pooling pooling, eb_tensor out) {
+  if (!h) return EB_ERR_INVALID_ARG;
+  if (indices.elem_type != EB_I32 && indices.elem_type != EB_I64) return EB_ERR_DTYPE;
+  if (offsets.elem_type != indices.elem_type) return EB_ERR_DTYPE;
+  if (out.elem_type != EB_T_F32) return EB_ERR_DTYPE;
+  if (pooling != EB_POOL_SUM && pooling != EB_POOL_MEAN) return EB_ERR_INVALID_ARG;
+  if (!offsets.data || !out.data) return EB_ERR_INVALID_ARG;
+  if (indices.numel < 0 || (indices.numel > 0 && !indices.data)) return EB_ERR_INVALID_ARG;
+  const bool weighted = per_sample_weights.data != nullptr;
+  if (weighted) {
+    if (per_sample_weights.elem_type != EB_T_F32) return EB_ERR_DTYPE;
+    if (pooling == EB_POOL_MEAN) return EB_ERR_INVALID_ARG;
+    if (per_sample_weights.numel != indices.numel) return EB_ERR_SHAPE;
+  }
+  if (offsets.numel < 2 || (offsets.numel - 1) % h->num_tables != 0) return EB_ERR_SHAPE;
+  const int64_t num_bags = offsets.numel - 1;
+  const int64_t batch = num_bags / h->num_tables;
+  if (num_bags > INT32_MAX) return EB_ERR_SHAPE;
+  if (out.numel != batch * h->sum_dim) return EB_ERR_SHAPE;
+  const size_t isz = indices.elem_type == EB_I64 ? 8 : 4;
+  if (reinterpret_cast<uintptr_t>(out.data) % 16 != 0 || reinterpret_cast<uintptr_t>(offsets.data) % isz != 0 ||
+      reinterpret_cast<uintptr_t>(indices.data) % isz != 0 ||
+      (weighted && reinterpret_cast<uintptr_t>(per_sample_weights.data) % 4 != 0))
+    return EB_ERR_UNSUPPORTED;
+
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return EB_ERR_HIP;
+  if (cur != h->device && hipSetDevice(h->device) != hipSuccess) return EB_ERR_HIP;
+
+  FwdArgs a;
+  a.meta = h->d_meta;
+  a.indices = indices.data;
+  a.offsets = offsets.data;
+  a.weights = static_cast<const float *>(per_sample_weights.data);
+  a.out = static_cast<float *>(const_cast<void *>(out.data));
+  a.err = h->d_err;
+  a.num_indices = indices.numel;
+  a.out_ld = h->sum_dim;
+  a.num_bags = (int32_t)num_bags;
+  a.batch = (int32_t)batch;
+  a.idx64 = indices.elem_type == EB_I64;
+  a.mean = pooling == EB_POOL_MEAN;
+
+  eb_status st = EB_OK;
+  hipError_t e = hipSuccess;
+  if (h->checked) e = hipMemsetAsync(h->d_err, 0, sizeof(int), h->stream);
+  if (e == hipSuccess) {
+    const unsigned grid = (unsigned)((num_bags + kWavesPerBlock - 1) / kWavesPerBlock);
+    if (weighted)
+      hipLaunchKernelGGL(eb_pool_kernel<true>, dim3(grid), dim3(kBlock), 0, h->stream, a);
+    else
+      hipLaunchKernelGGL(eb_pool_kernel<false>, dim3(grid), dim3(kBlock), 0, h->stream, a);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess && h->checked) {
+    int herr = 0;
+    e = hipMemcpyAsync(&herr, h->d_err, sizeof(int), hipMemcpyDeviceToHost, h->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
+    if (e == hipSuccess && (herr & kErrOffsets)) st = EB_ERR_OFFSETS;
+    else if (e == hipSuccess && (herr & kErrIndex)) st = EB_ERR_INDEX_OOB;
+  }
+  if (e != hipSuccess) st = EB_ERR_HIP;
+  if (cur != h->device) (void)hipSetDevice(cur);
+  return st;
+}
+
+eb_status eb_destroy(eb_tables *h) {
+  if (!h) return EB_OK;
+  int cur = -1;
+  eb_status st = EB_OK;
+  if (hipGetDevice(&cur) != hipSuccess) st = EB_ERR_HIP;
+  if (st == EB_OK && cur != h->device && hipSetDevice(h->device) != hipSuccess) st = EB_ERR_HIP;
+  if (st == EB_OK && hipStreamSynchronize(h->stream) != hipSuccess) st = EB_ERR_HIP;
+  if (hipFree(h->d_meta) != hipSuccess) st = EB_ERR_HIP;
+  if (cur >= 0 && cur != h->device) (void)hipSetDevice(cur);
+  free(h);
+  return st;
+}
+
+}  // extern "C"

@@ -1,0 +1,169 @@
+"""Python binding of libeb — argument marshalling only.
+
+Each function has the name of the C entry point it calls (include/eb.h) and
+turns torch tensors into the plain pointers and sizes the C ABI takes.  Every
+step of the pooled lookup runs in libeb's HIP kernels; torch only owns the
+device memory and the stream.  If libeb.so has not been built this module
+raises on first use: there is no other implementation to fall back to.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libeb.so")
+
+# eb_status
+EB_OK = 0
+EB_ERR_INVALID_ARG = -1
+EB_ERR_DTYPE = -2
+EB_ERR_SHAPE = -3
+EB_ERR_UNSUPPORTED = -4
+EB_ERR_INDEX_OOB = -5
+EB_ERR_OFFSETS = -6
+EB_ERR_OOM = -7
+EB_ERR_HIP = -8
+# eb_table_dtype
+EB_F32, EB_F16, EB_INT8_ROWWISE = 0, 1, 2
+# eb_elem_type
+EB_I32, EB_I64, EB_T_F32 = 0, 1, 2
+# eb_pooling
+EB_POOL_SUM, EB_POOL_MEAN = 0, 1
+
+TABLE_DTYPES = {"f32": EB_F32, "f16": EB_F16, "int8_rowwise": EB_INT8_ROWWISE}
+POOLING = {"sum": EB_POOL_SUM, "mean": EB_POOL_MEAN}
+EXPORTED = ("eb_create_tables", "eb_forward", "eb_destroy", "eb_status_string")
+
+
+class EBError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {eb_status_string(status)} ({status})")
+        self.status = status
+
+
+class eb_table_desc(ctypes.Structure):
+    _fields_ = [
+        ("data", ctypes.c_void_p),
+        ("num_rows", ctypes.c_int64),
+        ("dim", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("row_stride_bytes", ctypes.c_int64),
+    ]
+
+
+class eb_tensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("numel", ctypes.c_int64), ("elem_type", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libeb.so (once).  Raises if it is missing: build it first."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise RuntimeError(f"libeb.so not found at {path}; build it with "
+                               "`python -c 'import __graft_entry__ as g; g.build()'`")
+        lib = ctypes.CDLL(path)
+        lib.eb_create_tables.restype = ctypes.c_int
+        lib.eb_create_tables.argtypes = [ctypes.POINTER(eb_table_desc), ctypes.c_int32, ctypes.c_void_p,
+                                         ctypes.POINTER(ctypes.c_void_p)]
+        lib.eb_forward.restype = ctypes.c_int
+        lib.eb_forward.argtypes = [ctypes.c_void_p, eb_tensor, eb_tensor, eb_tensor, ctypes.c_int, eb_tensor]
+        lib.eb_destroy.restype = ctypes.c_int
+        lib.eb_destroy.argtypes = [ctypes.c_void_p]
+        lib.eb_status_string.restype = ctypes.c_char_p
+        lib.eb_status_string.argtypes = [ctypes.c_int]
+        _lib = lib
+    return _lib
+
+
+def eb_status_string(status: int) -> str:
+    return load_library().eb_status_string(int(status)).decode()
+
+
+class EbTables:
+    """Handle returned by eb_create_tables; keeps the table tensors alive."""
+
+    def __init__(self, ptr: int, tables, stream, sum_dim: int):
+        self.ptr = ptr
+        self.tables = list(tables)
+        self.stream = stream
+        self.sum_dim = sum_dim
+
+    @property
+    def num_tables(self) -> int:
+        return len(self.tables)
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        eb_destroy(self)
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        return None
+    if isinstance(stream, int):
+        return stream or None
+    return stream.cuda_stream or None
+
+
+def eb_create_tables(tables: Sequence, stream=None) -> EbTables:
+    """tables: objects with .rows (device tensor, first axis = row), .dim and
+    .dtype ("f32" | "f16" | "int8_rowwise"), or (rows, dim, dtype) tuples.
+    stream: torch.cuda.Stream, raw hipStream_t as int, or None (null stream)."""
+    lib = load_library()
+    norm = []
+    for t in tables:
+        rows, dim, dtype = (t.rows, t.dim, t.dtype) if hasattr(t, "rows") else t
+        norm.append((rows, int(dim), dtype))
+    descs = (eb_table_desc * len(norm))()
+    for i, (rows, dim, dtype) in enumerate(norm):
+        descs[i].data = rows.data_ptr() if rows.numel() else None
+        descs[i].num_rows = rows.shape[0]
+        descs[i].dim = dim
+        descs[i].dtype = TABLE_DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
+        descs[i].row_stride_bytes = rows.stride(0) * rows.element_size()
+    out = ctypes.c_void_p()
+    st = lib.eb_create_tables(descs, len(norm), _stream_handle(stream), ctypes.byref(out))
+    if st != EB_OK:
+        raise EBError(st, "eb_create_tables")
+    return EbTables(out.value, [r for r, _, _ in norm], stream, sum(d for _, d, _ in norm))
+
+
+_ELEM = {torch.int32: EB_I32, torch.int64: EB_I64, torch.float32: EB_T_F32}
+
+
+def _as_tensor(t: Optional[torch.Tensor]) -> eb_tensor:
+    if t is None:
+        return eb_tensor(None, 0, EB_T_F32)
+    if not t.is_contiguous():
+        raise ValueError("eb tensors must be contiguous")
+    return eb_tensor(t.data_ptr() if t.numel() else None, t.numel(), _ELEM.get(t.dtype, 99))
+
+
+def eb_forward(tables: EbTables, indices: torch.Tensor, offsets: torch.Tensor,
+               per_sample_weights: Optional[torch.Tensor], pooling, out: torch.Tensor) -> torch.Tensor:
+    """Enqueue the pooled lookup on the handle's stream; returns `out`."""
+    lib = load_library()
+    mode = POOLING[pooling] if isinstance(pooling, str) else int(pooling)
+    st = lib.eb_forward(tables.ptr, _as_tensor(indices), _as_tensor(offsets), _as_tensor(per_sample_weights),
+                        mode, _as_tensor(out))
+    if st != EB_OK:
+        raise EBError(st, "eb_forward")
+    return out
+
+
+def eb_destroy(tables: EbTables) -> None:
+    if tables.ptr:
+        st = load_library().eb_destroy(tables.ptr)
+        tables.ptr = None
+        if st != EB_OK:
+            raise EBError(st, "eb_destroy")

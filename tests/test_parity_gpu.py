@@ -1,0 +1,349 @@
+"""GPU parity: libeb's HIP path against the CPU oracle, through the C ABI.
+
+Bar (per output element of a bag with L lookups, oracle value o, GPU value g,
+and the oracle's error scale s = sum_i |w_i x_i| (divided by L for mean)):
+  * L <= 1: g and o have the same bits (a gather, or an empty bag = +0.0);
+  * otherwise |g - o| <= rtol * s with rtol = 1e-5 for fp32 tables and 2e-3
+    for fp16 / int8 row-wise tables;
+  * and, tighter, the a-priori bound of fp32 summation in any order,
+    |g - o| <= (L + 3) * 2^-24 * s (L - 1 additions, a rounded weight product
+    or dequantised value folded into an fma, the mean's division, and the
+    oracle's own final rounding).
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from conftest import oracle_forward, ulp_distance
+from oracle import OracleTable, ebo_forward
+from paper_2609_30656_amd import eb
+from paper_2609_30656_amd.workload import Table, make_workload
+
+pytestmark = pytest.mark.gpu
+
+RTOL = {"f32": 1e-5, "f16": 2e-3, "int8_rowwise": 2e-3}
+U = 2.0 ** -24
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    eb.load_library()
+    d = torch.device("cuda:0")
+    torch.cuda.set_device(d)
+    return d
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def run_gpu(w, stream=None, prefill=float("nan")):
+    out = torch.full((w.batch, w.sum_dim), prefill, dtype=torch.float32, device=w.indices.device)
+    with eb.eb_create_tables(w.tables, stream) as h:
+        eb.eb_forward(h, w.indices, w.offsets, w.weights, w.pooling, out)
+        torch.cuda.synchronize()
+    return out
+
+
+def check(got, ref, asum, L, rtol, label):
+    """got/ref fp32, asum fp64, L int (same shape)."""
+    got = np.asarray(got, np.float32)
+    err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
+    assert not np.isnan(got).any(), f"{label}: NaN in output (an element was not written)"
+    short = L <= 1
+    if short.any():
+        same = got.view(np.uint32)[short] == ref.view(np.uint32)[short]
+        assert same.all(), f"{label}: {np.count_nonzero(~same)} one-row/empty outputs not bit-exact"
+    long_ = ~short
+    if long_.any():
+        lim = rtol * asum[long_]
+        bad = err[long_] > lim
+        assert not bad.any(), (f"{label}: {bad.sum()} outputs beyond rtol {rtol}; worst ratio "
+                               f"{np.max(err[long_] / np.maximum(lim, 1e-300)):.3g}")
+        bound = (L[long_] + 3) * U * asum[long_]
+        over = err[long_] > bound
+        assert not over.any(), f"{label}: {over.sum()} outputs beyond the summation error bound"
+
+
+def per_element_lengths(w, bags=None):
+    lens = w.lengths.cpu().numpy().reshape(w.num_tables, w.batch)
+    if bags is None:
+        return np.concatenate([np.repeat(lens[t][:, None], tb.dim, axis=1) for t, tb in enumerate(w.tables)], 1)
+    return lens.reshape(-1)[bags][:, None]
+
+
+def full_check(w, label, stream=None):
+    got = run_gpu(w, stream).cpu().numpy()
+    ref, asum = oracle_forward(w)
+    rtol = max(RTOL[t.dtype] for t in w.tables)
+    check(got, ref, asum, per_element_lengths(w), rtol, label)
+    return got
+
+
+# ----------------------------------------------------------------------------
+# every config at sizes the oracle finishes in seconds (several tiles, ragged tails)
+
+REDUCED = {
+    "c1": {},
+    "c2": dict(rows_cap=20000, batch=256),
+    "c3a": dict(rows_cap=50000, batch=256),
+    "c3b": dict(rows_cap=50000, batch=256),
+    "c4": dict(rows_cap=20000, batch=96),
+    "c5": dict(rows_cap=20000, batch=128),
+}
+
+
+@pytest.mark.parametrize("name", list(REDUCED))
+def test_reduced_configs_elementwise(dev, name):
+    say(f"[parity] reduced {name} {REDUCED[name]}")
+    w = make_workload(name, dev, **REDUCED[name])
+    full_check(w, f"reduced {name}")
+
+
+@pytest.mark.parametrize("name", ["c2", "c3b", "c4", "c5"])
+def test_int32_indices(dev, name):
+    say(f"[parity] int32 indices {name}")
+    w = make_workload(name, dev, index_dtype=torch.int32, **REDUCED[name])
+    full_check(w, f"int32 {name}")
+
+
+@pytest.mark.parametrize("name", ["c2", "c5"])
+def test_uniform_index_control(dev, name):
+    say(f"[parity] uniform indices {name}")
+    w = make_workload(name, dev, index_law="uniform", **REDUCED[name])
+    full_check(w, f"uniform {name}")
+
+
+# ----------------------------------------------------------------------------
+# full sizes, in the launch configuration the benchmark times
+
+def test_full_c1(dev):
+    say("[parity] full c1")
+    full_check(make_workload("c1", dev), "full c1")
+
+
+def test_full_c2_every_element(dev):
+    say("[parity] full c2 (all 53,248 bags)")
+    w = make_workload("c2", dev)
+    full_check(w, "full c2")
+
+
+def _sampled(w, tables_to_check, n_random=400, seed=0):
+    """Bags of the given tables: random ones plus the longest, the empty and
+    one-row ones, and each table's first and last bag."""
+    rng = np.random.default_rng(seed)
+    lens = w.lengths.cpu().numpy()
+    B = w.batch
+    picks = []
+    for t in tables_to_check:
+        g = np.arange(t * B, (t + 1) * B)
+        L = lens[g]
+        picks += [g[0], g[-1], g[np.argmax(L)]]
+        picks += list(rng.choice(g, size=min(n_random, B), replace=False))
+        for cond in (L == 0, L == 1, L >= 100):
+            sel = g[cond]
+            if sel.size:
+                picks += list(rng.choice(sel, size=min(20, sel.size), replace=False))
+    return np.unique(np.array(picks, dtype=np.int64))
+
+
+@pytest.mark.parametrize("name", ["c3a", "c3b", "c4", "c5"])
+def test_full_size_sampled(dev, name):
+    say(f"[parity] full {name}: generating")
+    w = make_workload(name, dev)
+    T = w.num_tables
+    check_tables = sorted({0, T // 2, T - 1})
+    say(f"[parity] full {name}: {w.num_indices} lookups, {w.num_bags} bags; forward")
+    got = run_gpu(w)
+    assert not torch.isnan(got).any()
+    # empty bags are +0.0 everywhere, at full size
+    lens = w.lengths.view(T, w.batch)
+    col = 0
+    for t, tb in enumerate(w.tables):
+        empty = lens[t] == 0
+        if empty.any():
+            z = got[empty, col:col + tb.dim]
+            assert torch.equal(z.view(torch.int32), torch.zeros_like(z).view(torch.int32))
+        col += tb.dim
+    bags = _sampled(w, check_tables)
+    say(f"[parity] full {name}: oracle on {bags.size} sampled bags of tables {check_tables}")
+    tabs = [OracleTable(tb.rows.cpu().numpy() if t in check_tables else None, tb.dim, tb.dtype, tb.num_rows)
+            for t, tb in enumerate(w.tables)]
+    ref, asum = oracle_forward(w, tables=tabs, bags=bags)
+    g_host = got.cpu().numpy()
+    doff = np.concatenate([[0], np.cumsum([tb.dim for tb in w.tables])])
+    B = w.batch
+    L = per_element_lengths(w, bags)
+    for k, g in enumerate(bags):
+        t, b = divmod(int(g), B)
+        D = w.tables[t].dim
+        check(g_host[b, doff[t]:doff[t] + D], ref[k, :D], asum[k, :D], np.full(D, L[k, 0]),
+              RTOL[w.tables[t].dtype], f"full {name} bag {g}")
+
+
+# ----------------------------------------------------------------------------
+# shapes and edge cases
+
+
+def _table(dev, dtype, R, D, stride=None, seed=0):
+    g = torch.Generator(device=dev)
+    g.manual_seed(1000 + seed)
+    if dtype == "f32":
+        width = D if stride is None else stride // 4
+        rows = torch.rand((R, width), generator=g, device=dev) * 2 - 1
+    elif dtype == "f16":
+        width = D if stride is None else stride // 2
+        rows = (torch.randn((R, width), generator=g, device=dev) * 0.01).half()
+    else:
+        width = D + 4 if stride is None else stride
+        rows = torch.randint(0, 256, (R, width), generator=g, device=dev, dtype=torch.uint8)
+        sc = (torch.rand(R, generator=g, device=dev) * 3e-4 + 1e-4).half().view(torch.uint8).view(R, 2)
+        bi = (torch.rand(R, generator=g, device=dev) * 0.04 - 0.06).half().view(torch.uint8).view(R, 2)
+        rows[:, D:D + 2] = sc
+        rows[:, D + 2:D + 4] = bi
+    return Table(rows, D, dtype)
+
+
+def _custom(dev, tables, lens_per_table, weighted=False, pooling="sum", index_dtype=torch.int64, seed=0):
+    from paper_2609_30656_amd.workload import Workload
+
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    B = len(lens_per_table[0])
+    lengths = torch.tensor(np.concatenate(lens_per_table), dtype=torch.int64)
+    offsets = torch.zeros(lengths.numel() + 1, dtype=torch.int64)
+    torch.cumsum(lengths, 0, out=offsets[1:])
+    idx = []
+    for t, tb in enumerate(tables):
+        n = int(sum(lens_per_table[t]))
+        idx.append(torch.randint(0, tb.num_rows, (n,), generator=g))
+    indices = torch.cat(idx) if idx else torch.empty(0, dtype=torch.int64)
+    weights = torch.rand(indices.numel(), generator=g) if weighted else None
+    return Workload("custom", tables, B, indices.to(index_dtype).to(dev), offsets.to(index_dtype).to(dev),
+                    None if weights is None else weights.to(dev), pooling, lengths.to(dev))
+
+
+WIDTHS = [("f32", 4), ("f32", 12), ("f32", 20), ("f32", 100), ("f32", 260), ("f32", 1024), ("f32", 1028),
+          ("f16", 8), ("f16", 24), ("f16", 40), ("f16", 136), ("f16", 520), ("f16", 2048),
+          ("int8_rowwise", 16), ("int8_rowwise", 48), ("int8_rowwise", 272), ("int8_rowwise", 1024),
+          ("int8_rowwise", 2064)]
+
+
+@pytest.mark.parametrize("mode", ["sum", "mean", "weighted"])
+def test_every_width_in_one_launch(dev, mode):
+    say(f"[parity] widths {mode}")
+    rng = np.random.default_rng(5)
+    tables = [_table(dev, dt, 300 + 7 * i, D, seed=i) for i, (dt, D) in enumerate(WIDTHS)]
+    B = 37
+    lens = [rng.integers(0, 140, B) for _ in tables]
+    for l in lens:
+        l[0], l[1], l[2] = 0, 1, 129  # empty, one row, just over two index chunks
+    w = _custom(dev, tables, lens, weighted=(mode == "weighted"), pooling="mean" if mode == "mean" else "sum")
+    full_check(w, f"widths {mode}")
+
+
+def test_padded_row_strides(dev):
+    say("[parity] padded strides")
+    tables = [_table(dev, "f32", 500, 64, stride=512), _table(dev, "f16", 500, 64, stride=256),
+              _table(dev, "int8_rowwise", 500, 128, stride=144), _table(dev, "int8_rowwise", 500, 32, stride=40)]
+    rng = np.random.default_rng(6)
+    w = _custom(dev, tables, [rng.integers(0, 50, 64) for _ in tables], weighted=True)
+    full_check(w, "padded strides")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "int8_rowwise"])
+def test_long_bags(dev, dtype):
+    say(f"[parity] long bags {dtype}")
+    D = {"f32": 64, "f16": 128, "int8_rowwise": 128}[dtype]
+    tables = [_table(dev, dtype, 5000, D)]
+    w = _custom(dev, tables, [np.array([5000, 0, 1, 63, 64, 65, 1000, 4097])])
+    full_check(w, f"long {dtype}")
+
+
+def test_no_indices_at_all(dev):
+    say("[parity] N = 0")
+    tables = [_table(dev, "f32", 10, 16), _table(dev, "int8_rowwise", 10, 32)]
+    w = _custom(dev, tables, [np.zeros(5, np.int64), np.zeros(5, np.int64)])
+    got = run_gpu(w)
+    assert torch.equal(got.view(torch.int32), torch.zeros_like(got).view(torch.int32))
+
+
+def test_one_bag_one_table(dev):
+    say("[parity] B = 1, T = 1")
+    w = _custom(dev, [_table(dev, "f16", 50, 32)], [np.array([7])])
+    full_check(w, "B=1")
+
+
+def test_deterministic_bits(dev):
+    say("[parity] determinism")
+    w = make_workload("c3b", dev, **REDUCED["c3b"])
+    a = run_gpu(w)
+    b = run_gpu(w)
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+def test_side_stream(dev):
+    say("[parity] side stream")
+    w = make_workload("c5", dev, **REDUCED["c5"])
+    s = torch.cuda.Stream(device=dev)
+    full_check(w, "side stream", stream=s)
+
+
+# ----------------------------------------------------------------------------
+# argument errors through the ABI (host-side: nothing is enqueued)
+
+
+def test_forward_argument_errors(dev):
+    say("[parity] argument errors")
+    w = _custom(dev, [_table(dev, "f32", 10, 16), _table(dev, "f16", 10, 16)], [np.array([1, 2]), np.array([0, 3])])
+    out = torch.full((2, 32), 7.0, device=dev)
+    with eb.eb_create_tables(w.tables) as h:
+        def expect(status, **kw):
+            args = dict(indices=w.indices, offsets=w.offsets, per_sample_weights=None, pooling="sum", out=out)
+            args.update(kw)
+            with pytest.raises(eb.EBError) as e:
+                eb.eb_forward(h, **args)
+            assert e.value.status == status, kw.keys()
+
+        expect(eb.EB_ERR_DTYPE, offsets=w.offsets.int())
+        expect(eb.EB_ERR_DTYPE, indices=w.indices.float(), offsets=w.offsets.float())
+        expect(eb.EB_ERR_DTYPE, out=out.double())
+        expect(eb.EB_ERR_SHAPE, offsets=w.offsets[:-1].contiguous())
+        expect(eb.EB_ERR_SHAPE, out=out[:1].contiguous())
+        expect(eb.EB_ERR_SHAPE, per_sample_weights=torch.ones(w.num_indices + 1, device=dev))
+        expect(eb.EB_ERR_INVALID_ARG, per_sample_weights=torch.ones(w.num_indices, device=dev), pooling="mean")
+        expect(eb.EB_ERR_INVALID_ARG, pooling=5)
+        expect(eb.EB_ERR_UNSUPPORTED, out=torch.empty(2 * 32 + 1, device=dev)[1:])
+        torch.cuda.synchronize()
+        assert torch.all(out == 7.0)  # nothing was written
+
+
+def test_checked_mode_reports_bad_data(dev, monkeypatch):
+    say("[parity] checked mode")
+    monkeypatch.setenv("EB_CHECK", "1")
+    tb = _table(dev, "f32", 10, 16)
+    out = torch.empty((3, 16), device=dev)
+    with eb.eb_create_tables([tb]) as h:
+        ok_idx = torch.tensor([1, 2, 3, 4], device=dev)
+        off = torch.tensor([0, 2, 2, 4], device=dev)
+        eb.eb_forward(h, ok_idx, off, None, "sum", out)  # valid: no error
+        for bad_idx in ([1, 10, 3, 4], [1, -1, 3, 4]):  # the kernel skips such rows, never reads them
+            with pytest.raises(eb.EBError) as e:
+                eb.eb_forward(h, torch.tensor(bad_idx, device=dev), off, None, "sum", out)
+            assert e.value.status == eb.EB_ERR_INDEX_OOB
+        for bad_off in ([1, 2, 2, 4], [0, 3, 2, 4], [0, 2, 2, 3], [0, 2, 2, 9]):  # clamped in the kernel
+            with pytest.raises(eb.EBError) as e:
+                eb.eb_forward(h, ok_idx, torch.tensor(bad_off, device=dev), None, "sum", out)
+            assert e.value.status == eb.EB_ERR_OFFSETS
+        eb.eb_forward(h, ok_idx, off, None, "sum", out)  # the error word was cleared
+    ref = ebo_forward([OracleTable(tb.rows.cpu().numpy(), 16, "f32")], np.array([1, 2, 3, 4]), np.array([0, 2, 2, 4]))
+    assert ulp_distance(out.cpu().numpy(), ref).max() <= 1
+
+
+def test_native_library_is_the_one_loaded(dev):
+    lib = eb.load_library()
+    assert os.path.samefile(lib._name, eb.LIB_PATH)
