@@ -49,6 +49,11 @@
  * kernel and returns EB_ERR_INDEX_OOB or EB_ERR_OFFSETS if the kernel met
  * such data (offsets[0] != 0 and offsets[T*B] != numel(indices) included).
  * Checked mode is for debugging; it blocks the calling thread.
+ *
+ * Tuning.  EB_BAGS_PER_WAVE=k (1..32), read when a handle is created, fixes
+ * how many consecutive bags of one table a wavefront pools; without it the
+ * count is chosen per call from the number of bags.  Results do not depend
+ * on it.
  */
 #ifndef EB_H_
 #define EB_H_

@@ -37,6 +37,11 @@ constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr int kPassBytes = kWave * 16;  // one wave-wide 16-byte load covers 1 KiB
 constexpr uint32_t kBadRow = 0xFFFFFFFFu;
 constexpr int kMaxDim = 8192;
+// A wavefront pools up to this many consecutive bags (their offsets are read
+// with one vector load, one per lane, so at most 63).
+constexpr int kMaxBagsPerWave = 32;
+// Wavefronts resident on a full MI355X (256 CUs x 4 SIMDs x 8 waves).
+constexpr int64_t kResidentWaves = 256 * 4 * 8;
 
 // error bits raised by the kernel, reported in checked mode
 constexpr int kErrIndex = 1;
@@ -70,6 +75,9 @@ struct FwdArgs {
   int32_t batch;
   int32_t idx64;
   int32_t mean;
+  int32_t bags_per_wave;     // consecutive bags of one table per wavefront
+  int32_t groups_per_table;  // ceil(batch / bags_per_wave)
+  int32_t num_waves;         // num_tables * groups_per_table
 };
 
 // Table rows are plain device memory: address them in the global address
@@ -137,136 +145,303 @@ __device__ __forceinline__ u32x4 load_slice(gbyte *p) {
 }
 
 // Loads in flight per lane before the first is consumed: enough rows per
-// wave to cover HBM latency, within a 64-VGPR budget.
+// wave to cover HBM latency within the register budget.
 template <int RPL>
 struct Unroll {
   static constexpr int u = RPL >= 16 ? 2 : (RPL >= 8 ? 4 : 8);
 };
 
-// Pool one bag over the 1 KiB column window starting at byte col_base.
+// 64-bit value of lane `l` (wave-uniform l) of a per-lane value.
+__device__ __forceinline__ int64_t readlane64(int64_t v, int l) {
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, l);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)v >> 32), l);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// One chunk of up to 64 consecutive index positions of a bag, one per lane.
+struct Chunk {
+  uint32_t row;  // row number, or kBadRow (no row / outside the table)
+  float w;       // per-sample weight (weighted pooling only)
+  int n;         // positions in the chunk (wave-uniform)
+};
+
+template <bool W>
+__device__ __forceinline__ Chunk load_chunk(const TableMeta &m, const FwdArgs &a, int64_t c, int64_t hi) {
+  const int lane = threadIdx.x & (kWave - 1);
+  Chunk k;
+  k.n = (int)((hi - c) < kWave ? (hi - c) : kWave);
+  k.row = kBadRow;
+  k.w = 0.0f;
+  if (lane < k.n) {
+    // indices and weights are read once: stream them past the caches
+    const int64_t r = a.idx64 ? __builtin_nontemporal_load(static_cast<const int64_t *>(a.indices) + c + lane)
+                              : (int64_t)__builtin_nontemporal_load(static_cast<const int32_t *>(a.indices) + c + lane);
+    if (r >= 0 && r < m.num_rows) k.row = (uint32_t)r;
+    if constexpr (W) k.w = __builtin_nontemporal_load(a.weights + c + lane);
+  }
+  return k;
+}
+
+// Gather the rows of one chunk and add them into this lane's accumulators.
 template <int DT, int LPR, bool W>
-__device__ __forceinline__ void pool_bag(const TableMeta &m, const FwdArgs &a, int64_t lo, int64_t hi,
-                                         float *dst, int col_base) {
+__device__ __forceinline__ void gather_chunk(const TableMeta &m, const FwdArgs &a, const Chunk &k,
+                                             float (&acc)[Vals<DT>::n], int colb, bool colok) {
   constexpr int RPL = kWave / LPR;
-  constexpr int V = Vals<DT>::n;
   constexpr int U = Unroll<RPL>::u;
   const int lane = threadIdx.x & (kWave - 1);
   const int grp = lane / LPR;
+  if (__ballot(lane < k.n && k.row == kBadRow)) {
+    if (lane == 0) atomicOr(a.err, kErrIndex);
+  }
+  const int steps = (k.n + RPL - 1) / RPL;
+  for (int s = 0; s < steps; s += U) {
+    u32x4 v[U];
+    uint32_t sb[U];
+    float w[U];
+    bool ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int r = (s + u) * RPL + grp;
+      uint32_t row;
+      if constexpr (RPL == 1) {
+        row = __builtin_amdgcn_readlane(k.row, (s + u) & (kWave - 1));
+        if constexpr (W)
+          w[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(uint32_t, k.w),
+                                                                      (s + u) & (kWave - 1)));
+      } else {
+        row = (uint32_t)__shfl((int)k.row, r & (kWave - 1));
+        if constexpr (W) w[u] = __shfl(k.w, r & (kWave - 1));
+      }
+      ok[u] = (r < k.n) && (row != kBadRow) && colok;
+      v[u] = u32x4{0u, 0u, 0u, 0u};
+      sb[u] = 0u;
+      if (ok[u]) {
+        gbyte *p = (gbyte *)m.data + (uint64_t)row * m.row_stride;
+        v[u] = load_slice<DT>(p + colb);
+        if constexpr (DT == kU8) sb[u] = *reinterpret_cast<const EB_GLOBAL uint32_t *>(p + m.dim);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (ok[u]) accumulate<DT, W>(acc, v[u], sb[u], W ? w[u] : 1.0f);
+    }
+  }
+}
+
+__device__ __forceinline__ float dpp_row_ror(float x, int o) {
+  // rotate within each 16-lane row by o lanes (o is a compile-time constant)
+  const int xi = __builtin_bit_cast(int, x);
+  int r;
+  switch (o) {
+    case 1: r = __builtin_amdgcn_update_dpp(0, xi, 0x121, 0xf, 0xf, false); break;
+    case 2: r = __builtin_amdgcn_update_dpp(0, xi, 0x122, 0xf, 0xf, false); break;
+    case 4: r = __builtin_amdgcn_update_dpp(0, xi, 0x124, 0xf, 0xf, false); break;
+    default: r = __builtin_amdgcn_update_dpp(0, xi, 0x128, 0xf, 0xf, false); break;
+  }
+  return __builtin_bit_cast(float, r);
+}
+
+// Sum the RPL row groups' partial vectors (a reduce-scatter in a fixed order,
+// so results are deterministic).  On return, lane (row q of 16 lanes, slot
+// p) holds V / min(RPL, 4) consecutive values of the pooled slice of lane-slot
+// p % LPR, starting at value index first_value(); only lanes with
+// stores() == true write them.
+// (Elements of the swap builtins' two-lane result are read by value with
+// __uint_as_float: __builtin_bit_cast applied to such an element reads the
+// first element whatever the index.)
+template <int DT, int LPR>
+struct Reduce {
+  static constexpr int V = Vals<DT>::n;
+  static constexpr int KEEP = LPR >= 64 ? V : (LPR == 32 ? V / 2 : V / 4);
+
+  __device__ static __forceinline__ void run(float (&acc)[V]) {
+    if constexpr (LPR < 16) {
+      // combine the row groups that share a 16-lane row: all-reduce by rotation
+#pragma unroll
+      for (int o = LPR; o < 16; o <<= 1) {
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] += dpp_row_ror(acc[i], o);
+      }
+    }
+    if constexpr (LPR <= 16) {
+      // rows 0+1 and 2+3: pair value i with value i + V/2; rows 0,2 keep the
+      // first, rows 1,3 the second
+#pragma unroll
+      for (int i = 0; i < V / 2; ++i) {
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(acc[i]),
+                                                        __float_as_uint(acc[i + V / 2]), false, false);
+        acc[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+      }
+      // halves: pair value j with j + V/4 (of the V/2 left); the low half
+      // keeps the first, the high half the second
+#pragma unroll
+      for (int j = 0; j < V / 4; ++j) {
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[j]),
+                                                        __float_as_uint(acc[j + V / 4]), false, false);
+        acc[j] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+      }
+    } else if constexpr (LPR == 32) {
+#pragma unroll
+      for (int i = 0; i < V / 2; ++i) {
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i]),
+                                                        __float_as_uint(acc[i + V / 2]), false, false);
+        acc[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+      }
+    }
+  }
+
+  // index (within the lane-slot's V values) of the first value this lane holds
+  __device__ static __forceinline__ int first_value(int lane) {
+    if constexpr (LPR >= 64) {
+      return 0;
+    } else if constexpr (LPR == 32) {
+      return (lane >> 5) * (V / 2);
+    } else {
+      const int q = lane >> 4;  // 16-lane row
+      return ((q & 1) ? V / 2 : 0) + ((q & 2) ? V / 4 : 0);
+    }
+  }
+
+  __device__ static __forceinline__ bool stores(int lane) {
+    if constexpr (LPR >= 16) return true;
+    return (lane & 15) < LPR;
+  }
+};
+
+// Pool bags [g0, g0 + nb) of one table (batch rows b0 ..) over the 1 KiB column
+// window starting at byte col_base.  The bags' index positions are walked as
+// one stream of chunks of up to 64; the next chunk's indices are loaded before
+// the current chunk's rows are gathered, so each chunk costs one memory round
+// trip.
+template <int DT, int LPR, bool W>
+__device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, int32_t g0, int nb, int32_t b0,
+                                          int col_base) {
+  using R = Reduce<DT, LPR>;
+  constexpr int V = Vals<DT>::n;
+  const int lane = threadIdx.x & (kWave - 1);
   const int colb = col_base + (lane % LPR) * 16;
   const bool colok = colb < m.code_bytes;
+
+  // offsets[g0 .. g0 + nb]: one per lane
+  int64_t my_off = 0;
+  if (lane <= nb) {
+    my_off = a.idx64 ? static_cast<const int64_t *>(a.offsets)[g0 + lane]
+                     : (int64_t) static_cast<const int32_t *>(a.offsets)[g0 + lane];
+  }
+  // bag j's index range, clamped into [0, N) so nothing is read outside the
+  // index array whatever the offsets hold (a broken partition is reported)
+  auto bag_range = [&](int j, int64_t &lo, int64_t &hi) {
+    lo = readlane64(my_off, j);
+    hi = readlane64(my_off, j + 1);
+    const int32_t g = g0 + j;
+    bool bad = lo < 0 || hi < lo || hi > a.num_indices;
+    bad |= (g == 0 && lo != 0) || (g == a.num_bags - 1 && hi != a.num_indices);
+    if (bad) {
+      if (lane == 0) atomicOr(a.err, kErrOffsets);
+      lo = lo < 0 ? 0 : (lo > a.num_indices ? a.num_indices : lo);
+      hi = hi < lo ? lo : (hi > a.num_indices ? a.num_indices : hi);
+    }
+  };
 
   float acc[V];
 #pragma unroll
   for (int i = 0; i < V; ++i) acc[i] = 0.0f;
 
-  for (int64_t c = lo; c < hi; c += kWave) {
-    const int n = (int)((hi - c) < kWave ? (hi - c) : kWave);
-    uint32_t my_row = kBadRow;
-    float my_w = 0.0f;
-    if (lane < n) {
-      const int64_t r = a.idx64 ? static_cast<const int64_t *>(a.indices)[c + lane]
-                                : (int64_t) static_cast<const int32_t *>(a.indices)[c + lane];
-      if (r >= 0 && r < m.num_rows) my_row = (uint32_t)r;
-      if constexpr (W) my_w = a.weights[c + lane];
+  int j = 0;
+  int64_t blo, bhi;
+  bag_range(0, blo, bhi);
+  int64_t c = blo;
+  Chunk cur = load_chunk<W>(m, a, c, bhi);
+  while (true) {
+    const bool last = c + kWave >= bhi;
+    int jn = j;
+    int64_t cn = c + kWave, nlo = blo, nhi = bhi;
+    if (last) {
+      jn = j + 1;
+      if (jn < nb) {
+        bag_range(jn, nlo, nhi);
+        cn = nlo;
+      }
     }
-    if (__ballot(lane < n && my_row == kBadRow)) {
-      if (lane == 0) atomicOr(a.err, kErrIndex);
-    }
-    const int steps = (n + RPL - 1) / RPL;
-    for (int s = 0; s < steps; s += U) {
-      u32x4 v[U];
-      uint32_t sb[U];
-      float w[U];
-      bool ok[U];
+    const bool more = !last || jn < nb;
+    Chunk nxt;
+    if (more) nxt = load_chunk<W>(m, a, cn, nhi);
+
+    gather_chunk<DT, LPR, W>(m, a, cur, acc, colb, colok);
+
+    if (last) {
+      R::run(acc);
+      if (R::stores(lane) && colok) {
+        const int64_t L = bhi - blo;
+        const int f = R::first_value(lane);
+        float outv[R::KEEP];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int r = (s + u) * RPL + grp;
-        uint32_t row;
-        if constexpr (RPL == 1) {
-          row = __builtin_amdgcn_readlane(my_row, (s + u) & (kWave - 1));
-          if constexpr (W) w[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                       __builtin_bit_cast(uint32_t, my_w), (s + u) & (kWave - 1)));
+        for (int i = 0; i < R::KEEP; ++i) outv[i] = acc[i];
+        if (a.mean && L > 0) {
+          const float fl = (float)L;
+#pragma unroll
+          for (int i = 0; i < R::KEEP; ++i) outv[i] = outv[i] / fl;
+        }
+        float *dst = a.out + (int64_t)(b0 + j) * a.out_ld + m.out_col + colb / Vals<DT>::esize + f;
+        if constexpr (R::KEEP % 4 == 0) {
+#pragma unroll
+          for (int i = 0; i < R::KEEP; i += 4)
+            __builtin_nontemporal_store(f32x4{outv[i], outv[i + 1], outv[i + 2], outv[i + 3]},
+                                        reinterpret_cast<f32x4 *>(dst + i));
+        } else if constexpr (R::KEEP == 2) {
+          typedef float f32x2 __attribute__((ext_vector_type(2)));
+          __builtin_nontemporal_store(f32x2{outv[0], outv[1]}, reinterpret_cast<f32x2 *>(dst));
         } else {
-          row = (uint32_t)__shfl((int)my_row, r & (kWave - 1));
-          if constexpr (W) w[u] = __shfl(my_w, r & (kWave - 1));
-        }
-        ok[u] = (r < n) && (row != kBadRow) && colok;
-        v[u] = u32x4{0u, 0u, 0u, 0u};
-        sb[u] = 0u;
-        if (ok[u]) {
-          gbyte *p = (gbyte *)m.data + (uint64_t)row * m.row_stride;
-          v[u] = load_slice<DT>(p + colb);
-          if constexpr (DT == kU8) sb[u] = *reinterpret_cast<const EB_GLOBAL uint32_t *>(p + m.dim);
+          __builtin_nontemporal_store(outv[0], dst);
         }
       }
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (ok[u]) accumulate<DT, W>(acc, v[u], sb[u], W ? w[u] : 1.0f);
-      }
+      for (int i = 0; i < V; ++i) acc[i] = 0.0f;
     }
-  }
-
-  // combine the RPL row groups (fixed butterfly order: deterministic)
-#pragma unroll
-  for (int o = LPR; o < kWave; o <<= 1) {
-#pragma unroll
-    for (int i = 0; i < V; ++i) acc[i] += __shfl_xor(acc[i], o);
-  }
-
-  if (grp == 0 && colok) {
-    const int64_t L = hi - lo;
-    if (a.mean && L > 0) {
-      const float fl = (float)L;
-#pragma unroll
-      for (int i = 0; i < V; ++i) acc[i] = acc[i] / fl;
-    }
-    f32x4 *o4 = reinterpret_cast<f32x4 *>(dst + colb / Vals<DT>::esize);
-#pragma unroll
-    for (int i = 0; i < V / 4; ++i) o4[i] = f32x4{acc[4 * i], acc[4 * i + 1], acc[4 * i + 2], acc[4 * i + 3]};
+    if (!more) break;
+    j = jn;
+    c = cn;
+    blo = nlo;
+    bhi = nhi;
+    cur = nxt;
   }
 }
 
 template <int DT, int LPR, bool W>
-__device__ __forceinline__ void pool_all_passes(const TableMeta &m, const FwdArgs &a, int64_t lo, int64_t hi,
-                                                float *dst) {
+__device__ __forceinline__ void pool_all_passes(const TableMeta &m, const FwdArgs &a, int32_t g0, int nb,
+                                                int32_t b0) {
   if constexpr (LPR == kWave) {
-    for (int p = 0; p < m.passes; ++p) pool_bag<DT, LPR, W>(m, a, lo, hi, dst, p * kPassBytes);
+    for (int p = 0; p < m.passes; ++p) pool_bags<DT, LPR, W>(m, a, g0, nb, b0, p * kPassBytes);
   } else {
-    pool_bag<DT, LPR, W>(m, a, lo, hi, dst, 0);
+    pool_bags<DT, LPR, W>(m, a, g0, nb, b0, 0);
   }
+}
+
+// Workgroups are handed to the 8 XCDs round-robin (block i runs on XCD i % 8).
+// Renumber them so each XCD walks one contiguous eighth of the work: its L2
+// then caches the hot rows of fewer tables.
+__device__ __forceinline__ uint32_t xcd_contiguous(uint32_t i, uint32_t n) {
+  constexpr uint32_t kXcd = 8;
+  const uint32_t x = i % kXcd, slot = i / kXcd;
+  const uint32_t q = n / kXcd, r = n % kXcd;
+  return x < r ? x * (q + 1) + slot : r * (q + 1) + (x - r) * q + slot;
 }
 
 #define EB_KIND(DT, LOG2)                                                     \
   case (DT)*8 + (LOG2):                                                       \
-    pool_all_passes<DT, (1 << (LOG2)), W>(m, a, lo, hi, dst);                 \
+    pool_all_passes<DT, (1 << (LOG2)), W>(m, a, g0, nb, b0);                  \
     break;
 
 template <bool W>
 __global__ __launch_bounds__(kBlock) void eb_pool_kernel(FwdArgs a) {
-  const int32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int32_t g = (int32_t)blockIdx.x * kWavesPerBlock + wave;
-  if (g >= a.num_bags) return;
-  const int32_t t = g / a.batch;
-  const int32_t b = g - t * a.batch;
+  const uint32_t blk = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int32_t wid = (int32_t)blk * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  if (wid >= a.num_waves) return;
+  const int32_t t = wid / a.groups_per_table;
+  const int32_t b0 = (wid - t * a.groups_per_table) * a.bags_per_wave;
+  const int nb = (a.batch - b0) < a.bags_per_wave ? (a.batch - b0) : a.bags_per_wave;
+  const int32_t g0 = t * a.batch + b0;
   const TableMeta m = a.meta[t];
-
-  int64_t lo, hi;
-  if (a.idx64) {
-    lo = static_cast<const int64_t *>(a.offsets)[g];
-    hi = static_cast<const int64_t *>(a.offsets)[g + 1];
-  } else {
-    lo = static_cast<const int32_t *>(a.offsets)[g];
-    hi = static_cast<const int32_t *>(a.offsets)[g + 1];
-  }
-  // never read outside [0, N): clamp a broken partition and report it
-  bool bad = lo < 0 || hi < lo || hi > a.num_indices;
-  bad |= (g == 0 && lo != 0) || (g == a.num_bags - 1 && hi != a.num_indices);
-  if (bad) {
-    if ((threadIdx.x & (kWave - 1)) == 0) atomicOr(a.err, kErrOffsets);
-    lo = lo < 0 ? 0 : (lo > a.num_indices ? a.num_indices : lo);
-    hi = hi < lo ? lo : (hi > a.num_indices ? a.num_indices : hi);
-  }
-  float *dst = a.out + (int64_t)b * a.out_ld + m.out_col;
 
   switch (m.kind) {
     EB_KIND(kF32, 0) EB_KIND(kF32, 1) EB_KIND(kF32, 2) EB_KIND(kF32, 3)
@@ -296,6 +471,7 @@ struct eb_tables {
   hipStream_t stream;
   int32_t num_tables;
   int32_t checked;
+  int32_t bags_per_wave;  // 0: chosen per call from the bag count
   int64_t sum_dim;
   TableMeta *d_meta;  // device: num_tables descriptors followed by the error word
   int *d_err;
@@ -382,6 +558,9 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   h->sum_dim = col;
   const char *chk = getenv("EB_CHECK");
   h->checked = (chk && chk[0] == '1') ? 1 : 0;
+  const char *bpw = getenv("EB_BAGS_PER_WAVE");
+  h->bags_per_wave = bpw ? atoi(bpw) : 0;
+  if (h->bags_per_wave < 0 || h->bags_per_wave > kMaxBagsPerWave) h->bags_per_wave = 0;
 
   const size_t meta_bytes = sizeof(TableMeta) * (size_t)num_tables;
   void *dev = nullptr;
@@ -449,12 +628,27 @@ eb_status eb_forward(const eb_tables *h, eb_tensor indices, eb_tensor offsets, e
   a.batch = (int32_t)batch;
   a.idx64 = indices.elem_type == EB_I64;
   a.mean = pooling == EB_POOL_MEAN;
+  int64_t k = h->bags_per_wave;
+  if (k == 0) {
+    // More bags per wavefront hide more latency (each bag's indices arrive
+    // while the previous bag's rows are in flight); fewer leave more
+    // wavefronts to balance the load.  Measured optimum on MI355X: about
+    // sqrt(bags / resident wavefronts).
+    const int64_t per_slot = num_bags / kResidentWaves;
+    k = 1;
+    while ((k + 1) * (k + 1) <= per_slot) ++k;
+    k = k > kMaxBagsPerWave ? kMaxBagsPerWave : k;
+  }
+  a.bags_per_wave = (int32_t)k;
+  a.groups_per_table = (int32_t)((batch + k - 1) / k);
+  const int64_t num_waves = (int64_t)a.groups_per_table * h->num_tables;
+  a.num_waves = (int32_t)num_waves;
 
   eb_status st = EB_OK;
   hipError_t e = hipSuccess;
   if (h->checked) e = hipMemsetAsync(h->d_err, 0, sizeof(int), h->stream);
   if (e == hipSuccess) {
-    const unsigned grid = (unsigned)((num_bags + kWavesPerBlock - 1) / kWavesPerBlock);
+    const unsigned grid = (unsigned)((num_waves + kWavesPerBlock - 1) / kWavesPerBlock);
     if (weighted)
       hipLaunchKernelGGL(eb_pool_kernel<true>, dim3(grid), dim3(kBlock), 0, h->stream, a);
     else

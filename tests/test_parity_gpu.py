@@ -118,6 +118,17 @@ def test_uniform_index_control(dev, name):
     full_check(w, f"uniform {name}")
 
 
+@pytest.mark.parametrize("k", [2, 3, 7, 32])
+@pytest.mark.parametrize("name", ["c3a", "c4", "c5"])
+def test_bags_per_wave(dev, monkeypatch, name, k):
+    # several consecutive bags (and their chunk stream) per wavefront; the
+    # last group of each table is partial whenever k does not divide B
+    say(f"[parity] bags per wave {k} {name}")
+    monkeypatch.setenv("EB_BAGS_PER_WAVE", str(k))
+    w = make_workload(name, dev, **REDUCED[name])
+    full_check(w, f"k={k} {name}")
+
+
 # ----------------------------------------------------------------------------
 # full sizes, in the launch configuration the benchmark times
 
@@ -233,9 +244,11 @@ WIDTHS = [("f32", 4), ("f32", 12), ("f32", 20), ("f32", 100), ("f32", 260), ("f3
           ("int8_rowwise", 2064)]
 
 
+@pytest.mark.parametrize("k", ["0", "5"])
 @pytest.mark.parametrize("mode", ["sum", "mean", "weighted"])
-def test_every_width_in_one_launch(dev, mode):
-    say(f"[parity] widths {mode}")
+def test_every_width_in_one_launch(dev, monkeypatch, mode, k):
+    say(f"[parity] widths {mode} k={k}")
+    monkeypatch.setenv("EB_BAGS_PER_WAVE", k)
     rng = np.random.default_rng(5)
     tables = [_table(dev, dt, 300 + 7 * i, D, seed=i) for i, (dt, D) in enumerate(WIDTHS)]
     B = 37
@@ -255,9 +268,11 @@ def test_padded_row_strides(dev):
     full_check(w, "padded strides")
 
 
+@pytest.mark.parametrize("k", ["0", "3"])
 @pytest.mark.parametrize("dtype", ["f32", "f16", "int8_rowwise"])
-def test_long_bags(dev, dtype):
-    say(f"[parity] long bags {dtype}")
+def test_long_bags(dev, monkeypatch, dtype, k):
+    say(f"[parity] long bags {dtype} k={k}")
+    monkeypatch.setenv("EB_BAGS_PER_WAVE", k)
     D = {"f32": 64, "f16": 128, "int8_rowwise": 128}[dtype]
     tables = [_table(dev, dtype, 5000, D)]
     w = _custom(dev, tables, [np.array([5000, 0, 1, 63, 64, 65, 1000, 4097])])
