@@ -52,8 +52,10 @@
  *
  * Tuning.  EB_BAGS_PER_WAVE=k (1..32), read when a handle is created, fixes
  * how many consecutive bags of one table a wavefront pools; without it the
- * count is chosen per call from the number of bags.  Results do not depend
- * on it.
+ * count is chosen per call from the number of bags.  EB_XCD_REMAP=0|1, read
+ * at the same time, forces how workgroups map onto the GPU's XCDs (default:
+ * XCD-contiguous for handles of up to 32 tables, round-robin otherwise).
+ * Results do not depend on either.
  */
 #ifndef EB_H_
 #define EB_H_

@@ -29,6 +29,12 @@
 
 #include "eb.h"
 
+// Unweighted int8 row-wise pooling sums s*q and the biases separately (one
+// fma per element instead of two); 0 keeps the per-element dequantisation.
+#ifndef EB_INT8_SPLIT_BIAS
+#define EB_INT8_SPLIT_BIAS 1
+#endif
+
 namespace {
 
 constexpr int kWave = 64;
@@ -37,11 +43,16 @@ constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr int kPassBytes = kWave * 16;  // one wave-wide 16-byte load covers 1 KiB
 constexpr uint32_t kBadRow = 0xFFFFFFFFu;
 constexpr int kMaxDim = 8192;
+// An all-zero row as long as the widest row slice any lane can address
+// (8192 fp32 values) plus the int8 scale/bias word.
+constexpr size_t kZeroBytes = 4 * kMaxDim + 16;
 // A wavefront pools up to this many consecutive bags (their offsets are read
 // with one vector load, one per lane, so at most 63).
 constexpr int kMaxBagsPerWave = 32;
 // Wavefronts resident on a full MI355X (256 CUs x 4 SIMDs x 8 waves).
 constexpr int64_t kResidentWaves = 256 * 4 * 8;
+// Handles with at most this many tables renumber workgroups XCD-contiguously.
+constexpr int32_t kRemapMaxTables = 32;
 
 // error bits raised by the kernel, reported in checked mode
 constexpr int kErrIndex = 1;
@@ -64,6 +75,7 @@ struct TableMeta {
 
 struct FwdArgs {
   const TableMeta *meta;
+  const unsigned char *zero;  // kZeroBytes of zeros (read in place of rows that do not exist)
   const void *indices;
   const void *offsets;
   const float *weights;
@@ -78,6 +90,8 @@ struct FwdArgs {
   int32_t bags_per_wave;     // consecutive bags of one table per wavefront
   int32_t groups_per_table;  // ceil(batch / bags_per_wave)
   int32_t num_waves;         // num_tables * groups_per_table
+  float one;                 // 1.0f (see accumulate)
+  int32_t xcd_remap;         // renumber workgroups XCD-contiguously
 };
 
 // Table rows are plain device memory: address them in the global address
@@ -104,8 +118,17 @@ __device__ __forceinline__ float half_hi(uint32_t v) {
 }
 
 // acc += x (or acc = w*x + acc) for the 16-byte slice v of one row.
-template <int DT, bool W>
-__device__ __forceinline__ void accumulate(float (&acc)[Vals<DT>::n], u32x4 v, uint32_t sb, float w) {
+//   `one` is 1.0f passed in at run time: fmaf(x, one, acc) with an fp16 x
+//   then compiles to a single v_fma_mix_f32 that widens and adds (exact
+//   widening, one rounding: the same bits as acc + x).
+//   Unweighted int8 rows (SPLIT) accumulate s*q with one fma per element
+//   (s*q is exact in fp32) and the row's bias once into cb; the caller adds
+//   cb to every element before the cross-lane reduction.  For a one-row bag
+//   that gives fp32(s*q + c) exactly as the dequantisation is defined; for
+//   longer bags it is a reassociation of the same sum.
+template <int DT, bool W, bool SPLIT>
+__device__ __forceinline__ void accumulate(float (&acc)[Vals<DT>::n], float &cb, u32x4 v, uint32_t sb, float w,
+                                           float one) {
   if constexpr (DT == kF32) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -113,11 +136,19 @@ __device__ __forceinline__ void accumulate(float (&acc)[Vals<DT>::n], u32x4 v, u
       acc[i] = W ? fmaf(w, x, acc[i]) : acc[i] + x;
     }
   } else if constexpr (DT == kF16) {
+    const float f = W ? w : one;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float x0 = half_lo(v[i]), x1 = half_hi(v[i]);
-      acc[2 * i] = W ? fmaf(w, x0, acc[2 * i]) : acc[2 * i] + x0;
-      acc[2 * i + 1] = W ? fmaf(w, x1, acc[2 * i + 1]) : acc[2 * i + 1] + x1;
+      acc[2 * i] = fmaf(half_lo(v[i]), f, acc[2 * i]);
+      acc[2 * i + 1] = fmaf(half_hi(v[i]), f, acc[2 * i + 1]);
+    }
+  } else if constexpr (SPLIT && !W) {
+    const float s = half_lo(sb);
+    cb = fmaf(half_hi(sb), one, cb);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[4 * i + j] = fmaf(s, (float)((v[i] >> (8 * j)) & 0xFFu), acc[4 * i + j]);
     }
   } else {
     // x = fp32(s*q + c): s*q is exact in fp32 (11-bit by 8-bit significands),
@@ -144,11 +175,19 @@ __device__ __forceinline__ u32x4 load_slice(gbyte *p) {
   }
 }
 
-// Loads in flight per lane before the first is consumed: enough rows per
-// wave to cover HBM latency within the register budget.
-template <int RPL>
+// Row-load steps issued before the first is consumed: enough rows in flight
+// per wave to cover HBM latency within the register budget.
+#ifndef EB_INT8_MAX_UNROLL
+#define EB_INT8_MAX_UNROLL 4
+#endif
+#ifndef EB_WEIGHTED_MAX_UNROLL
+#define EB_WEIGHTED_MAX_UNROLL 4
+#endif
+template <int DT, int RPL, bool W>
 struct Unroll {
-  static constexpr int u = RPL >= 16 ? 2 : (RPL >= 8 ? 4 : 8);
+  static constexpr int c0 = DT == kU8 ? EB_INT8_MAX_UNROLL : 8;
+  static constexpr int cap = W && EB_WEIGHTED_MAX_UNROLL < c0 ? EB_WEIGHTED_MAX_UNROLL : c0;
+  static constexpr int u = (kWave / RPL) < cap ? (kWave / RPL) : cap;
 };
 
 // 64-bit value of lane `l` (wave-uniform l) of a per-lane value.
@@ -182,50 +221,75 @@ __device__ __forceinline__ Chunk load_chunk(const TableMeta &m, const FwdArgs &a
   return k;
 }
 
-// Gather the rows of one chunk and add them into this lane's accumulators.
-template <int DT, int LPR, bool W>
-__device__ __forceinline__ void gather_chunk(const TableMeta &m, const FwdArgs &a, const Chunk &k,
-                                             float (&acc)[Vals<DT>::n], int colb, bool colok) {
+// Gather steps [s0, s0 + N) of one chunk (RPL rows per step) and add them into
+// this lane's accumulators.  Straight-line code: a lane whose row does not
+// exist (past the chunk's end, outside the table, or a slice past the row's
+// end) reads the handle's all-zero row instead, which adds nothing, so no
+// branch separates a load from its use and the loads of all N steps are in
+// flight together.
+template <int DT, int LPR, bool W, bool SPLIT, int N>
+__device__ __forceinline__ void gather_steps(const TableMeta &m, const FwdArgs &a, const Chunk &k, int s0,
+                                             float (&acc)[Vals<DT>::n], float &cb, int colb, bool colok) {
   constexpr int RPL = kWave / LPR;
-  constexpr int U = Unroll<RPL>::u;
   const int lane = threadIdx.x & (kWave - 1);
   const int grp = lane / LPR;
+  u32x4 v[N];
+  uint32_t sb[N];
+  float w[N];
+#pragma unroll
+  for (int u = 0; u < N; ++u) {
+    const int r = (s0 + u) * RPL + grp;
+    uint32_t row;
+    if constexpr (RPL == 1) {
+      row = __builtin_amdgcn_readlane(k.row, (s0 + u) & (kWave - 1));
+      if constexpr (W)
+        w[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(uint32_t, k.w),
+                                                                    (s0 + u) & (kWave - 1)));
+    } else {
+      row = (uint32_t)__shfl((int)k.row, r & (kWave - 1));
+      if constexpr (W) w[u] = __shfl(k.w, r & (kWave - 1));
+    }
+    const bool ok = (r < k.n) && (row != kBadRow) && colok;
+    gbyte *p = ok ? (gbyte *)m.data + (uint64_t)row * m.row_stride : (gbyte *)a.zero;
+    v[u] = load_slice<DT>(p + colb);
+    if constexpr (DT == kU8) sb[u] = *reinterpret_cast<const EB_GLOBAL uint32_t *>(p + m.dim);
+    else sb[u] = 0u;
+    if constexpr (!W) w[u] = 1.0f;
+  }
+#pragma unroll
+  for (int u = 0; u < N; ++u) accumulate<DT, W, SPLIT>(acc, cb, v[u], sb[u], w[u], a.one);
+}
+
+// Gather all rows of one chunk: full batches of U steps, then one batch of
+// the smallest power-of-two size that covers the remaining steps (its
+// missing steps read the zero row), so a chunk of up to U steps costs one
+// memory round trip.
+template <int DT, int LPR, bool W, bool SPLIT>
+__device__ __forceinline__ void gather_chunk(const TableMeta &m, const FwdArgs &a, const Chunk &k,
+                                             float (&acc)[Vals<DT>::n], float &cb, int colb, bool colok) {
+  constexpr int RPL = kWave / LPR;
+  constexpr int U = Unroll<DT, RPL, W>::u;
+  const int lane = threadIdx.x & (kWave - 1);
   if (__ballot(lane < k.n && k.row == kBadRow)) {
     if (lane == 0) atomicOr(a.err, kErrIndex);
   }
   const int steps = (k.n + RPL - 1) / RPL;
-  for (int s = 0; s < steps; s += U) {
-    u32x4 v[U];
-    uint32_t sb[U];
-    float w[U];
-    bool ok[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int r = (s + u) * RPL + grp;
-      uint32_t row;
-      if constexpr (RPL == 1) {
-        row = __builtin_amdgcn_readlane(k.row, (s + u) & (kWave - 1));
-        if constexpr (W)
-          w[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(uint32_t, k.w),
-                                                                      (s + u) & (kWave - 1)));
-      } else {
-        row = (uint32_t)__shfl((int)k.row, r & (kWave - 1));
-        if constexpr (W) w[u] = __shfl(k.w, r & (kWave - 1));
-      }
-      ok[u] = (r < k.n) && (row != kBadRow) && colok;
-      v[u] = u32x4{0u, 0u, 0u, 0u};
-      sb[u] = 0u;
-      if (ok[u]) {
-        gbyte *p = (gbyte *)m.data + (uint64_t)row * m.row_stride;
-        v[u] = load_slice<DT>(p + colb);
-        if constexpr (DT == kU8) sb[u] = *reinterpret_cast<const EB_GLOBAL uint32_t *>(p + m.dim);
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (ok[u]) accumulate<DT, W>(acc, v[u], sb[u], W ? w[u] : 1.0f);
+  int s = 0;
+  for (; steps - s > U / 2; s += U) gather_steps<DT, LPR, W, SPLIT, U>(m, a, k, s, acc, cb, colb, colok);
+  const int rem = steps - s;  // 0 .. U/2
+  if constexpr (U >= 8) {
+    if (rem > 2) {
+      gather_steps<DT, LPR, W, SPLIT, 4>(m, a, k, s, acc, cb, colb, colok);
+      return;
     }
   }
+  if constexpr (U >= 4) {
+    if (rem > 1) {
+      gather_steps<DT, LPR, W, SPLIT, 2>(m, a, k, s, acc, cb, colb, colok);
+      return;
+    }
+  }
+  if (rem > 0) gather_steps<DT, LPR, W, SPLIT, 1>(m, a, k, s, acc, cb, colb, colok);
 }
 
 __device__ __forceinline__ float dpp_row_ror(float x, int o) {
@@ -343,7 +407,9 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
     }
   };
 
+  constexpr bool SPLIT = EB_INT8_SPLIT_BIAS && DT == kU8 && !W;
   float acc[V];
+  float cb = 0.0f;
 #pragma unroll
   for (int i = 0; i < V; ++i) acc[i] = 0.0f;
 
@@ -367,9 +433,14 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
     Chunk nxt;
     if (more) nxt = load_chunk<W>(m, a, cn, nhi);
 
-    gather_chunk<DT, LPR, W>(m, a, cur, acc, colb, colok);
+    gather_chunk<DT, LPR, W, SPLIT>(m, a, cur, acc, cb, colb, colok);
 
     if (last) {
+      if constexpr (SPLIT) {
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] += cb;
+        cb = 0.0f;
+      }
       R::run(acc);
       if (R::stores(lane) && colok) {
         const int64_t L = bhi - blo;
@@ -418,8 +489,11 @@ __device__ __forceinline__ void pool_all_passes(const TableMeta &m, const FwdArg
 }
 
 // Workgroups are handed to the 8 XCDs round-robin (block i runs on XCD i % 8).
-// Renumber them so each XCD walks one contiguous eighth of the work: its L2
-// then caches the hot rows of fewer tables.
+// Renumbering them so each XCD walks one contiguous eighth of the work keeps
+// each XCD's L2 on few tables for the whole launch; leaving them round-robin
+// puts all XCDs on the same table at once, so the shared Infinity Cache holds
+// that one table's hot rows.  The first wins with few tables (measured: 8 and
+// 26), the second with many large ones (64 and 100); the host picks.
 __device__ __forceinline__ uint32_t xcd_contiguous(uint32_t i, uint32_t n) {
   constexpr uint32_t kXcd = 8;
   const uint32_t x = i % kXcd, slot = i / kXcd;
@@ -427,14 +501,19 @@ __device__ __forceinline__ uint32_t xcd_contiguous(uint32_t i, uint32_t n) {
   return x < r ? x * (q + 1) + slot : r * (q + 1) + (x - r) * q + slot;
 }
 
-#define EB_KIND(DT, LOG2)                                                     \
-  case (DT)*8 + (LOG2):                                                       \
+#define EB_LPR(LOG2)                                                          \
+  case LOG2:                                                                  \
     pool_all_passes<DT, (1 << (LOG2)), W>(m, a, g0, nb, b0);                  \
     break;
 
-template <bool W>
+// One wavefront per run of bags.  DT is the storage type the launch serves
+// (wavefronts of other tables return at once).  LOG2 >= 0 fixes the lanes
+// per row for handles whose tables all share one kind; LOG2 < 0 switches on
+// each table's lanes per row.  Specialising keeps the register count (and so
+// the occupancy) at what that kind needs.
+template <int DT, int LOG2, bool W>
 __global__ __launch_bounds__(kBlock) void eb_pool_kernel(FwdArgs a) {
-  const uint32_t blk = xcd_contiguous(blockIdx.x, gridDim.x);
+  const uint32_t blk = a.xcd_remap ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x;
   const int32_t wid = (int32_t)blk * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if (wid >= a.num_waves) return;
   const int32_t t = wid / a.groups_per_table;
@@ -442,20 +521,43 @@ __global__ __launch_bounds__(kBlock) void eb_pool_kernel(FwdArgs a) {
   const int nb = (a.batch - b0) < a.bags_per_wave ? (a.batch - b0) : a.bags_per_wave;
   const int32_t g0 = t * a.batch + b0;
   const TableMeta m = a.meta[t];
+  if (m.kind / 8 != DT) return;
 
-  switch (m.kind) {
-    EB_KIND(kF32, 0) EB_KIND(kF32, 1) EB_KIND(kF32, 2) EB_KIND(kF32, 3)
-    EB_KIND(kF32, 4) EB_KIND(kF32, 5) EB_KIND(kF32, 6)
-    EB_KIND(kF16, 0) EB_KIND(kF16, 1) EB_KIND(kF16, 2) EB_KIND(kF16, 3)
-    EB_KIND(kF16, 4) EB_KIND(kF16, 5) EB_KIND(kF16, 6)
-    EB_KIND(kU8, 0) EB_KIND(kU8, 1) EB_KIND(kU8, 2) EB_KIND(kU8, 3)
-    EB_KIND(kU8, 4) EB_KIND(kU8, 5) EB_KIND(kU8, 6)
-    default:
-      break;
+  if constexpr (LOG2 >= 0) {
+    pool_all_passes<DT, (1 << LOG2), W>(m, a, g0, nb, b0);
+  } else {
+    switch (m.kind % 8) {
+      EB_LPR(0) EB_LPR(1) EB_LPR(2) EB_LPR(3) EB_LPR(4) EB_LPR(5) EB_LPR(6)
+      default:
+        break;
+    }
   }
 }
 
-#undef EB_KIND
+#undef EB_LPR
+
+typedef void (*KernelFn)(FwdArgs);
+
+// kernel for (storage type, log2 lanes per row or -1, weighted)
+template <int DT, bool W>
+KernelFn pick_kernel(int log2) {
+  switch (log2) {
+    case 0: return eb_pool_kernel<DT, 0, W>;
+    case 1: return eb_pool_kernel<DT, 1, W>;
+    case 2: return eb_pool_kernel<DT, 2, W>;
+    case 3: return eb_pool_kernel<DT, 3, W>;
+    case 4: return eb_pool_kernel<DT, 4, W>;
+    case 5: return eb_pool_kernel<DT, 5, W>;
+    case 6: return eb_pool_kernel<DT, 6, W>;
+    default: return eb_pool_kernel<DT, -1, W>;
+  }
+}
+
+KernelFn pick_kernel(int dt, int log2, bool weighted) {
+  if (dt == kF32) return weighted ? pick_kernel<kF32, true>(log2) : pick_kernel<kF32, false>(log2);
+  if (dt == kF16) return weighted ? pick_kernel<kF16, true>(log2) : pick_kernel<kF16, false>(log2);
+  return weighted ? pick_kernel<kU8, true>(log2) : pick_kernel<kU8, false>(log2);
+}
 
 int log2_lanes_per_row(int code_bytes) {
   int slices = (code_bytes + 15) / 16;
@@ -472,9 +574,13 @@ struct eb_tables {
   int32_t num_tables;
   int32_t checked;
   int32_t bags_per_wave;  // 0: chosen per call from the bag count
+  int32_t dtype_mask;     // bit d set: some table has storage type d
+  int32_t single_log2;    // lanes-per-row log2 shared by every table of one type, else -1
+  int32_t xcd_remap;      // see xcd_contiguous
   int64_t sum_dim;
-  TableMeta *d_meta;  // device: num_tables descriptors followed by the error word
+  TableMeta *d_meta;  // device: descriptors, then the error word, then the zero row
   int *d_err;
+  unsigned char *d_zero;
 };
 
 extern "C" {
@@ -555,26 +661,37 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   }
   h->stream = static_cast<hipStream_t>(hip_stream);
   h->num_tables = num_tables;
+  h->dtype_mask = 0;
+  h->single_log2 = meta[0].kind % 8;
+  for (int32_t t = 0; t < num_tables; ++t) {
+    h->dtype_mask |= 1 << (meta[t].kind / 8);
+    if (meta[t].kind != meta[0].kind) h->single_log2 = -1;
+  }
   h->sum_dim = col;
   const char *chk = getenv("EB_CHECK");
   h->checked = (chk && chk[0] == '1') ? 1 : 0;
+  const char *remap = getenv("EB_XCD_REMAP");
+  h->xcd_remap = remap ? (remap[0] == '1') : (num_tables <= kRemapMaxTables);
   const char *bpw = getenv("EB_BAGS_PER_WAVE");
   h->bags_per_wave = bpw ? atoi(bpw) : 0;
   if (h->bags_per_wave < 0 || h->bags_per_wave > kMaxBagsPerWave) h->bags_per_wave = 0;
 
   const size_t meta_bytes = sizeof(TableMeta) * (size_t)num_tables;
+  // [descriptors][error word, padded to 256 B][zero row]
+  const size_t err_off = (meta_bytes + 255) / 256 * 256;
+  const size_t zero_off = err_off + 256;
   void *dev = nullptr;
-  hipError_t e = hipMalloc(&dev, meta_bytes + 256);
+  hipError_t e = hipMalloc(&dev, zero_off + kZeroBytes);
   if (e != hipSuccess) {
     free(meta);
     free(h);
     return e == hipErrorOutOfMemory ? EB_ERR_OOM : EB_ERR_HIP;
   }
   h->d_meta = static_cast<TableMeta *>(dev);
-  // the error word sits in the 256 bytes after the descriptors
-  h->d_err = reinterpret_cast<int *>(static_cast<char *>(dev) + meta_bytes);
+  h->d_err = reinterpret_cast<int *>(static_cast<char *>(dev) + err_off);
+  h->d_zero = static_cast<unsigned char *>(dev) + zero_off;
   e = hipMemcpy(h->d_meta, meta, meta_bytes, hipMemcpyHostToDevice);
-  if (e == hipSuccess) e = hipMemset(h->d_err, 0, sizeof(int));
+  if (e == hipSuccess) e = hipMemset(static_cast<char *>(dev) + err_off, 0, 256 + kZeroBytes);
   free(meta);
   if (e != hipSuccess) {
     (void)hipFree(dev);
@@ -622,6 +739,9 @@ eb_status eb_forward(const eb_tables *h, eb_tensor indices, eb_tensor offsets, e
   a.weights = static_cast<const float *>(per_sample_weights.data);
   a.out = static_cast<float *>(const_cast<void *>(out.data));
   a.err = h->d_err;
+  a.zero = h->d_zero;
+  a.one = 1.0f;
+  a.xcd_remap = h->xcd_remap;
   a.num_indices = indices.numel;
   a.out_ld = h->sum_dim;
   a.num_bags = (int32_t)num_bags;
@@ -649,11 +769,12 @@ eb_status eb_forward(const eb_tables *h, eb_tensor indices, eb_tensor offsets, e
   if (h->checked) e = hipMemsetAsync(h->d_err, 0, sizeof(int), h->stream);
   if (e == hipSuccess) {
     const unsigned grid = (unsigned)((num_waves + kWavesPerBlock - 1) / kWavesPerBlock);
-    if (weighted)
-      hipLaunchKernelGGL(eb_pool_kernel<true>, dim3(grid), dim3(kBlock), 0, h->stream, a);
-    else
-      hipLaunchKernelGGL(eb_pool_kernel<false>, dim3(grid), dim3(kBlock), 0, h->stream, a);
-    e = hipGetLastError();
+    // one launch per storage type present (one in the usual case)
+    for (int dt = 0; dt < 3 && e == hipSuccess; ++dt) {
+      if (!(h->dtype_mask & (1 << dt))) continue;
+      hipLaunchKernelGGL(pick_kernel(dt, h->single_log2, weighted), dim3(grid), dim3(kBlock), 0, h->stream, a);
+      e = hipGetLastError();
+    }
   }
   if (e == hipSuccess && h->checked) {
     int herr = 0;

@@ -6,9 +6,10 @@ and the oracle's error scale s = sum_i |w_i x_i| (divided by L for mean)):
   * otherwise |g - o| <= rtol * s with rtol = 1e-5 for fp32 tables and 2e-3
     for fp16 / int8 row-wise tables;
   * and, tighter, the a-priori bound of fp32 summation in any order,
-    |g - o| <= (L + 3) * 2^-24 * s (L - 1 additions, a rounded weight product
-    or dequantised value folded into an fma, the mean's division, and the
-    oracle's own final rounding).
+    |g - o| <= (L + 3) * 2^-24 * s' + 2 * 2^-24 * s, where s' = s except for
+    unweighted int8 row-wise tables: the kernel sums s*q and the biases c
+    separately (a reassociation), so s' = sum_i (|s_i q_i| + |c_i|), obtained
+    by running the oracle over an fp32 table holding |s| q + |c|.
 """
 import os
 
@@ -16,7 +17,7 @@ import numpy as np
 import pytest
 import torch
 
-from conftest import oracle_forward, ulp_distance
+from conftest import oracle_forward, oracle_tables, ulp_distance
 from oracle import OracleTable, ebo_forward
 from paper_2609_30656_amd import eb
 from paper_2609_30656_amd.workload import Table, make_workload
@@ -49,8 +50,9 @@ def run_gpu(w, stream=None, prefill=float("nan")):
     return out
 
 
-def check(got, ref, asum, L, rtol, label):
-    """got/ref fp32, asum fp64, L int (same shape)."""
+def check(got, ref, asum, L, rtol, label, bscale=None):
+    """got/ref fp32, asum fp64, L int (same shape); bscale: scale of the
+    summation bound (asum when None)."""
     got = np.asarray(got, np.float32)
     err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
     assert not np.isnan(got).any(), f"{label}: NaN in output (an element was not written)"
@@ -64,7 +66,8 @@ def check(got, ref, asum, L, rtol, label):
         bad = err[long_] > lim
         assert not bad.any(), (f"{label}: {bad.sum()} outputs beyond rtol {rtol}; worst ratio "
                                f"{np.max(err[long_] / np.maximum(lim, 1e-300)):.3g}")
-        bound = (L[long_] + 3) * U * asum[long_]
+        bs = asum if bscale is None else bscale
+        bound = (L[long_] + 3) * U * bs[long_] + 2 * U * asum[long_]
         over = err[long_] > bound
         assert not over.any(), f"{label}: {over.sum()} outputs beyond the summation error bound"
 
@@ -76,11 +79,33 @@ def per_element_lengths(w, bags=None):
     return lens.reshape(-1)[bags][:, None]
 
 
+def split_scale_tables(w, tables):
+    """Oracle tables for the summation-bound scale: unweighted int8 row-wise
+    tables become fp32 tables of |s| q + |c| (others are unchanged)."""
+    if w.weights is not None or not any(t.dtype == "int8_rowwise" for t in w.tables):
+        return None
+    out = []
+    for tb, ot in zip(w.tables, tables):
+        if tb.dtype != "int8_rowwise" or ot.rows is None:
+            out.append(ot)
+            continue
+        D = tb.dim
+        rows = ot.rows
+        sc = np.abs(rows[:, D:D + 2].copy().view(np.float16).astype(np.float32))
+        bi = np.abs(rows[:, D + 2:D + 4].copy().view(np.float16).astype(np.float32))
+        a = rows[:, :D].astype(np.float32) * sc + bi
+        out.append(OracleTable(np.ascontiguousarray(a * np.float32(1.0001)), D, "f32", tb.num_rows))
+    return out
+
+
 def full_check(w, label, stream=None):
     got = run_gpu(w, stream).cpu().numpy()
-    ref, asum = oracle_forward(w)
+    tabs = oracle_tables(w)
+    ref, asum = oracle_forward(w, tables=tabs)
+    bs_tabs = split_scale_tables(w, tabs)
+    bscale = None if bs_tabs is None else oracle_forward(w, tables=bs_tabs)[1]
     rtol = max(RTOL[t.dtype] for t in w.tables)
-    check(got, ref, asum, per_element_lengths(w), rtol, label)
+    check(got, ref, asum, per_element_lengths(w), rtol, label, bscale)
     return got
 
 
@@ -185,6 +210,8 @@ def test_full_size_sampled(dev, name):
     tabs = [OracleTable(tb.rows.cpu().numpy() if t in check_tables else None, tb.dim, tb.dtype, tb.num_rows)
             for t, tb in enumerate(w.tables)]
     ref, asum = oracle_forward(w, tables=tabs, bags=bags)
+    bs_tabs = split_scale_tables(w, tabs)
+    bscale = asum if bs_tabs is None else oracle_forward(w, tables=bs_tabs, bags=bags)[1]
     g_host = got.cpu().numpy()
     doff = np.concatenate([[0], np.cumsum([tb.dim for tb in w.tables])])
     B = w.batch
@@ -193,7 +220,7 @@ def test_full_size_sampled(dev, name):
         t, b = divmod(int(g), B)
         D = w.tables[t].dim
         check(g_host[b, doff[t]:doff[t] + D], ref[k, :D], asum[k, :D], np.full(D, L[k, 0]),
-              RTOL[w.tables[t].dtype], f"full {name} bag {g}")
+              RTOL[w.tables[t].dtype], f"full {name} bag {g}", bscale[k, :D])
 
 
 # ----------------------------------------------------------------------------
