@@ -238,3 +238,222 @@ int ebo_max_threads(void) {
   return 1;
 #endif
 }
+
+/* ========================================================================
+ * Backward with a fused row-wise optimizer update (test infrastructure).
+ *
+ * The paper's component benchmark profiles both the forward and the
+ * backward pass of each submodule (Sec. III-A); for sparse_arch the backward
+ * is the gradient of the pooled lookup with respect to the table rows,
+ * followed by the optimizer's sparse update of the rows that were read.
+ * With c_i = w_i (weighted sum), 1 (sum) or 1/L (mean, L = the bag's length),
+ * for every table t and every row r that occurs in the batch:
+ *
+ *   G[d] = sum over positions i of table t with idx_i = r of
+ *          c_i * grad_out[b(i), Doff[t] + d]          (fp64, in position order)
+ *   SGD:                 W[r] <- W[r] - lr * G
+ *   row-wise Adagrad:    s[r] <- s[r] + (1/D) sum_d G[d]^2
+ *                        W[r] <- W[r] - lr * G / (sqrt(s[r]) + eps)
+ *
+ * computed in fp64 from the stored values and rounded once to the table's
+ * storage type (and s to fp32).  Rows that do not occur are left alone.
+ * Only fp32 and fp16 tables train; the optimizer and its state layout are
+ * readings (the paper names neither).
+ * ======================================================================== */
+
+/* double -> IEEE binary16, round to nearest even, from the bit-level
+ * definition (normal, subnormal, overflow to infinity, NaN). */
+uint16_t ebo_double_to_half(double x) {
+  uint16_t sign = signbit(x) ? 0x8000 : 0;
+  double a = fabs(x);
+  if (isnan(x)) return 0x7E00;
+  if (a >= 65520.0) return sign | 0x7C00; /* at or past max + half ulp: infinity */
+  if (a < ldexp(1.0, -14)) {
+    /* subnormal range: value = m * 2^-24, m in [0, 1024] (1024 = smallest normal) */
+    double m = a * ldexp(1.0, 24);
+    double f = floor(m);
+    double rem = m - f;
+    uint32_t mi = (uint32_t)f;
+    if (rem > 0.5 || (rem == 0.5 && (mi & 1u))) ++mi;
+    return sign | (uint16_t)mi; /* mi = 1024 encodes the smallest normal */
+  }
+  int e;
+  double fr = frexp(a, &e); /* a = fr * 2^e, fr in [0.5, 1) */
+  /* a = 1.m * 2^(e-1); significand with 10 fraction bits: fr * 2^11 in [1024, 2048) */
+  double m = ldexp(fr, 11);
+  double f = floor(m);
+  double rem = m - f;
+  uint32_t mi = (uint32_t)f;
+  if (rem > 0.5 || (rem == 0.5 && (mi & 1u))) ++mi;
+  int ex = e - 1 + 15;
+  if (mi == 2048) { mi = 1024; ++ex; }
+  if (ex >= 31) return sign | 0x7C00;
+  return sign | (uint16_t)((ex << 10) | (mi - 1024));
+}
+
+typedef struct {
+  int64_t row; /* row number */
+  int64_t pos; /* position in indices */
+  int64_t bag; /* global bag id g */
+} ebo_occ;
+
+static int ebo_occ_cmp(const void *pa, const void *pb) {
+  const ebo_occ *a = (const ebo_occ *)pa, *b = (const ebo_occ *)pb;
+  if (a->row != b->row) return a->row < b->row ? -1 : 1;
+  return a->pos < b->pos ? -1 : (a->pos > b->pos ? 1 : 0);
+}
+
+/* Optional per-table report of the touched rows: row ids (ascending), G and
+ * S = sum_i |c_i g| per element (fp64, [rows x D]) and occurrence counts.
+ * Arrays must hold at least as many rows as the table has positions. */
+typedef struct {
+  int64_t *rows;
+  double *grad;
+  double *scale;
+  int64_t *count;
+  int64_t num_rows; /* out */
+} ebo_row_report;
+
+#define EBO_OPT_SGD 0
+#define EBO_OPT_ROWWISE_ADAGRAD 1
+
+/*
+ * tables: writable rows (data == NULL: table skipped, left alone);
+ * grad_out: [B, sum D] fp32; state: fp32, table t's rows at
+ * state + sum_{s<t} R_s (row-wise Adagrad only, else NULL);
+ * reports: NULL or one entry per table (entries may have rows == NULL).
+ */
+int ebo_backward_update(const ebo_table *tables, int32_t num_tables, const void *indices,
+                        const void *offsets, int32_t index_type, int64_t num_indices,
+                        int64_t num_offsets, const float *weights, int32_t mode,
+                        const float *grad_out, int32_t opt, float lr, float eps, float *state,
+                        ebo_row_report *reports, int32_t num_threads) {
+  if (!tables || num_tables < 1 || !offsets || !grad_out) return EBO_ERR_INVALID_ARG;
+  if (num_indices < 0 || (num_indices > 0 && !indices)) return EBO_ERR_INVALID_ARG;
+  if (index_type != EBO_IDX_I32 && index_type != EBO_IDX_I64) return EBO_ERR_DTYPE;
+  if (mode != EBO_MODE_SUM && mode != EBO_MODE_MEAN) return EBO_ERR_INVALID_ARG;
+  if (weights && mode == EBO_MODE_MEAN) return EBO_ERR_INVALID_ARG;
+  if (opt != EBO_OPT_SGD && opt != EBO_OPT_ROWWISE_ADAGRAD) return EBO_ERR_INVALID_ARG;
+  if (opt == EBO_OPT_ROWWISE_ADAGRAD && !state) return EBO_ERR_INVALID_ARG;
+  if (num_offsets < 2 || (num_offsets - 1) % num_tables != 0) return EBO_ERR_SHAPE;
+  const int64_t B = (num_offsets - 1) / num_tables;
+  const int64_t nbags = num_offsets - 1;
+  int64_t sum_d = 0;
+  for (int32_t t = 0; t < num_tables; ++t) {
+    if (tables[t].dtype != EBO_ROW_F32 && tables[t].dtype != EBO_ROW_F16) return EBO_ERR_DTYPE;
+    if (tables[t].dim < 1 || tables[t].num_rows < 1) return EBO_ERR_INVALID_ARG;
+    sum_d += tables[t].dim;
+  }
+  if (ebo_read_index(offsets, index_type, 0) != 0) return EBO_ERR_OFFSETS;
+  for (int64_t g = 0; g < nbags; ++g)
+    if (ebo_read_index(offsets, index_type, g + 1) < ebo_read_index(offsets, index_type, g))
+      return EBO_ERR_OFFSETS;
+  if (ebo_read_index(offsets, index_type, nbags) != num_indices) return EBO_ERR_OFFSETS;
+  for (int32_t t = 0; t < num_tables; ++t) {
+    int64_t lo = ebo_read_index(offsets, index_type, (int64_t)t * B);
+    int64_t hi = ebo_read_index(offsets, index_type, (int64_t)(t + 1) * B);
+    for (int64_t i = lo; i < hi; ++i) {
+      int64_t r = ebo_read_index(indices, index_type, i);
+      if (r < 0 || r >= tables[t].num_rows) return EBO_ERR_INDEX_OOB;
+    }
+  }
+
+  int nthreads = 1;
+#ifdef _OPENMP
+  nthreads = num_threads > 0 ? num_threads : omp_get_max_threads();
+#endif
+  (void)nthreads;
+  int64_t doff = 0, state_base = 0;
+  for (int32_t t = 0; t < num_tables; ++t) {
+    const ebo_table *tb = &tables[t];
+    const int32_t D = tb->dim;
+    int64_t lo = ebo_read_index(offsets, index_type, (int64_t)t * B);
+    int64_t hi = ebo_read_index(offsets, index_type, (int64_t)(t + 1) * B);
+    int64_t n = hi - lo;
+    ebo_row_report *rep = reports ? &reports[t] : NULL;
+    if (rep) rep->num_rows = 0;
+    if (tb->data && n > 0) {
+      /* every occurrence of table t: (row, position, bag), sorted by row then position */
+      ebo_occ *occ = (ebo_occ *)malloc(sizeof(ebo_occ) * (size_t)n);
+      if (!occ) return EBO_ERR_INVALID_ARG;
+      int64_t k = 0;
+      for (int64_t g = (int64_t)t * B; g < (int64_t)(t + 1) * B; ++g)
+        for (int64_t i = ebo_read_index(offsets, index_type, g);
+             i < ebo_read_index(offsets, index_type, g + 1); ++i) {
+          occ[k].row = ebo_read_index(indices, index_type, i);
+          occ[k].pos = i;
+          occ[k].bag = g;
+          ++k;
+        }
+      qsort(occ, (size_t)n, sizeof(ebo_occ), ebo_occ_cmp);
+      /* run starts */
+      int64_t *starts = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n + 1));
+      int64_t nruns = 0;
+      for (int64_t j = 0; j < n; ++j)
+        if (j == 0 || occ[j].row != occ[j - 1].row) starts[nruns++] = j;
+      starts[nruns] = n;
+      if (rep) rep->num_rows = nruns;
+#pragma omp parallel for schedule(dynamic, 64) num_threads(nthreads)
+      for (int64_t u = 0; u < nruns; ++u) {
+        const int64_t row = occ[starts[u]].row;
+        unsigned char *w = (unsigned char *)tb->data + (size_t)row * (size_t)tb->row_stride_bytes;
+        double *G = (double *)malloc(sizeof(double) * (size_t)D);
+        double *S = (double *)malloc(sizeof(double) * (size_t)D);
+        for (int32_t d = 0; d < D; ++d) {
+          double acc = 0.0, mag = 0.0;
+          for (int64_t j = starts[u]; j < starts[u + 1]; ++j) {
+            const ebo_occ *o = &occ[j];
+            double c = 1.0;
+            if (weights) c = (double)weights[o->pos];
+            if (mode == EBO_MODE_MEAN) {
+              int64_t L = ebo_read_index(offsets, index_type, o->bag + 1) -
+                          ebo_read_index(offsets, index_type, o->bag);
+              c = 1.0 / (double)L;
+            }
+            double term = c * (double)grad_out[(o->bag % B) * sum_d + doff + d];
+            acc += term;
+            mag += fabs(term);
+          }
+          G[d] = acc;
+          S[d] = mag;
+        }
+        double step = (double)lr;
+        if (opt == EBO_OPT_ROWWISE_ADAGRAD) {
+          double sq = 0.0;
+          for (int32_t d = 0; d < D; ++d) sq += G[d] * G[d];
+          double s_new = (double)state[state_base + row] + sq / (double)D;
+          state[state_base + row] = (float)s_new;
+          step = (double)lr / (sqrt(s_new) + (double)eps);
+        }
+        for (int32_t d = 0; d < D; ++d) {
+          if (tb->dtype == EBO_ROW_F32) {
+            float v;
+            memcpy(&v, w + 4 * (size_t)d, 4);
+            v = (float)((double)v - step * G[d]);
+            memcpy(w + 4 * (size_t)d, &v, 4);
+          } else {
+            uint16_t h;
+            memcpy(&h, w + 2 * (size_t)d, 2);
+            h = ebo_double_to_half(ebo_half_to_double(h) - step * G[d]);
+            memcpy(w + 2 * (size_t)d, &h, 2);
+          }
+        }
+        if (rep && rep->rows) {
+          rep->rows[u] = row;
+          rep->count[u] = starts[u + 1] - starts[u];
+          for (int32_t d = 0; d < D; ++d) {
+            rep->grad[u * D + d] = G[d];
+            rep->scale[u * D + d] = S[d];
+          }
+        }
+        free(G);
+        free(S);
+      }
+      free(starts);
+      free(occ);
+    }
+    doff += D;
+    state_base += tb->num_rows;
+  }
+  return EBO_OK;
+}

@@ -76,6 +76,14 @@ def _load():
         lib.ebo_half_to_double.argtypes = [ctypes.c_uint16]
         lib.ebo_max_threads.restype = ctypes.c_int
         lib.ebo_max_threads.argtypes = []
+        lib.ebo_double_to_half.restype = ctypes.c_uint16
+        lib.ebo_double_to_half.argtypes = [ctypes.c_double]
+        lib.ebo_backward_update.restype = ctypes.c_int
+        lib.ebo_backward_update.argtypes = [
+            ctypes.POINTER(_CTable), ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+            ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+            ctypes.c_float, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+        ]
         _lib = lib
     return _lib
 
@@ -166,3 +174,92 @@ def ebo_forward(
     if rc != 0:
         raise OracleError(rc)
     return (out, absum) if with_absum else out
+
+
+class _CReport(ctypes.Structure):
+    _fields_ = [
+        ("rows", ctypes.c_void_p),
+        ("grad", ctypes.c_void_p),
+        ("scale", ctypes.c_void_p),
+        ("count", ctypes.c_void_p),
+        ("num_rows", ctypes.c_int64),
+    ]
+
+
+_OPT_CODES = {"sgd": 0, "rowwise_adagrad": 1}
+
+
+def double_to_half(x: float) -> int:
+    """The oracle's fp64 -> binary16 rounding (exposed so tests can pin it)."""
+    return int(_load().ebo_double_to_half(float(x)))
+
+
+def ebo_backward_update(
+    tables: Sequence[OracleTable],
+    indices: np.ndarray,
+    offsets: np.ndarray,
+    weights: Optional[np.ndarray],
+    pooling: str,
+    grad_out: np.ndarray,
+    optimizer: str = "sgd",
+    lr: float = 0.01,
+    eps: float = 1e-8,
+    state: Optional[np.ndarray] = None,
+    report=(),
+    num_threads: int = 0,
+):
+    """Backward of the pooled lookup plus the fused optimizer step, in place.
+
+    Updates each table's rows (tables whose rows are None are skipped) and,
+    for row-wise Adagrad, `state` (fp32 [sum_t R_t]).  `report` lists tables
+    whose touched rows to return as {t: (rows, grad, scale, count)}.
+    """
+    lib = _load()
+    offsets = np.ascontiguousarray(offsets)
+    indices = np.ascontiguousarray(indices)
+    itype = 1 if offsets.dtype == np.int64 else 0
+    if indices.dtype != offsets.dtype:
+        raise TypeError("indices and offsets must share a dtype")
+    grad_out = np.ascontiguousarray(grad_out, dtype=np.float32)
+    T = len(tables)
+    ct = (_CTable * T)()
+    for i, tb in enumerate(tables):
+        if tb.rows is not None:
+            if not tb.rows.flags["C_CONTIGUOUS"] or not tb.rows.flags["WRITEABLE"]:
+                raise ValueError("table rows must be C-contiguous and writable")
+            ct[i].data = tb.rows.ctypes.data
+            ct[i].num_rows = tb.rows.shape[0]
+            ct[i].row_stride_bytes = tb.rows.strides[0]
+        else:
+            ct[i].data = None
+            ct[i].num_rows = int(tb.num_rows)
+        ct[i].dim = int(tb.dim)
+        ct[i].dtype = _ROW_CODES[tb.dtype]
+    B = (offsets.size - 1) // T
+    lens = [int(offsets[(t + 1) * B] - offsets[t * B]) for t in range(T)]
+    reps = (_CReport * T)()
+    keep = {}
+    for t in report:
+        n = max(lens[t], 1)
+        D = int(tables[t].dim)
+        arrs = (np.zeros(n, np.int64), np.zeros((n, D), np.float64), np.zeros((n, D), np.float64),
+                np.zeros(n, np.int64))
+        keep[t] = arrs
+        reps[t].rows, reps[t].grad, reps[t].scale, reps[t].count = [a.ctypes.data for a in arrs]
+    if weights is not None:
+        weights = np.ascontiguousarray(weights, dtype=np.float32)
+    if state is not None:
+        assert state.dtype == np.float32 and state.flags["C_CONTIGUOUS"]
+    rc = lib.ebo_backward_update(
+        ct, T, indices.ctypes.data if indices.size else None, offsets.ctypes.data, itype, indices.size,
+        offsets.size, weights.ctypes.data if weights is not None else None, _MODE_CODES[pooling],
+        grad_out.ctypes.data, _OPT_CODES[optimizer], float(lr), float(eps),
+        state.ctypes.data if state is not None else None, reps, int(num_threads),
+    )
+    if rc != 0:
+        raise OracleError(rc)
+    out = {}
+    for t, (rows, g, s, c) in keep.items():
+        n = int(reps[t].num_rows)
+        out[t] = (rows[:n], g[:n], s[:n], c[:n])
+    return out

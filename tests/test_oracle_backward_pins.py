@@ -1,0 +1,178 @@
+"""Pins for the oracle's backward with a fused row-wise optimizer update.
+
+The gradient of the pooled lookup with respect to table t is A_t^T grad_out_t,
+where A_t[b, r] sums the coefficients (1, w_i or 1/L) of the occurrences of
+row r in bag (t, b).  The oracle is pinned by hand-worked cases with exact
+results, a dense A_t^T grad_out product in numpy, invariants, the fp64 ->
+fp16 rounding against numpy, and its error codes.
+"""
+import numpy as np
+import pytest
+
+from conftest import oracle_tables
+from oracle import OracleError, OracleTable, double_to_half, ebo_backward_update
+from paper_2609_30656_amd.workload import make_workload
+
+W4 = np.array([[1, 2], [3, 4], [5, 6], [7, 8]], dtype=np.float32)
+IDX = np.array([2, 0, 3, 3], dtype=np.int64)
+OFF = np.array([0, 2, 2, 4], dtype=np.int64)  # bags {2,0}, {}, {3,3}
+GRAD = np.array([[1, 2], [3, 4], [5, 6]], dtype=np.float32)
+
+
+def _t(rows, dtype="f32"):
+    return OracleTable(np.array(rows, copy=True), rows.shape[1], dtype)
+
+
+def test_worked_sgd_sum():
+    t = _t(W4)
+    rep = ebo_backward_update([t], IDX, OFF, None, "sum", GRAD, "sgd", lr=0.5, report=[0])
+    # G(row0) = g[b0] = [1,2]; G(row2) = [1,2]; G(row3) = 2*g[b2] = [10,12]; row 1 untouched
+    np.testing.assert_array_equal(t.rows, [[0.5, 1], [3, 4], [4.5, 5], [2, 2]])
+    rows, g, s, c = rep[0]
+    np.testing.assert_array_equal(rows, [0, 2, 3])
+    np.testing.assert_array_equal(g, [[1, 2], [1, 2], [10, 12]])
+    np.testing.assert_array_equal(c, [1, 1, 2])
+
+
+def test_worked_sgd_mean_and_weighted():
+    t = _t(W4)
+    ebo_backward_update([t], IDX, OFF, None, "mean", GRAD, "sgd", lr=1.0)
+    # mean: c = 1/2 in bags 0 and 2 -> G0 = G2 = [0.5, 1], G3 = 2 * 0.5 * [5,6]
+    np.testing.assert_array_equal(t.rows, [[0.5, 1], [3, 4], [4.5, 5], [2, 2]])
+    t = _t(W4)
+    w = np.array([0.5, 2, 1, 0.25], np.float32)
+    ebo_backward_update([t], IDX, OFF, w, "sum", GRAD, "sgd", lr=1.0)
+    # G2 = 0.5*[1,2], G0 = 2*[1,2], G3 = (1 + 0.25)*[5,6]
+    np.testing.assert_array_equal(t.rows, [[1 - 2, 2 - 4], [3, 4], [4.5, 5], [7 - 6.25, 8 - 7.5]])
+
+
+def test_worked_rowwise_adagrad():
+    # row 0 alone in bag 0 with g = [1, 7]: mean(G^2) = (1 + 49) / 2 = 25;
+    # state 11 -> 36, sqrt = 6; lr = 6, eps = 0 -> W0 - G exactly
+    t = _t(W4)
+    grad = np.array([[1, 7], [0, 0]], np.float32)
+    state = np.array([11, 5, 0, 0], np.float32)
+    ebo_backward_update([t], np.array([0], np.int64), np.array([0, 1, 1], np.int64), None, "sum", grad,
+                        "rowwise_adagrad", lr=6.0, eps=0.0, state=state)
+    np.testing.assert_array_equal(t.rows, [[0, -5], [3, 4], [5, 6], [7, 8]])
+    np.testing.assert_array_equal(state, [36, 5, 0, 0])  # untouched rows keep their state
+
+
+def test_worked_two_tables_and_fp16():
+    w16 = np.array([[1, 2, 3, 4, 5, 6, 7, 8], [0.5] * 8], np.float16)
+    t0, t1 = _t(W4), _t(w16, "f16")
+    idx = np.array([1, 0, 1], np.int64)
+    off = np.array([0, 1, 3], np.int64)  # T = 2, B = 1: table 0 bag {1}; table 1 bag {0, 1}
+    grad = np.array([[2, 4, 1, 1, 1, 1, 1, 1, 1, 1]], np.float32)  # [B=1, 2 + 8]
+    ebo_backward_update([t0, t1], idx, off, None, "sum", grad, "sgd", lr=0.25)
+    np.testing.assert_array_equal(t0.rows, [[1, 2], [2.5, 3], [5, 6], [7, 8]])
+    np.testing.assert_array_equal(t1.rows.astype(np.float32), [[0.75, 1.75, 2.75, 3.75, 4.75, 5.75, 6.75, 7.75],
+                                                               [0.25] * 8])
+
+
+def _dense_grad(tables, idx, off, w, pooling, grad):
+    T = len(tables)
+    B = (off.size - 1) // T
+    out, col = [], 0
+    for t, tb in enumerate(tables):
+        R, D = tb.rows.shape[0], tb.dim
+        A = np.zeros((B, R), np.float64)
+        for b in range(B):
+            g = t * B + b
+            L = off[g + 1] - off[g]
+            for i in range(off[g], off[g + 1]):
+                c = 1.0 if w is None else float(w[i])
+                if pooling == "mean":
+                    c = 1.0 / L
+                A[b, idx[i]] += c
+        G = A.T @ grad[:, col:col + D].astype(np.float64)
+        out.append((G, np.count_nonzero(A, axis=0) > 0, np.abs(A).T @ np.abs(grad[:, col:col + D])))
+        col += D
+    return out
+
+
+@pytest.mark.parametrize("name", ["c2", "c3a", "c3b", "c4"])
+def test_brute_force_dense_transpose(name):
+    w = make_workload(name, "cpu", rows_cap=300, batch=16, num_tables=3)
+    tabs = oracle_tables(w)
+    old = [t.rows.copy() for t in tabs]
+    rng = np.random.default_rng(3)
+    grad = rng.standard_normal((w.batch, w.sum_dim)).astype(np.float32)
+    idx, off = w.indices.numpy(), w.offsets.numpy()
+    wt = None if w.weights is None else w.weights.numpy()
+    lr = 0.125
+    rep = ebo_backward_update(tabs, idx, off, wt, w.pooling, grad, "sgd", lr=lr, report=range(3))
+    for t, (G, touched, S) in enumerate(_dense_grad(tabs, idx, off, wt, w.pooling, grad)):
+        rows, g, s, c = rep[t]
+        np.testing.assert_array_equal(rows, np.nonzero(touched)[0])
+        np.testing.assert_allclose(g, G[rows], rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(s, S[rows], rtol=1e-12, atol=0)
+        expect = old[t].astype(np.float64)
+        expect[rows] -= lr * G[rows]
+        expect = expect.astype(old[t].dtype)  # one rounding to the storage type
+        if tabs[t].dtype == "f32":
+            assert np.array_equal(tabs[t].rows.view(np.uint32), expect.view(np.uint32))
+        else:
+            # G is summed in a different order by numpy: allow the rare tie
+            diff = np.abs(tabs[t].rows.view(np.uint16).astype(np.int32) - expect.view(np.uint16).astype(np.int32))
+            assert diff.max() <= 1 and (diff == 0).mean() > 0.999
+
+
+def test_zero_learning_rate_leaves_tables_alone():
+    w = make_workload("c3b", "cpu", rows_cap=200, batch=8, num_tables=2)
+    tabs = oracle_tables(w)
+    old = [t.rows.copy() for t in tabs]
+    grad = np.ones((w.batch, w.sum_dim), np.float32)
+    ebo_backward_update(tabs, w.indices.numpy(), w.offsets.numpy(), w.weights.numpy(), "sum", grad, "sgd", lr=0.0)
+    for a, b in zip(tabs, old):
+        assert np.array_equal(a.rows.view(np.uint16), b.view(np.uint16))
+
+
+def test_adagrad_matches_closed_form():
+    w = make_workload("c2", "cpu", rows_cap=100, batch=8, num_tables=2)
+    tabs = oracle_tables(w)
+    old = [t.rows.copy() for t in tabs]
+    R = [t.rows.shape[0] for t in tabs]
+    state = np.abs(np.random.default_rng(4).standard_normal(sum(R))).astype(np.float32)
+    st0 = state.copy()
+    grad = np.random.default_rng(5).standard_normal((w.batch, w.sum_dim)).astype(np.float32)
+    rep = ebo_backward_update(tabs, w.indices.numpy(), w.offsets.numpy(), None, "sum", grad, "rowwise_adagrad",
+                              lr=0.05, eps=1e-3, state=state, report=range(2))
+    base = 0
+    for t in range(2):
+        rows, g, _, _ = rep[t]
+        s_new = st0[base + rows].astype(np.float64) + (g * g).mean(axis=1)
+        np.testing.assert_allclose(state[base + rows], s_new, rtol=1e-7)
+        untouched = np.setdiff1d(np.arange(R[t]), rows)
+        assert np.array_equal(state[base + untouched], st0[base + untouched])
+        expect = old[t][rows].astype(np.float64) - 0.05 * g / (np.sqrt(s_new)[:, None] + 1e-3)
+        np.testing.assert_allclose(tabs[t].rows[rows], expect.astype(np.float32), rtol=1e-6, atol=1e-9)
+        base += R[t]
+
+
+def test_double_to_half_against_numpy():
+    rng = np.random.default_rng(6)
+    xs = np.concatenate([
+        rng.standard_normal(20000) * 10.0 ** rng.integers(-9, 5, 20000),
+        # exact ties between neighbouring halves, subnormals, the overflow edge
+        (np.arange(-2048, 2048) + 0.5) * 2.0 ** -24,
+        (np.arange(1024, 2048) + 0.5) * 2.0 ** -10,
+        [0.0, -0.0, 65504.0, 65519.99, 65520.0, -65520.0, 1e9, 2.0 ** -25, 2.0 ** -26, 3 * 2.0 ** -26],
+    ])
+    got = np.array([double_to_half(x) for x in xs], np.uint16)
+    with np.errstate(over="ignore"):
+        ref = xs.astype(np.float16).view(np.uint16)
+    assert np.array_equal(got, ref)
+
+
+def test_backward_error_codes():
+    t8 = OracleTable(np.zeros((4, 20), np.uint8), 16, "int8_rowwise")
+    with pytest.raises(OracleError) as e:
+        ebo_backward_update([t8], IDX, OFF, None, "sum", np.zeros((3, 16), np.float32))
+    assert e.value.code == -2
+    with pytest.raises(OracleError) as e:
+        ebo_backward_update([_t(W4)], IDX, OFF, None, "sum", GRAD, "rowwise_adagrad", state=None)
+    assert e.value.code == -1
+    with pytest.raises(OracleError) as e:
+        ebo_backward_update([_t(W4)], np.array([2, 0, 9, 3], np.int64), OFF, None, "sum", GRAD)
+    assert e.value.code == -5
