@@ -31,12 +31,16 @@ PEAK_HBM_GBS = 8000.0
 METRIC = "EmbeddingBag fwd achieved HBM GB/s (% of peak) + pooled lookups/sec, 1 GPU"
 KERNEL_NAME = "eb_pool_kernel"
 SAMPLE = 7
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_30656_amd", "csrc", "eb.hip")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_30656_amd", "csrc", f) for f in ("eb_device.h", "eb_forward.hip")]
 
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the sources the forward kernel is built from."""
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def counter_traffic(config: str, index_law: str):

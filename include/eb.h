@@ -55,7 +55,9 @@
  * count is chosen per call from the number of bags.  EB_XCD_REMAP=0|1, read
  * at the same time, forces how workgroups map onto the GPU's XCDs (default:
  * XCD-contiguous for handles of up to 32 tables, round-robin otherwise).
- * Results do not depend on either.
+ * EB_BWD_TILE_CHUNKS=c (1..16) fixes the backward's tiles at 64*c sorted
+ * positions (default: 64 to 256, from the number of lookups).  Results do not
+ * depend on any of these.
  */
 #ifndef EB_H_
 #define EB_H_
@@ -165,6 +167,55 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables,
 eb_status eb_forward(const eb_tables *tables, eb_tensor indices,
                      eb_tensor offsets, eb_tensor per_sample_weights,
                      eb_pooling pooling, eb_tensor out);
+
+/*
+ * Training: backward of eb_forward with a fused row-wise optimizer update.
+ *
+ * The paper profiles each submodule's forward and backward pass (Sec. III-A).
+ * For the pooled lookup the gradient of row r of table t is
+ *   G[d] = sum over positions i of table t with indices[i] = r of
+ *          c_i * grad_out[b(i), Doff[t] + d],
+ * c_i = 1 (sum), w_i (weighted sum) or 1/|I_g| (mean), and the rows that
+ * occur in the batch are updated in place (the others are left alone):
+ *   EB_OPT_SGD:              W[r] -= lr * G
+ *   EB_OPT_ROWWISE_ADAGRAD:  s[r] += (1/D) sum_d G[d]^2;
+ *                            W[r] -= lr * G / (sqrt(s[r]) + eps)
+ * computed in fp32 and rounded once to the table's storage type.  The result
+ * does not depend on thread scheduling (no floating-point atomics).
+ */
+typedef enum { EB_OPT_SGD = 0, EB_OPT_ROWWISE_ADAGRAD = 1 } eb_optimizer;
+
+/*
+ * Device workspace (bytes) eb_backward_update needs for num_indices lookups
+ * on this handle (about 17 bytes per lookup plus per-tile partial sums and
+ * the sort's scratch).  Synchronous, host only.
+ */
+eb_status eb_backward_workspace_size(const eb_tables *tables, int64_t num_indices, size_t *bytes);
+
+/*
+ * indices, offsets, per_sample_weights, pooling: as for eb_forward (the batch
+ * whose output gradient is grad_out).
+ *   grad_out:        EB_T_F32 [B * sum_t D_t], 16-byte aligned, row-major
+ *                    [B, sum_t D_t] (the gradient of eb_forward's out).
+ *   optimizer:       eb_optimizer; learning_rate, eps as above (eps unused by
+ *                    SGD).
+ *   optimizer_state: EB_OPT_ROWWISE_ADAGRAD: EB_T_F32 [sum_t R_t], table t's
+ *                    rows starting at sum_{s<t} R_s, updated in place;
+ *                    ignored by SGD (data may be NULL).
+ *   workspace:       device memory of at least eb_backward_workspace_size()
+ *                    bytes, 256-byte aligned, owned by the caller; its
+ *                    contents are scratch.
+ * The tables' rows (the descriptors' data) are written in place.  Only fp32
+ * and fp16 tables with dim <= 256 train (else EB_ERR_UNSUPPORTED), and the
+ * handle's total row count plus its table count must stay below 2^32.
+ * Asynchronous on the handle's stream (checked mode as for eb_forward);
+ * allocates nothing.  Forwards and backwards on one handle are ordered by
+ * the stream; two backwards that update the same rows must not overlap.
+ */
+eb_status eb_backward_update(const eb_tables *tables, eb_tensor indices, eb_tensor offsets,
+                             eb_tensor per_sample_weights, eb_pooling pooling, eb_tensor grad_out,
+                             int32_t optimizer, float learning_rate, float eps,
+                             eb_tensor optimizer_state, void *workspace, size_t workspace_bytes);
 
 /* Release a handle (synchronises its stream first).  NULL is a no-op. */
 eb_status eb_destroy(eb_tables *tables);

@@ -1,0 +1,635 @@
+// eb_backward.hip — backward of the pooled EmbeddingBag lookup with a fused
+// row-wise optimizer update, for the AMD Instinct MI355X (gfx950).
+//
+// The paper's component benchmark profiles each submodule's forward and
+// backward pass (Sec. III-A).  For sparse_arch (Sec. IV-A.2) the backward
+// turns the gradient of the pooled output embeddings into a gradient for
+// every table row that was read, and a sparse optimizer updates those rows.
+// For row r of table t, with c_i = 1, w_i or 1/L (sum, weighted sum, mean):
+//
+//   G[d] = sum over positions i of table t with idx_i = r of
+//          c_i * grad_out[b(i), Doff[t] + d]
+//   SGD:               W[r] -= lr * G
+//   row-wise Adagrad:  s[r] += mean_d G[d]^2;  W[r] -= lr * G / (sqrt(s[r]) + eps)
+//
+// Computed without atomics on data, and deterministically:
+//   1. every position gets a 32-bit sort key (the table's key base + row) and
+//      its bag id;
+//   2. (key, position) pairs are radix-sorted (rocPRIM): each row's
+//      occurrences become one run, in position order, and each table's
+//      positions stay inside that table's range of the sorted array;
+//   3. each table's sorted range is cut into tiles of 64..256 positions; a
+//      wavefront walks its tile's runs, pools each run's gradient rows with the
+//      forward's 16-byte-slice gather and reduce-scatter (the gradient is an
+//      fp32 "table" of B rows), and updates the run's table row; a run that
+//      crosses a tile boundary leaves a partial sum in a per-tile slot;
+//   4. a fix-up pass sums each crossing run's partials in tile order and
+//      updates its row.
+// Long runs (the hottest rows of a Zipf workload appear tens of thousands of
+// times per batch) are thereby spread over as many wavefronts as they have
+// tiles, and no wavefront waits for another.
+
+#include <rocprim/device/device_radix_sort.hpp>
+#include <rocprim/iterator/counting_iterator.hpp>
+
+#include "eb_device.h"
+
+namespace eb {
+namespace {
+
+constexpr uint32_t kNoKey = 0xFFFFFFFFu;  // larger than any key (keys fit below it)
+constexpr uint8_t kTileContinues = 1;      // the tile's last run goes on into the next tile
+constexpr uint8_t kTileOwnsRun = 2;        // ... and started in this tile: this tile finishes it
+constexpr int kOptRowwiseAdagrad = 1;
+
+struct BwdArgs {
+  const TableMeta *meta;
+  GatherCtx ctx;
+  const void *indices;
+  const void *offsets;
+  const float *weights;
+  const float *grad;      // grad_out [B, sum D]
+  float *state;           // row-wise Adagrad state [sum R]
+  uint32_t *keys;         // [N] sort keys by position
+  int32_t *bag_of;        // [N] bag id by position
+  const uint32_t *skeys;  // [N] sorted keys
+  const uint32_t *spos;   // [N] positions in sorted order
+  int32_t *tile_start;    // [T + 1] first tile of each table; [T] = number of tiles
+  uint8_t *tile_flags;    // [tiles] kTileContinues | kTileOwnsRun
+  float *carry;           // [2 * tiles * max_dim]: slot 2w = head run partial, 2w+1 = tail run partial
+  int64_t num_indices;
+  int64_t grad_ld;        // sum D
+  int32_t num_bags;
+  int32_t batch;
+  int32_t num_tables;
+  int32_t idx64;
+  int32_t coef;           // 0: c = 1, 1: c = w_i, 2: c = 1 / L
+  int32_t opt;
+  float lr;
+  float eps;
+  int32_t tile_size;      // positions per tile (multiple of 64)
+  int32_t max_dim;
+  int32_t bags_per_wave;  // keys kernel: bags per wavefront
+  int32_t groups_per_table;
+  int32_t num_waves;
+};
+
+__device__ __forceinline__ int64_t load_offset(const BwdArgs &a, int64_t g) {
+  return a.idx64 ? static_cast<const int64_t *>(a.offsets)[g] : (int64_t) static_cast<const int32_t *>(a.offsets)[g];
+}
+
+__device__ __forceinline__ int64_t clamp_pos(int64_t p, int64_t lo, int64_t hi) {
+  return p < lo ? lo : (p > hi ? hi : p);
+}
+
+// Step 1: sort key and bag id of every position.  A wavefront takes a run of
+// consecutive bags of one table and walks their positions 64 at a time (the
+// same work map as the forward).  An index outside its table gets the table's
+// sentinel key (one past its last row), which sorts after the table's rows
+// and is skipped later.
+__global__ __launch_bounds__(kBlock) void eb_bwd_keys_kernel(BwdArgs a) {
+  const int32_t wid = (int32_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  if (wid >= a.num_waves) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t t = wid / a.groups_per_table;
+  const int32_t b0 = (wid - t * a.groups_per_table) * a.bags_per_wave;
+  const int nb = (a.batch - b0) < a.bags_per_wave ? (a.batch - b0) : a.bags_per_wave;
+  const int32_t g0 = t * a.batch + b0;
+  const TableMeta m = a.meta[t];
+  const int64_t N = a.num_indices;
+
+  int64_t raw = 0;
+  if (lane <= nb) raw = load_offset(a, g0 + lane);
+  // report a broken partition (checked mode); positions are clamped into [0, N)
+  const int64_t nxt = __shfl_down(raw, 1);
+  bool bad = lane < nb && (raw < 0 || nxt < raw || nxt > N);
+  bad |= lane == 0 && g0 == 0 && raw != 0;
+  bad |= lane == nb && g0 + nb == a.num_bags && raw != N;
+  if (__ballot(bad)) {
+    if (lane == 0) atomicOr(a.ctx.err, kErrOffsets);
+  }
+  const int64_t my_off = clamp_pos(raw, 0, N);
+  const int64_t P0 = readlane64(my_off, 0);
+  const int64_t P1 = readlane64(my_off, nb);
+  bool oob = false;
+  for (int64_t c = P0; c < P1; c += kWave) {
+    const int64_t p = c + lane;
+    if (p < P1) {
+      int j = 0;
+      for (int jj = 1; jj < nb; ++jj)
+        if (readlane64(my_off, jj) <= p) j = jj;
+      const int64_t r = a.idx64 ? __builtin_nontemporal_load(static_cast<const int64_t *>(a.indices) + p)
+                                : (int64_t)__builtin_nontemporal_load(static_cast<const int32_t *>(a.indices) + p);
+      const bool ok = r >= 0 && r < m.num_rows;
+      oob |= !ok;
+      a.keys[p] = m.key_base + (ok ? (uint32_t)r : (uint32_t)m.num_rows);
+      a.bag_of[p] = g0 + j;
+    }
+  }
+  if (__ballot(oob)) {
+    if (lane == 0) atomicOr(a.ctx.err, kErrIndex);
+  }
+}
+
+// tiles of table t (its clamped position range cut into tile_size pieces)
+__device__ __forceinline__ void table_range(const BwdArgs &a, int32_t t, int64_t &p0, int64_t &p1) {
+  p0 = clamp_pos(load_offset(a, (int64_t)t * a.batch), 0, a.num_indices);
+  p1 = clamp_pos(load_offset(a, (int64_t)(t + 1) * a.batch), p0, a.num_indices);
+}
+
+// Step 3a: first tile of every table (one workgroup; exclusive scan over tables).
+__global__ __launch_bounds__(1024) void eb_bwd_tile_start_kernel(BwdArgs a) {
+  __shared__ int64_t part[1024];
+  const int T = a.num_tables;
+  const int tid = threadIdx.x;
+  const int per = (T + 1023) / 1024;
+  const int t0 = tid * per < T ? tid * per : T;
+  const int t1 = t0 + per < T ? t0 + per : T;
+  int64_t sum = 0;
+  for (int t = t0; t < t1; ++t) {
+    int64_t p0, p1;
+    table_range(a, t, p0, p1);
+    sum += (p1 - p0 + a.tile_size - 1) / a.tile_size;
+  }
+  part[tid] = sum;
+  __syncthreads();
+  if (tid == 0) {
+    int64_t run = 0;
+    for (int i = 0; i < 1024; ++i) {
+      const int64_t v = part[i];
+      part[i] = run;
+      run += v;
+    }
+    a.tile_start[T] = (int32_t)run;
+  }
+  __syncthreads();
+  int64_t run = part[tid];
+  for (int t = t0; t < t1; ++t) {
+    a.tile_start[t] = (int32_t)run;
+    int64_t p0, p1;
+    table_range(a, t, p0, p1);
+    run += (p1 - p0 + a.tile_size - 1) / a.tile_size;
+  }
+}
+
+// table owning tile w: the last table whose first tile is <= w (empty tables
+// own no tile and are skipped)
+__device__ __forceinline__ int32_t table_of_tile(const BwdArgs &a, int32_t w) {
+  int32_t lo = 0, hi = a.num_tables - 1;
+  while (lo < hi) {
+    const int32_t mid = (lo + hi + 1) / 2;
+    if (a.tile_start[mid] <= w) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Sum of x over the 64 lanes (fixed butterfly order).
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+// Optimizer step on row `row` of table m.  Lane holds K gradient values for
+// columns [col, col + K) when `own`; the columns of all owning lanes cover
+// the row exactly once.
+template <int TDT, int K>
+__device__ __forceinline__ void apply_update(const TableMeta &m, const BwdArgs &a, int64_t row, const float (&g)[K],
+                                             bool own, int col) {
+  float scale = a.lr;
+  if (a.opt == kOptRowwiseAdagrad) {
+    float sq = 0.0f;
+    if (own) {
+#pragma unroll
+      for (int i = 0; i < K; ++i) sq = fmaf(g[i], g[i], sq);
+    }
+    sq = wave_sum(sq);
+    float *sp = a.state + m.state_base + row;
+    const float s_new = *sp + sq / (float)m.dim;
+    scale = a.lr / (sqrtf(s_new) + a.eps);
+    if ((threadIdx.x & (kWave - 1)) == 0) *sp = s_new;
+  }
+  if (own) {
+    unsigned char *base = const_cast<unsigned char *>(m.data) + (uint64_t)row * m.row_stride;
+    if constexpr (TDT == kF32) {
+      float *wp = reinterpret_cast<float *>(base) + col;
+#pragma unroll
+      for (int i = 0; i < K; ++i) wp[i] = fmaf(-scale, g[i], wp[i]);
+    } else {
+      _Float16 *wp = reinterpret_cast<_Float16 *>(base) + col;
+#pragma unroll
+      for (int i = 0; i < K; ++i) wp[i] = (_Float16)fmaf(-scale, g[i], (float)wp[i]);
+    }
+  }
+}
+
+// Step 3b: pool the runs of one tile and update their rows (or leave
+// partials).  LPR lanes hold one fp32 gradient row of 4*dim bytes.
+template <int TDT, int LPR>
+__device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, int32_t t, int32_t w, int32_t k) {
+  using R = Reduce<kF32, LPR>;
+  constexpr int KEEP = R::KEEP;
+  const int lane = threadIdx.x & (kWave - 1);
+  int64_t p0, p1;
+  table_range(a, t, p0, p1);
+  const int64_t s = p0 + (int64_t)k * a.tile_size;
+  const int64_t e = s + a.tile_size < p1 ? s + a.tile_size : p1;
+  if (s >= e) return;
+  const uint32_t before = s > p0 ? a.skeys[s - 1] : kNoKey;
+  const uint32_t after = e < p1 ? a.skeys[e] : kNoKey;
+  const uint32_t key_last = a.skeys[e - 1];
+  const uint32_t kmin = m.key_base, sentinel = m.key_base + (uint32_t)m.num_rows;
+  if (lane == 0) {
+    const bool cont = after != kNoKey && after == key_last;
+    const bool owns = cont && key_last != before && key_last < sentinel && key_last >= kmin;
+    a.tile_flags[w] = (uint8_t)((cont ? kTileContinues : 0) | (owns ? kTileOwnsRun : 0));
+  }
+
+  // the gradient rows of this table as an fp32 table of B rows
+  TableMeta gm = m;
+  gm.data = reinterpret_cast<const unsigned char *>(a.grad + m.out_col);
+  gm.row_stride = (uint32_t)(a.grad_ld * 4);
+  gm.num_rows = a.batch;
+  gm.code_bytes = 4 * m.dim;
+  const int colb = (lane % LPR) * 16;
+  const bool colok = colb < gm.code_bytes;
+  const int col = colb / 4 + R::first_value(lane);
+  const bool own = R::stores(lane) && colok;
+
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  bool first_run = true;
+  // Finish the run with key rkey whose terms are all in acc: update its row,
+  // or leave a partial when it crosses a tile boundary.
+  auto finish = [&](uint32_t rkey, bool reaches_end) {
+    const bool valid = rkey >= kmin && rkey < sentinel;
+    const bool started_before = first_run && rkey == before;
+    const bool continues_after = reaches_end && rkey == after;
+    if (valid) {
+      R::run(acc);
+      float gk[KEEP];
+#pragma unroll
+      for (int i = 0; i < KEEP; ++i) gk[i] = acc[i];
+      if (!started_before && !continues_after) {
+        apply_update<TDT, KEEP>(m, a, (int64_t)(rkey - kmin), gk, own, col);
+      } else if (own) {
+        float *slot = a.carry + ((int64_t)2 * w + (started_before ? 0 : 1)) * a.max_dim + col;
+#pragma unroll
+        for (int i = 0; i < KEEP; ++i) slot[i] = gk[i];
+      }
+    }
+    first_run = false;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = 0.0f;
+  };
+  bool pending = false;  // acc holds a run that reached the end of the previous chunk
+  uint32_t pending_key = kNoKey;
+  uint32_t prev_last = before;
+  for (int64_t c = s; c < e; c += kWave) {
+    const int n = (int)((e - c) < kWave ? (e - c) : kWave);
+    const bool last_chunk = c + kWave >= e;
+    uint32_t key = kNoKey;
+    Chunk ch;
+    ch.row = kBadRow;
+    ch.w = 0.0f;
+    ch.n = n;
+    if (lane < n) {
+      key = a.skeys[c + lane];
+      const uint32_t pos = a.spos[c + lane];
+      const int32_t g = a.bag_of[pos];
+      const int64_t b = (int64_t)g - (int64_t)t * a.batch;
+      if (key >= kmin && key < sentinel && b >= 0 && b < a.batch) {
+        ch.row = (uint32_t)b;
+        if (a.coef == 1) {
+          ch.w = a.weights[pos];
+        } else if (a.coef == 2) {
+          const int64_t L = load_offset(a, g + 1) - load_offset(a, g);
+          ch.w = L > 0 ? 1.0f / (float)L : 0.0f;
+        } else {
+          ch.w = 1.0f;
+        }
+      }
+    }
+    const uint32_t up = (uint32_t)__shfl_up((int)key, 1);
+    const uint32_t prev = lane == 0 ? prev_last : up;
+    const uint64_t heads = __ballot(lane < n && key != prev);
+    // a run that ended exactly at the previous chunk's end
+    if (pending && (heads & 1ull)) {
+      finish(pending_key, false);
+      pending = false;
+    }
+    int a0 = 0;
+    while (a0 < n) {
+      const uint64_t above = a0 + 1 < kWave ? heads & (~0ull << (a0 + 1)) : 0ull;
+      const int z = above ? (int)__builtin_ctzll(above) : n;
+      const uint32_t rkey = __builtin_amdgcn_readlane(key, a0);
+      gather_range<kF32, LPR, true>(gm, a.ctx, ch, a0, z - a0, acc, colb, colok);
+      if (z < n || last_chunk) {
+        finish(rkey, z == n);
+        pending = false;
+      } else {
+        pending = true;  // the run may go on in the next chunk
+        pending_key = rkey;
+      }
+      a0 = z;
+    }
+    prev_last = __builtin_amdgcn_readlane(key, n - 1);
+  }
+}
+
+#define EB_BWD_LPR(LOG2)                                                        \
+  case LOG2:                                                                    \
+    tile_body<TDT, (1 << (LOG2))>(a, m, t, w, w - a.tile_start[t]);             \
+    break;
+
+template <int TDT, int LOG2>
+__global__ __launch_bounds__(kBlock) void eb_bwd_tiles_kernel(BwdArgs a) {
+  const int32_t w = (int32_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  if (w >= a.tile_start[a.num_tables]) return;
+  const int32_t t = table_of_tile(a, w);
+  const TableMeta m = a.meta[t];
+  if (m.kind / 8 != TDT) return;
+  if constexpr (LOG2 >= 0) {
+    tile_body<TDT, (1 << LOG2)>(a, m, t, w, w - a.tile_start[t]);
+  } else {
+    switch (log2_lanes_per_row(4 * m.dim)) {
+      EB_BWD_LPR(0) EB_BWD_LPR(1) EB_BWD_LPR(2) EB_BWD_LPR(3) EB_BWD_LPR(4) EB_BWD_LPR(5) EB_BWD_LPR(6)
+      default:
+        break;
+    }
+  }
+}
+
+#undef EB_BWD_LPR
+
+// Step 4: a run that starts in tile w and goes on past it: sum its partial
+// from tile w and the head partials of the tiles it covers, in tile order,
+// then update its row.  Lane l handles columns [4l, 4l + 4).
+template <int TDT>
+__global__ __launch_bounds__(kBlock) void eb_bwd_fixup_kernel(BwdArgs a) {
+  const int32_t w = (int32_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int32_t total = a.tile_start[a.num_tables];
+  if (w >= total) return;
+  if (!(a.tile_flags[w] & kTileOwnsRun)) return;
+  const int32_t t = table_of_tile(a, w);
+  const TableMeta m = a.meta[t];
+  if (m.kind / 8 != TDT) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  int64_t p0, p1;
+  table_range(a, t, p0, p1);
+  const int32_t k0 = w - a.tile_start[t];
+  const int32_t ntiles = a.tile_start[t + 1] - a.tile_start[t];
+  auto tile_last = [&](int32_t kk) {
+    const int64_t e = p0 + (int64_t)(kk + 1) * a.tile_size;
+    return (e < p1 ? e : p1) - 1;
+  };
+  const uint32_t key = a.skeys[tile_last(k0)];
+  const int col = 4 * lane;
+  const bool own = col < m.dim;
+  float g[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (own) {
+    const float *slot = a.carry + ((int64_t)2 * w + 1) * a.max_dim + col;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) g[i] = slot[i];
+  }
+  for (int32_t kk = k0 + 1; kk < ntiles; ++kk) {
+    const int32_t wk = a.tile_start[t] + kk;
+    if (own) {
+      const float *slot = a.carry + ((int64_t)2 * wk) * a.max_dim + col;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) g[i] += slot[i];
+    }
+    // the run goes on past tile kk only if it fills that tile and the tile continues
+    if (!((a.tile_flags[wk] & kTileContinues) && a.skeys[tile_last(kk)] == key)) break;
+  }
+  apply_update<TDT, 4>(m, a, (int64_t)(key - m.key_base), g, own, col);
+}
+
+typedef void (*KernelFn)(BwdArgs);
+
+template <int TDT>
+KernelFn pick_tiles(int log2) {
+  switch (log2) {
+    case 0: return eb_bwd_tiles_kernel<TDT, 0>;
+    case 1: return eb_bwd_tiles_kernel<TDT, 1>;
+    case 2: return eb_bwd_tiles_kernel<TDT, 2>;
+    case 3: return eb_bwd_tiles_kernel<TDT, 3>;
+    case 4: return eb_bwd_tiles_kernel<TDT, 4>;
+    case 5: return eb_bwd_tiles_kernel<TDT, 5>;
+    case 6: return eb_bwd_tiles_kernel<TDT, 6>;
+    default: return eb_bwd_tiles_kernel<TDT, -1>;
+  }
+}
+
+// Workspace regions (each 256-byte aligned).
+struct BwdLayout {
+  size_t keys, skeys, spos, bag_of, tile_start, tile_flags, carry, sort_tmp, total;
+  size_t sort_bytes;
+  int64_t tiles_ub;
+  int32_t tile_size;
+};
+
+inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+// Bits the largest sort key of handle h needs.
+unsigned key_bits(const eb_tables *h) {
+  const TableMeta &last = h->h_meta[h->num_tables - 1];
+  const uint64_t max_key = (uint64_t)last.key_base + (uint64_t)last.num_rows;
+  unsigned bits = 1;
+  while (bits < 32 && (max_key >> bits) != 0) ++bits;
+  return bits;
+}
+
+eb_status layout(const eb_tables *h, int64_t n, BwdLayout *L) {
+  // Tiles of 64 positions keep short workloads spread over many wavefronts;
+  // large ones use up to 256 (fewer partial sums to carry).
+  int64_t chunks = n / (64 * 32768);
+  chunks = chunks < 1 ? 1 : (chunks > 4 ? 4 : chunks);
+  if (h->bwd_tile_chunks > 0) chunks = h->bwd_tile_chunks;
+  L->tile_size = (int32_t)(64 * chunks);
+  L->tiles_ub = (n + L->tile_size - 1) / L->tile_size + h->num_tables;
+  size_t sort_bytes = 0;
+  if (n > 0) {
+    hipError_t e = rocprim::radix_sort_pairs(nullptr, sort_bytes, static_cast<const uint32_t *>(nullptr),
+                                             static_cast<uint32_t *>(nullptr), rocprim::counting_iterator<uint32_t>(0),
+                                             static_cast<uint32_t *>(nullptr), (unsigned int)n, 0, key_bits(h),
+                                             h->stream);
+    if (e != hipSuccess) return EB_ERR_HIP;
+  }
+  L->sort_bytes = sort_bytes;
+  size_t off = 0;
+  L->keys = off;
+  off += align256(4 * (size_t)n);
+  L->skeys = off;
+  off += align256(4 * (size_t)n);
+  L->spos = off;
+  off += align256(4 * (size_t)n);
+  L->bag_of = off;
+  off += align256(4 * (size_t)n);
+  L->tile_start = off;
+  off += align256(4 * (size_t)(h->num_tables + 1));
+  L->tile_flags = off;
+  off += align256((size_t)L->tiles_ub);
+  L->carry = off;
+  off += align256(4 * (size_t)2 * L->tiles_ub * h->max_dim);
+  L->sort_tmp = off;
+  off += align256(sort_bytes);
+  L->total = off;
+  return EB_OK;
+}
+
+}  // namespace
+}  // namespace eb
+
+using namespace eb;
+
+extern "C" {
+
+eb_status eb_backward_workspace_size(const eb_tables *h, int64_t num_indices, size_t *bytes) {
+  if (!h || !bytes || num_indices < 0) return EB_ERR_INVALID_ARG;
+  if (num_indices > INT32_MAX) return EB_ERR_UNSUPPORTED;
+  BwdLayout L;
+  const eb_status st = layout(h, num_indices, &L);
+  if (st != EB_OK) return st;
+  *bytes = L.total;
+  return EB_OK;
+}
+
+eb_status eb_backward_update(const eb_tables *h, eb_tensor indices, eb_tensor offsets, eb_tensor per_sample_weights,
+                             eb_pooling pooling, eb_tensor grad_out, int32_t optimizer, float learning_rate,
+                             float eps, eb_tensor optimizer_state, void *workspace, size_t workspace_bytes) {
+  if (!h) return EB_ERR_INVALID_ARG;
+  if (!h->backward_ok) return EB_ERR_UNSUPPORTED;
+  if (indices.elem_type != EB_I32 && indices.elem_type != EB_I64) return EB_ERR_DTYPE;
+  if (offsets.elem_type != indices.elem_type) return EB_ERR_DTYPE;
+  if (grad_out.elem_type != EB_T_F32) return EB_ERR_DTYPE;
+  if (pooling != EB_POOL_SUM && pooling != EB_POOL_MEAN) return EB_ERR_INVALID_ARG;
+  if (optimizer != EB_OPT_SGD && optimizer != EB_OPT_ROWWISE_ADAGRAD) return EB_ERR_INVALID_ARG;
+  if (!offsets.data || !grad_out.data) return EB_ERR_INVALID_ARG;
+  if (indices.numel < 0 || (indices.numel > 0 && !indices.data)) return EB_ERR_INVALID_ARG;
+  if (indices.numel > INT32_MAX) return EB_ERR_UNSUPPORTED;
+  const bool weighted = per_sample_weights.data != nullptr;
+  if (weighted) {
+    if (per_sample_weights.elem_type != EB_T_F32) return EB_ERR_DTYPE;
+    if (pooling == EB_POOL_MEAN) return EB_ERR_INVALID_ARG;
+    if (per_sample_weights.numel != indices.numel) return EB_ERR_SHAPE;
+  }
+  if (optimizer == EB_OPT_ROWWISE_ADAGRAD) {
+    if (!optimizer_state.data) return EB_ERR_INVALID_ARG;
+    if (optimizer_state.elem_type != EB_T_F32) return EB_ERR_DTYPE;
+    if (optimizer_state.numel != h->total_rows) return EB_ERR_SHAPE;
+  }
+  if (offsets.numel < 2 || (offsets.numel - 1) % h->num_tables != 0) return EB_ERR_SHAPE;
+  const int64_t num_bags = offsets.numel - 1;
+  const int64_t batch = num_bags / h->num_tables;
+  if (num_bags > INT32_MAX) return EB_ERR_SHAPE;
+  if (grad_out.numel != batch * h->sum_dim) return EB_ERR_SHAPE;
+  const size_t isz = indices.elem_type == EB_I64 ? 8 : 4;
+  if (reinterpret_cast<uintptr_t>(grad_out.data) % 16 != 0 || reinterpret_cast<uintptr_t>(offsets.data) % isz != 0 ||
+      reinterpret_cast<uintptr_t>(indices.data) % isz != 0 ||
+      (weighted && reinterpret_cast<uintptr_t>(per_sample_weights.data) % 4 != 0) ||
+      reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+    return EB_ERR_UNSUPPORTED;
+  const int64_t n = indices.numel;
+  BwdLayout L;
+  eb_status st = layout(h, n, &L);
+  if (st != EB_OK) return st;
+  if (n > 0 && (!workspace || workspace_bytes < L.total)) return EB_ERR_INVALID_ARG;
+  if (n == 0) return EB_OK;  // no row was read: nothing to update
+
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return EB_ERR_HIP;
+  if (cur != h->device && hipSetDevice(h->device) != hipSuccess) return EB_ERR_HIP;
+
+  unsigned char *ws = static_cast<unsigned char *>(workspace);
+  BwdArgs a;
+  a.meta = h->d_meta;
+  a.ctx.err = h->d_err;
+  a.ctx.zero = h->d_zero;
+  a.ctx.one = 1.0f;
+  a.indices = indices.data;
+  a.offsets = offsets.data;
+  a.weights = static_cast<const float *>(per_sample_weights.data);
+  a.grad = static_cast<const float *>(grad_out.data);
+  a.state = static_cast<float *>(const_cast<void *>(optimizer_state.data));
+  a.keys = reinterpret_cast<uint32_t *>(ws + L.keys);
+  a.bag_of = reinterpret_cast<int32_t *>(ws + L.bag_of);
+  a.skeys = reinterpret_cast<const uint32_t *>(ws + L.skeys);
+  a.spos = reinterpret_cast<const uint32_t *>(ws + L.spos);
+  a.tile_start = reinterpret_cast<int32_t *>(ws + L.tile_start);
+  a.tile_flags = reinterpret_cast<uint8_t *>(ws + L.tile_flags);
+  a.carry = reinterpret_cast<float *>(ws + L.carry);
+  a.num_indices = n;
+  a.grad_ld = h->sum_dim;
+  a.num_bags = (int32_t)num_bags;
+  a.batch = (int32_t)batch;
+  a.num_tables = h->num_tables;
+  a.idx64 = indices.elem_type == EB_I64;
+  a.coef = pooling == EB_POOL_MEAN ? 2 : (weighted ? 1 : 0);
+  a.opt = optimizer;
+  a.lr = learning_rate;
+  a.eps = eps;
+  a.tile_size = L.tile_size;
+  a.max_dim = h->max_dim;
+  int64_t k = 1;
+  {
+    const int64_t per_slot = num_bags / kResidentWaves;
+    while ((k + 1) * (k + 1) <= per_slot) ++k;
+    k = k > kMaxBagsPerWave ? kMaxBagsPerWave : k;
+  }
+  a.bags_per_wave = (int32_t)k;
+  a.groups_per_table = (int32_t)((batch + k - 1) / k);
+  a.num_waves = (int32_t)((int64_t)a.groups_per_table * h->num_tables);
+
+  hipError_t e = hipSuccess;
+  if (h->checked) e = hipMemsetAsync(h->d_err, 0, sizeof(int), h->stream);
+  // 1. keys
+  if (e == hipSuccess) {
+    const unsigned grid = (unsigned)((a.num_waves + kWavesPerBlock - 1) / kWavesPerBlock);
+    hipLaunchKernelGGL(eb_bwd_keys_kernel, dim3(grid), dim3(kBlock), 0, h->stream, a);
+    e = hipGetLastError();
+  }
+  // 2. sort (key, position) pairs on the bits the largest key needs
+  if (e == hipSuccess) {
+    const unsigned end_bit = key_bits(h);
+    size_t tmp = L.sort_bytes;
+    e = rocprim::radix_sort_pairs(ws + L.sort_tmp, tmp, a.keys, const_cast<uint32_t *>(a.skeys),
+                                  rocprim::counting_iterator<uint32_t>(0), const_cast<uint32_t *>(a.spos),
+                                  (unsigned int)n, 0, end_bit, h->stream);
+  }
+  // 3. tiles: first tile per table, then pool and update
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(eb_bwd_tile_start_kernel, dim3(1), dim3(1024), 0, h->stream, a);
+    e = hipGetLastError();
+  }
+  const unsigned tgrid = (unsigned)((L.tiles_ub + kWavesPerBlock - 1) / kWavesPerBlock);
+  // one launch per storage type present; fixed row width when all tables share it
+  int32_t glog2 = log2_lanes_per_row(4 * h->h_meta[0].dim);
+  for (int32_t t = 1; t < h->num_tables; ++t)
+    if (log2_lanes_per_row(4 * h->h_meta[t].dim) != glog2) glog2 = -1;
+  for (int dt = 0; dt < 2 && e == hipSuccess; ++dt) {
+    if (!(h->dtype_mask & (1 << dt))) continue;
+    hipLaunchKernelGGL(dt == kF32 ? pick_tiles<kF32>(glog2) : pick_tiles<kF16>(glog2), dim3(tgrid), dim3(kBlock), 0,
+                       h->stream, a);
+    e = hipGetLastError();
+  }
+  // 4. runs that cross tiles
+  for (int dt = 0; dt < 2 && e == hipSuccess; ++dt) {
+    if (!(h->dtype_mask & (1 << dt))) continue;
+    hipLaunchKernelGGL(dt == kF32 ? eb_bwd_fixup_kernel<kF32> : eb_bwd_fixup_kernel<kF16>, dim3(tgrid), dim3(kBlock),
+                       0, h->stream, a);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess && h->checked) {
+    int herr = 0;
+    e = hipMemcpyAsync(&herr, h->d_err, sizeof(int), hipMemcpyDeviceToHost, h->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
+    if (e == hipSuccess && (herr & kErrOffsets)) st = EB_ERR_OFFSETS;
+    else if (e == hipSuccess && (herr & kErrIndex)) st = EB_ERR_INDEX_OOB;
+  }
+  if (e != hipSuccess) st = EB_ERR_HIP;
+  if (cur != h->device) (void)hipSetDevice(cur);
+  return st;
+}
+
+}  // extern "C"

@@ -22,65 +22,18 @@
 //     is uniform across the wave.
 // Rows wider than 1 KiB take several 1 KiB column passes.
 
-#include <hip/hip_runtime.h>
-#include <stdint.h>
-#include <stdlib.h>
-#include <string.h>
+#include "eb_device.h"
 
-#include "eb.h"
-
-// Unweighted int8 row-wise pooling sums s*q and the biases separately (one
-// fma per element instead of two); 0 keeps the per-element dequantisation.
-#ifndef EB_INT8_SPLIT_BIAS
-#define EB_INT8_SPLIT_BIAS 1
-#endif
-
+namespace eb {
 namespace {
-
-constexpr int kWave = 64;
-constexpr int kWavesPerBlock = 4;
-constexpr int kBlock = kWave * kWavesPerBlock;
-constexpr int kPassBytes = kWave * 16;  // one wave-wide 16-byte load covers 1 KiB
-constexpr uint32_t kBadRow = 0xFFFFFFFFu;
-constexpr int kMaxDim = 8192;
-// An all-zero row as long as the widest row slice any lane can address
-// (8192 fp32 values) plus the int8 scale/bias word.
-constexpr size_t kZeroBytes = 4 * kMaxDim + 16;
-// A wavefront pools up to this many consecutive bags (their offsets are read
-// with one vector load, one per lane, so at most 63).
-constexpr int kMaxBagsPerWave = 32;
-// Wavefronts resident on a full MI355X (256 CUs x 4 SIMDs x 8 waves).
-constexpr int64_t kResidentWaves = 256 * 4 * 8;
-// Handles with at most this many tables renumber workgroups XCD-contiguously.
-constexpr int32_t kRemapMaxTables = 32;
-
-// error bits raised by the kernel, reported in checked mode
-constexpr int kErrIndex = 1;
-constexpr int kErrOffsets = 2;
-
-enum : int32_t { kF32 = 0, kF16 = 1, kU8 = 2 };
-
-// Per-table descriptor as the kernel sees it (one scalar-cache line each).
-struct TableMeta {
-  const unsigned char *data;
-  uint32_t row_stride;  // bytes
-  int32_t num_rows;
-  int32_t dim;
-  int32_t code_bytes;   // element bytes per row: 4*dim, 2*dim or dim
-  int32_t out_col;      // first output column of this table
-  int32_t kind;         // dtype * 8 + log2(lanes per row)
-  int32_t passes;       // 1 KiB column passes per row
-  int32_t pad_;
-};
 
 struct FwdArgs {
   const TableMeta *meta;
-  const unsigned char *zero;  // kZeroBytes of zeros (read in place of rows that do not exist)
+  GatherCtx ctx;
   const void *indices;
   const void *offsets;
   const float *weights;
   float *out;
-  int *err;
   int64_t num_indices;
   int64_t out_ld;
   int32_t num_bags;
@@ -90,118 +43,7 @@ struct FwdArgs {
   int32_t bags_per_wave;     // consecutive bags of one table per wavefront
   int32_t groups_per_table;  // ceil(batch / bags_per_wave)
   int32_t num_waves;         // num_tables * groups_per_table
-  float one;                 // 1.0f (see accumulate)
   int32_t xcd_remap;         // renumber workgroups XCD-contiguously
-};
-
-// Table rows are plain device memory: address them in the global address
-// space so gathers compile to global (not flat) loads.
-#define EB_GLOBAL __attribute__((address_space(1)))
-typedef const EB_GLOBAL unsigned char gbyte;
-
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-// same vector, only 4-byte aligned: int8 rows of D+4 bytes start on any dword
-typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-template <int DT>
-struct Vals {
-  static constexpr int n = DT == kF32 ? 4 : (DT == kF16 ? 8 : 16);  // values per 16 B
-  static constexpr int esize = DT == kF32 ? 4 : (DT == kF16 ? 2 : 1);
-};
-
-__device__ __forceinline__ float half_lo(uint32_t v) {
-  return (float)__builtin_bit_cast(_Float16, (uint16_t)(v & 0xFFFFu));
-}
-__device__ __forceinline__ float half_hi(uint32_t v) {
-  return (float)__builtin_bit_cast(_Float16, (uint16_t)(v >> 16));
-}
-
-// acc += x (or acc = w*x + acc) for the 16-byte slice v of one row.
-//   `one` is 1.0f passed in at run time: fmaf(x, one, acc) with an fp16 x
-//   then compiles to a single v_fma_mix_f32 that widens and adds (exact
-//   widening, one rounding: the same bits as acc + x).
-//   Unweighted int8 rows (SPLIT) accumulate s*q with one fma per element
-//   (s*q is exact in fp32) and the row's bias once into cb; the caller adds
-//   cb to every element before the cross-lane reduction.  For a one-row bag
-//   that gives fp32(s*q + c) exactly as the dequantisation is defined; for
-//   longer bags it is a reassociation of the same sum.
-template <int DT, bool W, bool SPLIT>
-__device__ __forceinline__ void accumulate(float (&acc)[Vals<DT>::n], float &cb, u32x4 v, uint32_t sb, float w,
-                                           float one) {
-  if constexpr (DT == kF32) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float x = __uint_as_float(v[i]);
-      acc[i] = W ? fmaf(w, x, acc[i]) : acc[i] + x;
-    }
-  } else if constexpr (DT == kF16) {
-    const float f = W ? w : one;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      acc[2 * i] = fmaf(half_lo(v[i]), f, acc[2 * i]);
-      acc[2 * i + 1] = fmaf(half_hi(v[i]), f, acc[2 * i + 1]);
-    }
-  } else if constexpr (SPLIT && !W) {
-    const float s = half_lo(sb);
-    cb = fmaf(half_hi(sb), one, cb);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[4 * i + j] = fmaf(s, (float)((v[i] >> (8 * j)) & 0xFFu), acc[4 * i + j]);
-    }
-  } else {
-    // x = fp32(s*q + c): s*q is exact in fp32 (11-bit by 8-bit significands),
-    // so the fma rounds once, as the dequantisation is defined
-    const float s = half_lo(sb), c = half_hi(sb);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float q = (float)((v[i] >> (8 * j)) & 0xFFu);
-        const float x = fmaf(s, q, c);
-        acc[4 * i + j] = W ? fmaf(w, x, acc[4 * i + j]) : acc[4 * i + j] + x;
-      }
-    }
-  }
-}
-
-template <int DT>
-__device__ __forceinline__ u32x4 load_slice(gbyte *p) {
-  if constexpr (DT == kU8) {
-    return *reinterpret_cast<const EB_GLOBAL u32x4_a4 *>(p);
-  } else {
-    return *reinterpret_cast<const EB_GLOBAL u32x4 *>(p);
-  }
-}
-
-// Row-load steps issued before the first is consumed: enough rows in flight
-// per wave to cover HBM latency within the register budget.
-#ifndef EB_INT8_MAX_UNROLL
-#define EB_INT8_MAX_UNROLL 4
-#endif
-#ifndef EB_WEIGHTED_MAX_UNROLL
-#define EB_WEIGHTED_MAX_UNROLL 4
-#endif
-template <int DT, int RPL, bool W>
-struct Unroll {
-  static constexpr int c0 = DT == kU8 ? EB_INT8_MAX_UNROLL : 8;
-  static constexpr int cap = W && EB_WEIGHTED_MAX_UNROLL < c0 ? EB_WEIGHTED_MAX_UNROLL : c0;
-  static constexpr int u = (kWave / RPL) < cap ? (kWave / RPL) : cap;
-};
-
-// 64-bit value of lane `l` (wave-uniform l) of a per-lane value.
-__device__ __forceinline__ int64_t readlane64(int64_t v, int l) {
-  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, l);
-  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)v >> 32), l);
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
-// One chunk of up to 64 consecutive index positions of a bag, one per lane.
-struct Chunk {
-  uint32_t row;  // row number, or kBadRow (no row / outside the table)
-  float w;       // per-sample weight (weighted pooling only)
-  int n;         // positions in the chunk (wave-uniform)
 };
 
 template <bool W>
@@ -220,157 +62,6 @@ __device__ __forceinline__ Chunk load_chunk(const TableMeta &m, const FwdArgs &a
   }
   return k;
 }
-
-// Gather steps [s0, s0 + N) of one chunk (RPL rows per step) and add them into
-// this lane's accumulators.  Straight-line code: a lane whose row does not
-// exist (past the chunk's end, outside the table, or a slice past the row's
-// end) reads the handle's all-zero row instead, which adds nothing, so no
-// branch separates a load from its use and the loads of all N steps are in
-// flight together.
-template <int DT, int LPR, bool W, bool SPLIT, int N>
-__device__ __forceinline__ void gather_steps(const TableMeta &m, const FwdArgs &a, const Chunk &k, int s0,
-                                             float (&acc)[Vals<DT>::n], float &cb, int colb, bool colok) {
-  constexpr int RPL = kWave / LPR;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int grp = lane / LPR;
-  u32x4 v[N];
-  uint32_t sb[N];
-  float w[N];
-#pragma unroll
-  for (int u = 0; u < N; ++u) {
-    const int r = (s0 + u) * RPL + grp;
-    uint32_t row;
-    if constexpr (RPL == 1) {
-      row = __builtin_amdgcn_readlane(k.row, (s0 + u) & (kWave - 1));
-      if constexpr (W)
-        w[u] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(uint32_t, k.w),
-                                                                    (s0 + u) & (kWave - 1)));
-    } else {
-      row = (uint32_t)__shfl((int)k.row, r & (kWave - 1));
-      if constexpr (W) w[u] = __shfl(k.w, r & (kWave - 1));
-    }
-    const bool ok = (r < k.n) && (row != kBadRow) && colok;
-    gbyte *p = ok ? (gbyte *)m.data + (uint64_t)row * m.row_stride : (gbyte *)a.zero;
-    v[u] = load_slice<DT>(p + colb);
-    if constexpr (DT == kU8) sb[u] = *reinterpret_cast<const EB_GLOBAL uint32_t *>(p + m.dim);
-    else sb[u] = 0u;
-    if constexpr (!W) w[u] = 1.0f;
-  }
-#pragma unroll
-  for (int u = 0; u < N; ++u) accumulate<DT, W, SPLIT>(acc, cb, v[u], sb[u], w[u], a.one);
-}
-
-// Gather all rows of one chunk: full batches of U steps, then one batch of
-// the smallest power-of-two size that covers the remaining steps (its
-// missing steps read the zero row), so a chunk of up to U steps costs one
-// memory round trip.
-template <int DT, int LPR, bool W, bool SPLIT>
-__device__ __forceinline__ void gather_chunk(const TableMeta &m, const FwdArgs &a, const Chunk &k,
-                                             float (&acc)[Vals<DT>::n], float &cb, int colb, bool colok) {
-  constexpr int RPL = kWave / LPR;
-  constexpr int U = Unroll<DT, RPL, W>::u;
-  const int lane = threadIdx.x & (kWave - 1);
-  if (__ballot(lane < k.n && k.row == kBadRow)) {
-    if (lane == 0) atomicOr(a.err, kErrIndex);
-  }
-  const int steps = (k.n + RPL - 1) / RPL;
-  int s = 0;
-  for (; steps - s > U / 2; s += U) gather_steps<DT, LPR, W, SPLIT, U>(m, a, k, s, acc, cb, colb, colok);
-  const int rem = steps - s;  // 0 .. U/2
-  if constexpr (U >= 8) {
-    if (rem > 2) {
-      gather_steps<DT, LPR, W, SPLIT, 4>(m, a, k, s, acc, cb, colb, colok);
-      return;
-    }
-  }
-  if constexpr (U >= 4) {
-    if (rem > 1) {
-      gather_steps<DT, LPR, W, SPLIT, 2>(m, a, k, s, acc, cb, colb, colok);
-      return;
-    }
-  }
-  if (rem > 0) gather_steps<DT, LPR, W, SPLIT, 1>(m, a, k, s, acc, cb, colb, colok);
-}
-
-__device__ __forceinline__ float dpp_row_ror(float x, int o) {
-  // rotate within each 16-lane row by o lanes (o is a compile-time constant)
-  const int xi = __builtin_bit_cast(int, x);
-  int r;
-  switch (o) {
-    case 1: r = __builtin_amdgcn_update_dpp(0, xi, 0x121, 0xf, 0xf, false); break;
-    case 2: r = __builtin_amdgcn_update_dpp(0, xi, 0x122, 0xf, 0xf, false); break;
-    case 4: r = __builtin_amdgcn_update_dpp(0, xi, 0x124, 0xf, 0xf, false); break;
-    default: r = __builtin_amdgcn_update_dpp(0, xi, 0x128, 0xf, 0xf, false); break;
-  }
-  return __builtin_bit_cast(float, r);
-}
-
-// Sum the RPL row groups' partial vectors (a reduce-scatter in a fixed order,
-// so results are deterministic).  On return, lane (row q of 16 lanes, slot
-// p) holds V / min(RPL, 4) consecutive values of the pooled slice of lane-slot
-// p % LPR, starting at value index first_value(); only lanes with
-// stores() == true write them.
-// (Elements of the swap builtins' two-lane result are read by value with
-// __uint_as_float: __builtin_bit_cast applied to such an element reads the
-// first element whatever the index.)
-template <int DT, int LPR>
-struct Reduce {
-  static constexpr int V = Vals<DT>::n;
-  static constexpr int KEEP = LPR >= 64 ? V : (LPR == 32 ? V / 2 : V / 4);
-
-  __device__ static __forceinline__ void run(float (&acc)[V]) {
-    if constexpr (LPR < 16) {
-      // combine the row groups that share a 16-lane row: all-reduce by rotation
-#pragma unroll
-      for (int o = LPR; o < 16; o <<= 1) {
-#pragma unroll
-        for (int i = 0; i < V; ++i) acc[i] += dpp_row_ror(acc[i], o);
-      }
-    }
-    if constexpr (LPR <= 16) {
-      // rows 0+1 and 2+3: pair value i with value i + V/2; rows 0,2 keep the
-      // first, rows 1,3 the second
-#pragma unroll
-      for (int i = 0; i < V / 2; ++i) {
-        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(acc[i]),
-                                                        __float_as_uint(acc[i + V / 2]), false, false);
-        acc[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-      }
-      // halves: pair value j with j + V/4 (of the V/2 left); the low half
-      // keeps the first, the high half the second
-#pragma unroll
-      for (int j = 0; j < V / 4; ++j) {
-        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[j]),
-                                                        __float_as_uint(acc[j + V / 4]), false, false);
-        acc[j] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-      }
-    } else if constexpr (LPR == 32) {
-#pragma unroll
-      for (int i = 0; i < V / 2; ++i) {
-        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[i]),
-                                                        __float_as_uint(acc[i + V / 2]), false, false);
-        acc[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-      }
-    }
-  }
-
-  // index (within the lane-slot's V values) of the first value this lane holds
-  __device__ static __forceinline__ int first_value(int lane) {
-    if constexpr (LPR >= 64) {
-      return 0;
-    } else if constexpr (LPR == 32) {
-      return (lane >> 5) * (V / 2);
-    } else {
-      const int q = lane >> 4;  // 16-lane row
-      return ((q & 1) ? V / 2 : 0) + ((q & 2) ? V / 4 : 0);
-    }
-  }
-
-  __device__ static __forceinline__ bool stores(int lane) {
-    if constexpr (LPR >= 16) return true;
-    return (lane & 15) < LPR;
-  }
-};
 
 // Pool bags [g0, g0 + nb) of one table (batch rows b0 ..) over the 1 KiB column
 // window starting at byte col_base.  The bags' index positions are walked as
@@ -401,7 +92,7 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
     bool bad = lo < 0 || hi < lo || hi > a.num_indices;
     bad |= (g == 0 && lo != 0) || (g == a.num_bags - 1 && hi != a.num_indices);
     if (bad) {
-      if (lane == 0) atomicOr(a.err, kErrOffsets);
+      if (lane == 0) atomicOr(a.ctx.err, kErrOffsets);
       lo = lo < 0 ? 0 : (lo > a.num_indices ? a.num_indices : lo);
       hi = hi < lo ? lo : (hi > a.num_indices ? a.num_indices : hi);
     }
@@ -433,7 +124,7 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
     Chunk nxt;
     if (more) nxt = load_chunk<W>(m, a, cn, nhi);
 
-    gather_chunk<DT, LPR, W, SPLIT>(m, a, cur, acc, cb, colb, colok);
+    gather_chunk<DT, LPR, W, SPLIT>(m, a.ctx, cur, acc, cb, colb, colok);
 
     if (last) {
       if constexpr (SPLIT) {
@@ -486,19 +177,6 @@ __device__ __forceinline__ void pool_all_passes(const TableMeta &m, const FwdArg
   } else {
     pool_bags<DT, LPR, W>(m, a, g0, nb, b0, 0);
   }
-}
-
-// Workgroups are handed to the 8 XCDs round-robin (block i runs on XCD i % 8).
-// Renumbering them so each XCD walks one contiguous eighth of the work keeps
-// each XCD's L2 on few tables for the whole launch; leaving them round-robin
-// puts all XCDs on the same table at once, so the shared Infinity Cache holds
-// that one table's hot rows.  The first wins with few tables (measured: 8 and
-// 26), the second with many large ones (64 and 100); the host picks.
-__device__ __forceinline__ uint32_t xcd_contiguous(uint32_t i, uint32_t n) {
-  constexpr uint32_t kXcd = 8;
-  const uint32_t x = i % kXcd, slot = i / kXcd;
-  const uint32_t q = n / kXcd, r = n % kXcd;
-  return x < r ? x * (q + 1) + slot : r * (q + 1) + (x - r) * q + slot;
 }
 
 #define EB_LPR(LOG2)                                                          \
@@ -559,29 +237,10 @@ KernelFn pick_kernel(int dt, int log2, bool weighted) {
   return weighted ? pick_kernel<kU8, true>(log2) : pick_kernel<kU8, false>(log2);
 }
 
-int log2_lanes_per_row(int code_bytes) {
-  int slices = (code_bytes + 15) / 16;
-  int l = 0;
-  while ((1 << l) < slices && l < 6) ++l;
-  return l;
-}
-
 }  // namespace
+}  // namespace eb
 
-struct eb_tables {
-  int device;
-  hipStream_t stream;
-  int32_t num_tables;
-  int32_t checked;
-  int32_t bags_per_wave;  // 0: chosen per call from the bag count
-  int32_t dtype_mask;     // bit d set: some table has storage type d
-  int32_t single_log2;    // lanes-per-row log2 shared by every table of one type, else -1
-  int32_t xcd_remap;      // see xcd_contiguous
-  int64_t sum_dim;
-  TableMeta *d_meta;  // device: descriptors, then the error word, then the zero row
-  int *d_err;
-  unsigned char *d_zero;
-};
+using namespace eb;
 
 extern "C" {
 
@@ -607,7 +266,8 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
 
   TableMeta *meta = static_cast<TableMeta *>(calloc((size_t)num_tables, sizeof(TableMeta)));
   if (!meta) return EB_ERR_OOM;
-  int64_t col = 0;
+  int64_t col = 0, rows_before = 0;
+  uint64_t key_before = 0;
   eb_status st = EB_OK;
   for (int32_t t = 0; t < num_tables && st == EB_OK; ++t) {
     const eb_table_desc &d = descs[t];
@@ -640,6 +300,10 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
       m.out_col = (int32_t)col;
       m.kind = d.dtype * 8 + log2_lanes_per_row((int)code_bytes);
       m.passes = (int32_t)((code_bytes + kPassBytes - 1) / kPassBytes);
+      m.state_base = rows_before;
+      m.key_base = (uint32_t)(key_before <= UINT32_MAX ? key_before : 0);
+      rows_before += d.num_rows;
+      key_before += d.num_rows + 1;
       col += d.dim;
       if (col > INT32_MAX) st = EB_ERR_SHAPE;
     }
@@ -663,15 +327,24 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   h->num_tables = num_tables;
   h->dtype_mask = 0;
   h->single_log2 = meta[0].kind % 8;
+  h->max_dim = 0;
+  h->total_rows = rows_before;
+  // the backward sorts (table, row) as one 32-bit key: sum of (rows + 1) must fit
+  h->backward_ok = key_before <= (uint64_t)UINT32_MAX;
   for (int32_t t = 0; t < num_tables; ++t) {
     h->dtype_mask |= 1 << (meta[t].kind / 8);
     if (meta[t].kind != meta[0].kind) h->single_log2 = -1;
+    if (meta[t].dim > h->max_dim) h->max_dim = meta[t].dim;
+    if (meta[t].kind / 8 == kU8 || meta[t].dim > kMaxBackwardDim) h->backward_ok = 0;
   }
   h->sum_dim = col;
   const char *chk = getenv("EB_CHECK");
   h->checked = (chk && chk[0] == '1') ? 1 : 0;
   const char *remap = getenv("EB_XCD_REMAP");
   h->xcd_remap = remap ? (remap[0] == '1') : (num_tables <= kRemapMaxTables);
+  const char *btc = getenv("EB_BWD_TILE_CHUNKS");
+  h->bwd_tile_chunks = btc ? atoi(btc) : 0;
+  if (h->bwd_tile_chunks < 0 || h->bwd_tile_chunks > 16) h->bwd_tile_chunks = 0;
   const char *bpw = getenv("EB_BAGS_PER_WAVE");
   h->bags_per_wave = bpw ? atoi(bpw) : 0;
   if (h->bags_per_wave < 0 || h->bags_per_wave > kMaxBagsPerWave) h->bags_per_wave = 0;
@@ -692,12 +365,13 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   h->d_zero = static_cast<unsigned char *>(dev) + zero_off;
   e = hipMemcpy(h->d_meta, meta, meta_bytes, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemset(static_cast<char *>(dev) + err_off, 0, 256 + kZeroBytes);
-  free(meta);
   if (e != hipSuccess) {
+    free(meta);
     (void)hipFree(dev);
     free(h);
     return EB_ERR_HIP;
   }
+  h->h_meta = meta;
   *out = h;
   return EB_OK;
 }
@@ -738,9 +412,9 @@ eb_status eb_forward(const eb_tables *h, eb_tensor indices, eb_tensor offsets, e
   a.offsets = offsets.data;
   a.weights = static_cast<const float *>(per_sample_weights.data);
   a.out = static_cast<float *>(const_cast<void *>(out.data));
-  a.err = h->d_err;
-  a.zero = h->d_zero;
-  a.one = 1.0f;
+  a.ctx.err = h->d_err;
+  a.ctx.zero = h->d_zero;
+  a.ctx.one = 1.0f;
   a.xcd_remap = h->xcd_remap;
   a.num_indices = indices.numel;
   a.out_ld = h->sum_dim;
@@ -796,6 +470,7 @@ eb_status eb_destroy(eb_tables *h) {
   if (st == EB_OK && cur != h->device && hipSetDevice(h->device) != hipSuccess) st = EB_ERR_HIP;
   if (st == EB_OK && hipStreamSynchronize(h->stream) != hipSuccess) st = EB_ERR_HIP;
   if (hipFree(h->d_meta) != hipSuccess) st = EB_ERR_HIP;
+  free(h->h_meta);
   if (cur >= 0 && cur != h->device) (void)hipSetDevice(cur);
   free(h);
   return st;

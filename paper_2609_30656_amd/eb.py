@@ -33,10 +33,14 @@ EB_F32, EB_F16, EB_INT8_ROWWISE = 0, 1, 2
 EB_I32, EB_I64, EB_T_F32 = 0, 1, 2
 # eb_pooling
 EB_POOL_SUM, EB_POOL_MEAN = 0, 1
+# eb_optimizer
+EB_OPT_SGD, EB_OPT_ROWWISE_ADAGRAD = 0, 1
 
 TABLE_DTYPES = {"f32": EB_F32, "f16": EB_F16, "int8_rowwise": EB_INT8_ROWWISE}
 POOLING = {"sum": EB_POOL_SUM, "mean": EB_POOL_MEAN}
-EXPORTED = ("eb_create_tables", "eb_forward", "eb_destroy", "eb_status_string")
+OPTIMIZERS = {"sgd": EB_OPT_SGD, "rowwise_adagrad": EB_OPT_ROWWISE_ADAGRAD}
+EXPORTED = ("eb_create_tables", "eb_forward", "eb_destroy", "eb_status_string", "eb_backward_workspace_size",
+            "eb_backward_update")
 
 
 class EBError(RuntimeError):
@@ -79,6 +83,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.eb_destroy.argtypes = [ctypes.c_void_p]
         lib.eb_status_string.restype = ctypes.c_char_p
         lib.eb_status_string.argtypes = [ctypes.c_int]
+        lib.eb_backward_workspace_size.restype = ctypes.c_int
+        lib.eb_backward_workspace_size.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]
+        lib.eb_backward_update.restype = ctypes.c_int
+        lib.eb_backward_update.argtypes = [ctypes.c_void_p, eb_tensor, eb_tensor, eb_tensor, ctypes.c_int, eb_tensor,
+                                           ctypes.c_int32, ctypes.c_float, ctypes.c_float, eb_tensor,
+                                           ctypes.c_void_p, ctypes.c_size_t]
         _lib = lib
     return _lib
 
@@ -167,3 +177,33 @@ def eb_destroy(tables: EbTables) -> None:
         tables.ptr = None
         if st != EB_OK:
             raise EBError(st, "eb_destroy")
+
+
+def eb_backward_workspace_size(tables: EbTables, num_indices: int) -> int:
+    n = ctypes.c_size_t()
+    st = load_library().eb_backward_workspace_size(tables.ptr, int(num_indices), ctypes.byref(n))
+    if st != EB_OK:
+        raise EBError(st, "eb_backward_workspace_size")
+    return int(n.value)
+
+
+def eb_backward_update(tables: EbTables, indices: torch.Tensor, offsets: torch.Tensor,
+                       per_sample_weights: Optional[torch.Tensor], pooling, grad_out: torch.Tensor,
+                       optimizer="sgd", learning_rate: float = 0.01, eps: float = 1e-8,
+                       optimizer_state: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None) -> None:
+    """Enqueue the backward + optimizer step on the handle's stream.
+
+    workspace: a device uint8 tensor of at least eb_backward_workspace_size()
+    bytes; when None one is allocated (torch owns it)."""
+    lib = load_library()
+    if workspace is None:
+        nbytes = eb_backward_workspace_size(tables, indices.numel())
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=grad_out.device)
+    mode = POOLING[pooling] if isinstance(pooling, str) else int(pooling)
+    opt = OPTIMIZERS[optimizer] if isinstance(optimizer, str) else int(optimizer)
+    st = lib.eb_backward_update(tables.ptr, _as_tensor(indices), _as_tensor(offsets), _as_tensor(per_sample_weights),
+                                mode, _as_tensor(grad_out), opt, float(learning_rate), float(eps),
+                                _as_tensor(optimizer_state), workspace.data_ptr(), workspace.numel())
+    if st != EB_OK:
+        raise EBError(st, "eb_backward_update")

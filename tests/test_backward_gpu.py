@@ -1,0 +1,241 @@
+"""GPU parity of the backward + fused optimizer step against the CPU oracle.
+
+For every table row the oracle reports (rows that occur in the batch) with
+gradient G (fp64), error scale S = sum_i |c_i g| and occurrence count n:
+  * rows that do not occur keep their bits;
+  * SGD:    |W_gpu - W_oracle| <= lr (n + 8) u S + rounding of the stored value
+            (2u|W| for fp32 tables, one fp16 ulp for fp16 tables);
+  * Adagrad: the same with the error of the state and of the step size
+            propagated (bounds computed below from G, S, n), and the state
+            itself within its bound,
+with u = 2^-24: fp32 summation of the n terms in any order, the tile partial
+sums included.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import OracleTable, ebo_backward_update
+from paper_2609_30656_amd import eb
+from paper_2609_30656_amd.workload import Table, Workload, make_workload
+
+pytestmark = pytest.mark.gpu
+U = 2.0 ** -24
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    eb.load_library()
+    d = torch.device("cuda:0")
+    torch.cuda.set_device(d)
+    return d
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def _grad(w, dev, seed=7):
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    return torch.randn((w.batch, w.sum_dim), generator=g, device=dev, dtype=torch.float32)
+
+
+def _ulp16(x):
+    """One fp16 ulp at |x| (subnormal spacing below 2^-14)."""
+    a = np.maximum(np.abs(x), 2.0 ** -14)
+    return 2.0 ** (np.floor(np.log2(a)) - 10)
+
+
+def run_and_check(w, dev, optimizer, lr=0.05, eps=1e-4, check_tables=None, label=""):
+    T = w.num_tables
+    check_tables = list(range(T)) if check_tables is None else check_tables
+    grad = _grad(w, dev)
+    R = [t.num_rows for t in w.tables]
+    state = None
+    if optimizer == "rowwise_adagrad":
+        gs = torch.Generator(device=dev)
+        gs.manual_seed(11)
+        state = torch.rand(sum(R), generator=gs, device=dev, dtype=torch.float32)
+    before = {t: w.tables[t].rows.detach().cpu().numpy().copy() for t in check_tables}
+    state0 = None if state is None else state.cpu().numpy().copy()
+    say(f"[bwd] {label}: {w.num_indices} lookups, {optimizer}; backward on the GPU")
+    with eb.eb_create_tables(w.tables) as h:
+        eb.eb_backward_update(h, w.indices, w.offsets, w.weights, w.pooling, grad, optimizer, lr, eps, state)
+        torch.cuda.synchronize()
+    after = {t: w.tables[t].rows.detach().cpu().numpy() for t in check_tables}
+    state1 = None if state is None else state.cpu().numpy()
+    say(f"[bwd] {label}: oracle on tables {check_tables}")
+    tabs = [OracleTable(before[t] if t in before else None, tb.dim, tb.dtype, tb.num_rows)
+            for t, tb in enumerate(w.tables)]
+    st_or = None if state0 is None else state0.copy()
+    rep = ebo_backward_update(tabs, w.indices.cpu().numpy(), w.offsets.cpu().numpy(),
+                              None if w.weights is None else w.weights.cpu().numpy(), w.pooling,
+                              grad.cpu().numpy(), optimizer, lr, eps, st_or, report=check_tables)
+    base = np.concatenate([[0], np.cumsum(R)])
+    for t in check_tables:
+        tb = w.tables[t]
+        rows, G, S, n = rep[t]
+        ref = tabs[t].rows  # updated in place by the oracle
+        got = after[t]
+        untouched = np.ones(tb.num_rows, bool)
+        untouched[rows] = False
+        raw = np.uint16 if tb.dtype == "f16" else np.uint32
+        assert np.array_equal(got[untouched].view(raw), before[t][untouched].view(raw)), f"{label} t{t}: untouched rows"
+        if rows.size == 0:
+            continue
+        g64 = got[rows].astype(np.float64)
+        r64 = ref[rows].astype(np.float64)
+        dG = (n[:, None] + 8) * U * S
+        store = (2 * U * np.abs(r64)) if tb.dtype == "f32" else _ulp16(r64)
+        if optimizer == "sgd":
+            bound = lr * dG + store
+        else:
+            s_new = st_or[base[t] + rows].astype(np.float64)
+            D = tb.dim
+            ds = 2 * (np.abs(G) * dG).sum(axis=1) / D + (D + 8) * U * s_new
+            scale = lr / (np.sqrt(s_new) + eps)
+            rel = 0.5 * ds / np.maximum(s_new, 1e-30) + 6 * U
+            bound = scale[:, None] * dG + np.abs(scale[:, None] * G) * rel[:, None] + store
+            np.testing.assert_array_less(np.abs(state1[base[t] + rows] - s_new), ds + 2 * U * s_new + 1e-30)
+            assert np.array_equal(state1[base[t]:base[t + 1]][untouched], state0[base[t]:base[t + 1]][untouched])
+        err = np.abs(g64 - r64)
+        bad = err > bound * 1.0001 + 1e-30
+        assert not bad.any(), (f"{label} t{t}: {bad.sum()} elements beyond the bound; worst ratio "
+                               f"{np.max(err / np.maximum(bound, 1e-30)):.3g}")
+
+
+REDUCED = {
+    "c1": {},
+    "c2": dict(rows_cap=20000, batch=256),
+    "c3a": dict(rows_cap=50000, batch=256),
+    "c3b": dict(rows_cap=50000, batch=256),
+    "c4": dict(rows_cap=20000, batch=96),
+}
+
+
+@pytest.mark.parametrize("optimizer", ["sgd", "rowwise_adagrad"])
+@pytest.mark.parametrize("name", list(REDUCED))
+def test_reduced_configs(dev, name, optimizer):
+    w = make_workload(name, dev, **REDUCED[name])
+    run_and_check(w, dev, optimizer, label=f"reduced {name}")
+
+
+@pytest.mark.parametrize("chunks", ["2", "3", "4", "16"])
+@pytest.mark.parametrize("name", ["c2", "c3b", "c4"])
+def test_multi_chunk_tiles(dev, monkeypatch, name, chunks):
+    # tiles of several 64-position chunks: runs that end exactly at a chunk
+    # boundary inside a tile, and runs that cross chunks
+    monkeypatch.setenv("EB_BWD_TILE_CHUNKS", chunks)
+    w = make_workload(name, dev, **REDUCED[name])
+    run_and_check(w, dev, "rowwise_adagrad", label=f"{chunks} chunks {name}")
+
+
+@pytest.mark.parametrize("name", ["c2", "c4"])
+def test_int32_indices(dev, name):
+    w = make_workload(name, dev, index_dtype=torch.int32, **REDUCED[name])
+    run_and_check(w, dev, "rowwise_adagrad", label=f"int32 {name}")
+
+
+@pytest.mark.parametrize("chunks", ["1", "3"])
+def test_hot_row_spans_many_tiles(dev, monkeypatch, chunks):
+    monkeypatch.setenv("EB_BWD_TILE_CHUNKS", chunks)
+    # one row read 5000 times (about 80 tiles of 64 positions), next to short runs
+    g = torch.Generator(device="cpu")
+    g.manual_seed(1)
+    B = 64
+    lens = torch.full((B,), 100, dtype=torch.int64)
+    idx = torch.randint(0, 300, (B * 100,), generator=g)
+    idx[torch.rand(B * 100, generator=g) < 0.8] = 17
+    off = torch.zeros(B + 1, dtype=torch.int64)
+    torch.cumsum(lens, 0, out=off[1:])
+    rows = torch.randn((300, 64), generator=g).to(dev)
+    w = Workload("hot", [Table(rows, 64, "f32")], B, idx.to(dev), off.to(dev), None, "sum", lens.to(dev))
+    run_and_check(w, dev, "rowwise_adagrad", label="hot row")
+    w.tables[0].rows.copy_(torch.randn((300, 64), generator=g).to(dev))
+    run_and_check(w, dev, "sgd", label="hot row sgd")
+
+
+def test_mixed_storage_and_widths(dev):
+    g = torch.Generator(device="cpu")
+    g.manual_seed(2)
+    tables = [Table(torch.randn((500, 4), generator=g).to(dev), 4, "f32"),
+              Table((torch.randn((400, 256), generator=g) * 0.01).half().to(dev), 256, "f16"),
+              Table(torch.randn((300, 40), generator=g).to(dev), 40, "f32"),
+              Table((torch.randn((200, 8), generator=g) * 0.01).half().to(dev), 8, "f16")]
+    B = 50
+    lens = torch.randint(0, 150, (4 * B,), generator=g)
+    lens[:5] = 0
+    off = torch.zeros(4 * B + 1, dtype=torch.int64)
+    torch.cumsum(lens, 0, out=off[1:])
+    parts = [torch.randint(0, t.num_rows, (int(lens[i * B:(i + 1) * B].sum()),), generator=g)
+             for i, t in enumerate(tables)]
+    idx = torch.cat(parts)
+    wts = torch.rand(idx.numel(), generator=g)
+    for pooling, weights in (("sum", wts), ("mean", None)):
+        w = Workload("mixed", tables, B, idx.to(dev), off.to(dev), None if weights is None else weights.to(dev),
+                     pooling, lens.to(dev))
+        run_and_check(w, dev, "rowwise_adagrad", label=f"mixed {pooling}")
+
+
+def test_deterministic(dev):
+    w = make_workload("c3b", dev, **REDUCED["c3b"])
+    init = [t.rows.clone() for t in w.tables]
+    grad = _grad(w, dev)
+    res = []
+    for _ in range(2):
+        for t, r in zip(w.tables, init):
+            t.rows.copy_(r)
+        st = torch.zeros(sum(t.num_rows for t in w.tables), device=dev)
+        with eb.eb_create_tables(w.tables) as h:
+            eb.eb_backward_update(h, w.indices, w.offsets, w.weights, w.pooling, grad, "rowwise_adagrad", 0.1, 1e-3,
+                                  st)
+            torch.cuda.synchronize()
+        res.append(([t.rows.clone() for t in w.tables], st.clone()))
+    for a, b in zip(res[0][0], res[1][0]):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    assert torch.equal(res[0][1], res[1][1])
+
+
+@pytest.mark.parametrize("name", ["c3a", "c4"])
+def test_full_size(dev, name):
+    say(f"[bwd] full {name}: generating")
+    w = make_workload(name, dev)
+    T = w.num_tables
+    run_and_check(w, dev, "rowwise_adagrad", check_tables=sorted({0, T // 2, T - 1}), label=f"full {name}")
+
+
+def test_backward_argument_errors(dev):
+    g = torch.Generator(device="cpu")
+    g.manual_seed(3)
+    t8 = torch.randint(0, 255, (10, 20), generator=g, dtype=torch.uint8).to(dev)
+    idx = torch.tensor([1, 2], device=dev)
+    off = torch.tensor([0, 1, 2], device=dev)
+    with eb.eb_create_tables([Table(t8, 16, "int8_rowwise")]) as h:
+        with pytest.raises(eb.EBError) as e:
+            eb.eb_backward_update(h, idx, off, None, "sum", torch.zeros((2, 16), device=dev))
+        assert e.value.status == eb.EB_ERR_UNSUPPORTED
+    wide = torch.zeros((10, 512), device=dev)
+    with eb.eb_create_tables([Table(wide, 512, "f32")]) as h:
+        with pytest.raises(eb.EBError) as e:
+            eb.eb_backward_update(h, idx, off, None, "sum", torch.zeros((2, 512), device=dev))
+        assert e.value.status == eb.EB_ERR_UNSUPPORTED
+    tab = torch.zeros((10, 16), device=dev)
+    with eb.eb_create_tables([Table(tab, 16, "f32")]) as h:
+        gr = torch.zeros((2, 16), device=dev)
+        with pytest.raises(eb.EBError) as e:  # Adagrad without state
+            eb.eb_backward_update(h, idx, off, None, "sum", gr, "rowwise_adagrad")
+        assert e.value.status == eb.EB_ERR_INVALID_ARG
+        with pytest.raises(eb.EBError) as e:  # state of the wrong length
+            eb.eb_backward_update(h, idx, off, None, "sum", gr, "rowwise_adagrad", optimizer_state=torch.zeros(9, device=dev))
+        assert e.value.status == eb.EB_ERR_SHAPE
+        with pytest.raises(eb.EBError) as e:
+            eb.eb_backward_update(h, idx, off, None, "sum", torch.zeros((3, 16), device=dev))
+        assert e.value.status == eb.EB_ERR_SHAPE
+        with pytest.raises(eb.EBError) as e:  # workspace too small
+            eb.eb_backward_update(h, idx, off, None, "sum", gr, workspace=torch.empty(16, dtype=torch.uint8, device=dev))
+        assert e.value.status == eb.EB_ERR_INVALID_ARG
+        torch.cuda.synchronize()
+        assert torch.all(tab == 0)
