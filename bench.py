@@ -29,6 +29,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
 METRIC = "EmbeddingBag fwd achieved HBM GB/s (% of peak) + pooled lookups/sec, 1 GPU"
+METRIC_BACKWARD = ("EmbeddingBag bwd + fused row-wise Adagrad update achieved HBM GB/s (% of peak) + "
+                   "lookups/sec, 1 GPU")
 KERNEL_NAME = "eb_pool_kernel"
 SAMPLE = 7
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_30656_amd", "csrc", f) for f in ("eb_device.h", "eb_forward.hip")]
@@ -61,6 +63,27 @@ def counter_traffic(config: str, index_law: str):
         return float(vals["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def backward_algorithmic_bytes(w) -> int:
+    """Bytes one backward + row-wise Adagrad step must move at minimum: the
+    gathered gradient rows (4*D per lookup), each touched table row read and
+    written once, its optimizer state read and written once, and the indices,
+    offsets and weights."""
+    import torch
+
+    esz = w.indices.element_size()
+    B = w.batch
+    total = w.num_indices * esz + int(w.offsets.numel()) * esz
+    if w.weights is not None:
+        total += w.num_indices * 4
+    off = w.offsets.cpu()
+    for t, tb in enumerate(w.tables):
+        lo, hi = int(off[t * B]), int(off[(t + 1) * B])
+        n = hi - lo
+        u = int(torch.unique(w.indices[lo:hi]).numel()) if n else 0
+        total += n * 4 * tb.dim + u * (2 * tb.row_bytes + 8)
+    return total
 
 
 def cpu_cores() -> int:
@@ -121,6 +144,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing (0 = skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (to scale rocprofv3 byte counters)")
+    ap.add_argument("--mode", default="forward", choices=["forward", "backward"],
+                    help="backward: eb_backward_update with row-wise Adagrad instead of eb_forward")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -144,7 +169,10 @@ def main():
         batches.append(make_workload(args.config, dev, batch_seed=s, index_law=law, tables=batches[0].tables))
     w0 = batches[0]
     out = torch.empty((w0.batch, w0.sum_dim), dtype=torch.float32, device=dev)
-    algo = [b.algorithmic_bytes() for b in batches]
+    if args.mode == "forward":
+        algo = [b.algorithmic_bytes() for b in batches]
+    else:
+        algo = [backward_algorithmic_bytes(b) for b in batches]
     nlook = [b.num_indices for b in batches]
     torch.cuda.synchronize()
 
@@ -155,11 +183,27 @@ def main():
               eb.POOLING[b.pooling]) for b in batches]
     o = eb._as_tensor(out)
 
-    def step(k):
-        i, f, wt, mode = calls[k % 3]
-        st = lib.eb_forward(h.ptr, i, f, wt, mode, o)
-        if st != eb.EB_OK:
-            raise eb.EBError(st, "eb_forward")
+    if args.mode == "forward":
+        def step(k):
+            i, f, wt, mode = calls[k % 3]
+            st = lib.eb_forward(h.ptr, i, f, wt, mode, o)
+            if st != eb.EB_OK:
+                raise eb.EBError(st, "eb_forward")
+    else:
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(5)
+        grad = torch.randn((w0.batch, w0.sum_dim), generator=gen, device=dev, dtype=torch.float32)
+        state = torch.zeros(sum(t.num_rows for t in w0.tables), dtype=torch.float32, device=dev)
+        ws_bytes = max(eb.eb_backward_workspace_size(h, b.num_indices) for b in batches)
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+        g_t, s_t = eb._as_tensor(grad), eb._as_tensor(state)
+
+        def step(k):
+            i, f, wt, mode = calls[k % 3]
+            st = lib.eb_backward_update(h.ptr, i, f, wt, mode, g_t, eb.EB_OPT_ROWWISE_ADAGRAD, 1e-3, 1e-8, s_t,
+                                        ws.data_ptr(), ws_bytes)
+            if st != eb.EB_OK:
+                raise eb.EBError(st, "eb_backward_update")
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for k in range(args.warmup):
@@ -193,7 +237,7 @@ def main():
     look_total = sum(nlook[k % 3] for k in range(args.steps))
     value = bytes_total / wall / 1e9
     achieved = kern_bytes / kern_avg_s / 1e9
-    traffic = counter_traffic(args.config, args.index_law)
+    traffic = counter_traffic(args.config, args.index_law) if args.mode == "forward" else None
 
     if args.copy_calibration:
         n = 1 << 28  # 1 GiB of fp32
@@ -207,7 +251,7 @@ def main():
     eb.eb_destroy(h)
 
     cpu = None
-    if args.cpu_budget > 0:
+    if args.cpu_budget > 0 and args.mode == "forward":
         print(f"[bench] CPU oracle baseline ({args.cpu_budget:.0f} s budget)", file=sys.stderr, flush=True)
         reps, el, threads, look, nbytes, use = run_cpu_baseline(w0, args.cpu_budget)
         what = "the whole batch" if use == w0.num_tables else f"the bags of tables 0..{use - 1} of {w0.num_tables}"
@@ -223,7 +267,7 @@ def main():
 
     dtypes = sorted({t.dtype for t in w0.tables})
     line = {
-        "metric": METRIC,
+        "metric": METRIC if args.mode == "forward" else METRIC_BACKWARD,
         "value": round(value, 2),
         "unit": "GB/s",
         "pct_of_peak_hbm": round(100.0 * value / PEAK_HBM_GBS, 2),
@@ -248,9 +292,10 @@ def main():
             "index_dtype": str(w0.indices.dtype).replace("torch.", ""),
             "table_storage": dtypes,
         },
+        "mode": args.mode,
         "roofline": {
             "bound": "hbm",
-            "kernel": KERNEL_NAME,
+            "kernel": KERNEL_NAME if args.mode == "forward" else "eb_backward_update (all its kernels)",
             "achieved": round(achieved, 2),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",

@@ -56,8 +56,9 @@
  * at the same time, forces how workgroups map onto the GPU's XCDs (default:
  * XCD-contiguous for handles of up to 32 tables, round-robin otherwise).
  * EB_BWD_TILE_CHUNKS=c (1..16) fixes the backward's tiles at 64*c sorted
- * positions (default: 64 to 256, from the number of lookups).  Results do not
- * depend on any of these.
+ * positions (default: 64 to 256, from the number of lookups), and
+ * EB_BWD_XCD_REMAP=0|1 its workgroup order (default as for the forward).
+ * Results do not depend on any of these.
  */
 #ifndef EB_H_
 #define EB_H_

@@ -72,6 +72,7 @@ struct BwdArgs {
   int32_t bags_per_wave;  // keys kernel: bags per wavefront
   int32_t groups_per_table;
   int32_t num_waves;
+  int32_t xcd_remap;      // tiles kernel: XCD-contiguous workgroup order
 };
 
 __device__ __forceinline__ int64_t load_offset(const BwdArgs &a, int64_t g) {
@@ -191,12 +192,42 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// The values a row update reads, loaded ahead of the gather that produces
+// the row's gradient: the lane's K table values and the Adagrad state.
+template <int TDT, int K>
+struct RowPrefetch {
+  float w[K];
+  float s;
+};
+
+template <int TDT, int K>
+__device__ __forceinline__ RowPrefetch<TDT, K> prefetch_row(const TableMeta &m, const BwdArgs &a, int64_t row, bool own,
+                                                           int col) {
+  RowPrefetch<TDT, K> p;
+  p.s = a.opt == kOptRowwiseAdagrad ? a.state[m.state_base + row] : 0.0f;
+#pragma unroll
+  for (int i = 0; i < K; ++i) p.w[i] = 0.0f;
+  if (own) {
+    const unsigned char *base = m.data + (uint64_t)row * m.row_stride;
+    if constexpr (TDT == kF32) {
+      const float *wp = reinterpret_cast<const float *>(base) + col;
+#pragma unroll
+      for (int i = 0; i < K; ++i) p.w[i] = wp[i];
+    } else {
+      const _Float16 *wp = reinterpret_cast<const _Float16 *>(base) + col;
+#pragma unroll
+      for (int i = 0; i < K; ++i) p.w[i] = (float)wp[i];
+    }
+  }
+  return p;
+}
+
 // Optimizer step on row `row` of table m.  Lane holds K gradient values for
 // columns [col, col + K) when `own`; the columns of all owning lanes cover
-// the row exactly once.
+// the row exactly once.  `p` holds the row's values read beforehand.
 template <int TDT, int K>
 __device__ __forceinline__ void apply_update(const TableMeta &m, const BwdArgs &a, int64_t row, const float (&g)[K],
-                                             bool own, int col) {
+                                             bool own, int col, const RowPrefetch<TDT, K> &p) {
   float scale = a.lr;
   if (a.opt == kOptRowwiseAdagrad) {
     float sq = 0.0f;
@@ -205,21 +236,20 @@ __device__ __forceinline__ void apply_update(const TableMeta &m, const BwdArgs &
       for (int i = 0; i < K; ++i) sq = fmaf(g[i], g[i], sq);
     }
     sq = wave_sum(sq);
-    float *sp = a.state + m.state_base + row;
-    const float s_new = *sp + sq / (float)m.dim;
+    const float s_new = p.s + sq / (float)m.dim;
     scale = a.lr / (sqrtf(s_new) + a.eps);
-    if ((threadIdx.x & (kWave - 1)) == 0) *sp = s_new;
+    if ((threadIdx.x & (kWave - 1)) == 0) a.state[m.state_base + row] = s_new;
   }
   if (own) {
     unsigned char *base = const_cast<unsigned char *>(m.data) + (uint64_t)row * m.row_stride;
     if constexpr (TDT == kF32) {
       float *wp = reinterpret_cast<float *>(base) + col;
 #pragma unroll
-      for (int i = 0; i < K; ++i) wp[i] = fmaf(-scale, g[i], wp[i]);
+      for (int i = 0; i < K; ++i) wp[i] = fmaf(-scale, g[i], p.w[i]);
     } else {
       _Float16 *wp = reinterpret_cast<_Float16 *>(base) + col;
 #pragma unroll
-      for (int i = 0; i < K; ++i) wp[i] = (_Float16)fmaf(-scale, g[i], (float)wp[i]);
+      for (int i = 0; i < K; ++i) wp[i] = (_Float16)fmaf(-scale, g[i], p.w[i]);
     }
   }
 }
@@ -259,6 +289,15 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
 
   float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   bool first_run = true;
+  // Values of the row the current run will update, read when the run starts
+  // (a run that crossed into this tile, or goes on past it, updates nothing
+  // here); no other wavefront writes that row during this launch.
+  RowPrefetch<TDT, KEEP> pre;
+  auto start_run = [&](uint32_t rkey) {
+    const bool valid = rkey >= kmin && rkey < sentinel;
+    if (valid && !(first_run && rkey == before) && rkey != after)
+      pre = prefetch_row<TDT, KEEP>(m, a, (int64_t)(rkey - kmin), own, col);
+  };
   // Finish the run with key rkey whose terms are all in acc: update its row,
   // or leave a partial when it crosses a tile boundary.
   auto finish = [&](uint32_t rkey, bool reaches_end) {
@@ -271,7 +310,7 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
 #pragma unroll
       for (int i = 0; i < KEEP; ++i) gk[i] = acc[i];
       if (!started_before && !continues_after) {
-        apply_update<TDT, KEEP>(m, a, (int64_t)(rkey - kmin), gk, own, col);
+        apply_update<TDT, KEEP>(m, a, (int64_t)(rkey - kmin), gk, own, col, pre);
       } else if (own) {
         float *slot = a.carry + ((int64_t)2 * w + (started_before ? 0 : 1)) * a.max_dim + col;
 #pragma unroll
@@ -323,6 +362,7 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
       const uint64_t above = a0 + 1 < kWave ? heads & (~0ull << (a0 + 1)) : 0ull;
       const int z = above ? (int)__builtin_ctzll(above) : n;
       const uint32_t rkey = __builtin_amdgcn_readlane(key, a0);
+      if (!(a0 == 0 && pending)) start_run(rkey);  // a pending run was started in an earlier chunk
       gather_range<kF32, LPR, true>(gm, a.ctx, ch, a0, z - a0, acc, colb, colok);
       if (z < n || last_chunk) {
         finish(rkey, z == n);
@@ -342,9 +382,14 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
     tile_body<TDT, (1 << (LOG2))>(a, m, t, w, w - a.tile_start[t]);             \
     break;
 
+// Tiles are numbered table by table; with XCD-contiguous workgroup order each
+// XCD walks one eighth of the tables, so its L2 keeps those tables' gradient
+// rows (B x D fp32 per table, re-read by every run of the table) instead of
+// all eight XCDs pulling the same table's gradient through the fabric.
 template <int TDT, int LOG2>
 __global__ __launch_bounds__(kBlock) void eb_bwd_tiles_kernel(BwdArgs a) {
-  const int32_t w = (int32_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const uint32_t blk = a.xcd_remap ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x;
+  const int32_t w = (int32_t)blk * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if (w >= a.tile_start[a.num_tables]) return;
   const int32_t t = table_of_tile(a, w);
   const TableMeta m = a.meta[t];
@@ -364,7 +409,9 @@ __global__ __launch_bounds__(kBlock) void eb_bwd_tiles_kernel(BwdArgs a) {
 
 // Step 4: a run that starts in tile w and goes on past it: sum its partial
 // from tile w and the head partials of the tiles it covers, in tile order,
-// then update its row.  Lane l handles columns [4l, 4l + 4).
+// then update its row.  The run's last tile is found 64 tiles at a time (one
+// per lane); the partials are summed with eight loads in flight.  Lane l
+// handles columns [4l, 4l + 4).
 template <int TDT>
 __global__ __launch_bounds__(kBlock) void eb_bwd_fixup_kernel(BwdArgs a) {
   const int32_t w = (int32_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -384,25 +431,48 @@ __global__ __launch_bounds__(kBlock) void eb_bwd_fixup_kernel(BwdArgs a) {
     return (e < p1 ? e : p1) - 1;
   };
   const uint32_t key = a.skeys[tile_last(k0)];
+  // last tile of the run: the first tile kk > k0 that the run does not fill
+  // and go on past (the table's last tile never goes on)
+  int32_t kend = ntiles - 1;
+  for (int32_t base = k0 + 1; base < ntiles; base += kWave) {
+    const int32_t kk = base + lane;
+    bool stop = false;
+    if (kk < ntiles) {
+      const int32_t wk = a.tile_start[t] + kk;
+      stop = !((a.tile_flags[wk] & kTileContinues) && a.skeys[tile_last(kk)] == key);
+    }
+    const uint64_t hit = __ballot(kk < ntiles && stop);
+    if (hit) {
+      kend = base + (int32_t)__builtin_ctzll(hit);
+      break;
+    }
+  }
   const int col = 4 * lane;
   const bool own = col < m.dim;
+  const RowPrefetch<TDT, 4> pre = prefetch_row<TDT, 4>(m, a, (int64_t)(key - m.key_base), own, col);
   float g[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (own) {
-    const float *slot = a.carry + ((int64_t)2 * w + 1) * a.max_dim + col;
+    const f32x4 v = *reinterpret_cast<const f32x4 *>(a.carry + ((int64_t)2 * w + 1) * a.max_dim + col);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) g[i] = slot[i];
-  }
-  for (int32_t kk = k0 + 1; kk < ntiles; ++kk) {
-    const int32_t wk = a.tile_start[t] + kk;
-    if (own) {
-      const float *slot = a.carry + ((int64_t)2 * wk) * a.max_dim + col;
+    for (int i = 0; i < 4; ++i) g[i] = v[i];
+    constexpr int kBatch = 8;
+    for (int32_t kk = k0 + 1; kk <= kend; kk += kBatch) {
+      f32x4 v8[kBatch];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) g[i] += slot[i];
+      for (int j = 0; j < kBatch; ++j) {
+        const int32_t kj = kk + j <= kend ? kk + j : kend;  // past the end: re-read the last, not added
+        v8[j] = *reinterpret_cast<const f32x4 *>(a.carry + ((int64_t)2 * (a.tile_start[t] + kj)) * a.max_dim + col);
+      }
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        if (kk + j <= kend) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) g[i] += v8[j][i];
+        }
+      }
     }
-    // the run goes on past tile kk only if it fills that tile and the tile continues
-    if (!((a.tile_flags[wk] & kTileContinues) && a.skeys[tile_last(kk)] == key)) break;
   }
-  apply_update<TDT, 4>(m, a, (int64_t)(key - m.key_base), g, own, col);
+  apply_update<TDT, 4>(m, a, (int64_t)(key - m.key_base), g, own, col, pre);
 }
 
 typedef void (*KernelFn)(BwdArgs);
@@ -571,6 +641,7 @@ eb_status eb_backward_update(const eb_tables *h, eb_tensor indices, eb_tensor of
   a.eps = eps;
   a.tile_size = L.tile_size;
   a.max_dim = h->max_dim;
+  a.xcd_remap = h->bwd_xcd_remap;
   int64_t k = 1;
   {
     const int64_t per_slot = num_bags / kResidentWaves;

@@ -394,6 +394,7 @@ struct eb_tables {
   int64_t sum_dim;
   int32_t backward_ok;    // every table fp32/fp16 with dim <= 256, sort keys fit in 32 bits
   int32_t bwd_tile_chunks;  // 0: chosen per call; else backward tiles of this many 64-position chunks
+  int32_t bwd_xcd_remap;    // backward tiles in XCD-contiguous order
   int32_t max_dim;
   int64_t total_rows;     // sum of the tables' row counts (optimizer-state length)
   eb::TableMeta *d_meta;  // device: descriptors, then the error word, then the zero row

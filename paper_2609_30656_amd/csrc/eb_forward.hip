@@ -342,6 +342,8 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   h->checked = (chk && chk[0] == '1') ? 1 : 0;
   const char *remap = getenv("EB_XCD_REMAP");
   h->xcd_remap = remap ? (remap[0] == '1') : (num_tables <= kRemapMaxTables);
+  const char *bremap = getenv("EB_BWD_XCD_REMAP");
+  h->bwd_xcd_remap = bremap ? (bremap[0] == '1') : (num_tables <= kRemapMaxTables);
   const char *btc = getenv("EB_BWD_TILE_CHUNKS");
   h->bwd_tile_chunks = btc ? atoi(btc) : 0;
   if (h->bwd_tile_chunks < 0 || h->bwd_tile_chunks > 16) h->bwd_tile_chunks = 0;
