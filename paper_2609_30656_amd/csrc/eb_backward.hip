@@ -254,10 +254,114 @@ __device__ __forceinline__ void apply_update(const TableMeta &m, const BwdArgs &
   }
 }
 
+// Complete runs inside one chunk, several at once: the runs that start at
+// heads h_0 < ... < h_nruns of the chunk (run k is [h_k, h_k+1)) go to lane
+// groups of LPRS lanes, one run per group, G = 64 / LPRS runs per round.  A
+// group walks its run's entries in order (P 16-byte loads per lane per
+// gradient row), then applies the optimizer step to the run's row itself:
+// no cross-group reduction, and one memory round trip per round of G runs.
+template <int TDT, int LPR_NAT>
+__device__ __forceinline__ void short_runs(const BwdArgs &a, const TableMeta &m, const TableMeta &gm, const Chunk &ch,
+                                           uint32_t key, uint64_t hs, int nruns, int *starts) {
+  constexpr int LPRS = LPR_NAT < 32 ? LPR_NAT : 32;
+  constexpr int P = LPR_NAT / LPRS;
+  constexpr int G = kWave / LPRS;
+  constexpr int US = P >= 2 ? 2 : 4;
+  constexpr int NV = 4 * P;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int grp = lane / LPRS, sub = lane % LPRS;
+  const uint32_t kmin = m.key_base, sentinel = m.key_base + (uint32_t)m.num_rows;
+  // position of the head of each rank (rank = heads below it)
+  if ((hs >> lane) & 1ull) starts[__builtin_popcountll(hs & ((1ull << lane) - 1ull))] = lane;
+  __builtin_amdgcn_wave_barrier();
+  const int colb0 = sub * 16 * P;
+  for (int r0 = 0; r0 < nruns; r0 += G) {
+    const int k = r0 + grp;
+    const bool active = k < nruns;
+    const int st = active ? starts[k] : 0;
+    const int len = active ? starts[k + 1] - st : 0;
+    const uint32_t rkey = (uint32_t)__shfl((int)key, st & (kWave - 1));
+    const bool valid = active && rkey >= kmin && rkey < sentinel;
+    const int64_t row = valid ? (int64_t)(rkey - kmin) : 0;
+    int maxlen = len;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) maxlen = max(maxlen, __shfl_xor(maxlen, o));
+    // the row's values and state, read before the gradient gather
+    float wv[NV];
+    float s_old = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) wv[i] = 0.0f;
+    const int col0 = colb0 / 4;
+    if (valid) {
+      if (a.opt == kOptRowwiseAdagrad) s_old = a.state[m.state_base + row];
+      const unsigned char *base = m.data + (uint64_t)row * m.row_stride;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        if (col0 + i < m.dim) {
+          if constexpr (TDT == kF32) wv[i] = reinterpret_cast<const float *>(base)[col0 + i];
+          else wv[i] = (float)reinterpret_cast<const _Float16 *>(base)[col0 + i];
+        }
+      }
+    }
+    float acc[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) acc[i] = 0.0f;
+    for (int u = 0; u < maxlen; u += US) {
+      u32x4 v[US][P];
+      float c[US];
+#pragma unroll
+      for (int q = 0; q < US; ++q) {
+        const int e = st + u + q;
+        const uint32_t b = (uint32_t)__shfl((int)ch.row, e & (kWave - 1));
+        c[q] = __shfl(ch.w, e & (kWave - 1));
+        const bool ok = valid && (u + q < len) && b != kBadRow;
+        gbyte *pr = ok ? (gbyte *)gm.data + (uint64_t)b * gm.row_stride : (gbyte *)a.ctx.zero;
+#pragma unroll
+        for (int pp = 0; pp < P; ++pp) {
+          const int cb = colb0 + 16 * pp;
+          v[q][pp] = load_slice<kF32>((cb < gm.code_bytes ? pr : (gbyte *)a.ctx.zero) + cb);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < US; ++q) {
+#pragma unroll
+        for (int pp = 0; pp < P; ++pp) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[4 * pp + i] = fmaf(c[q], __uint_as_float(v[q][pp][i]), acc[4 * pp + i]);
+        }
+      }
+    }
+    float scale = a.lr;
+    if (a.opt == kOptRowwiseAdagrad) {
+      float sq = 0.0f;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) sq = fmaf(acc[i], acc[i], sq);  // zero past the row's end
+#pragma unroll
+      for (int o = 1; o < LPRS; o <<= 1) sq += __shfl_xor(sq, o);
+      const float s_new = s_old + sq / (float)m.dim;
+      scale = a.lr / (sqrtf(s_new) + a.eps);
+      if (valid && sub == 0) a.state[m.state_base + row] = s_new;
+    }
+    if (valid) {
+      unsigned char *base = const_cast<unsigned char *>(m.data) + (uint64_t)row * m.row_stride;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        if (col0 + i < m.dim) {
+          const float nw = fmaf(-scale, acc[i], wv[i]);
+          if constexpr (TDT == kF32) reinterpret_cast<float *>(base)[col0 + i] = nw;
+          else reinterpret_cast<_Float16 *>(base)[col0 + i] = (_Float16)nw;
+        }
+      }
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+}
+
 // Step 3b: pool the runs of one tile and update their rows (or leave
 // partials).  LPR lanes hold one fp32 gradient row of 4*dim bytes.
 template <int TDT, int LPR>
-__device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, int32_t t, int32_t w, int32_t k) {
+__device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, int32_t t, int32_t w, int32_t k,
+                                          int *starts) {
   using R = Reduce<kF32, LPR>;
   constexpr int KEEP = R::KEEP;
   const int lane = threadIdx.x & (kWave - 1);
@@ -358,20 +462,42 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
       pending = false;
     }
     int a0 = 0;
-    while (a0 < n) {
-      const uint64_t above = a0 + 1 < kWave ? heads & (~0ull << (a0 + 1)) : 0ull;
-      const int z = above ? (int)__builtin_ctzll(above) : n;
-      const uint32_t rkey = __builtin_amdgcn_readlane(key, a0);
-      if (!(a0 == 0 && pending)) start_run(rkey);  // a pending run was started in an earlier chunk
-      gather_range<kF32, LPR, true>(gm, a.ctx, ch, a0, z - a0, acc, colb, colok);
+    if (!(heads & 1ull)) {
+      // the chunk opens inside a run: the pending one, or the tile's first
+      // run when it started in the previous tile
+      const int z = heads ? (int)__builtin_ctzll(heads) : n;
+      const uint32_t rkey = __builtin_amdgcn_readlane(key, 0);
+      if (!pending) start_run(rkey);
+      gather_range<kF32, LPR, true>(gm, a.ctx, ch, 0, z, acc, colb, colok);
       if (z < n || last_chunk) {
         finish(rkey, z == n);
         pending = false;
       } else {
-        pending = true;  // the run may go on in the next chunk
+        pending = true;
         pending_key = rkey;
       }
       a0 = z;
+    }
+    if (a0 < n) {
+      // runs starting at heads: all but the last are complete inside this
+      // chunk and are updated here, several at once
+      const uint64_t hs = heads;
+      const int nheads = __builtin_popcountll(hs);
+      if (nheads > 1) {
+        short_runs<TDT, LPR>(a, m, gm, ch, key, hs, nheads - 1, starts);
+        first_run = false;
+      }
+      const int hl = 63 - __builtin_clzll(hs);
+      const uint32_t rkey = __builtin_amdgcn_readlane(key, hl);
+      start_run(rkey);
+      gather_range<kF32, LPR, true>(gm, a.ctx, ch, hl, n - hl, acc, colb, colok);
+      if (last_chunk) {
+        finish(rkey, true);
+        pending = false;
+      } else {
+        pending = true;
+        pending_key = rkey;
+      }
     }
     prev_last = __builtin_amdgcn_readlane(key, n - 1);
   }
@@ -379,7 +505,7 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
 
 #define EB_BWD_LPR(LOG2)                                                        \
   case LOG2:                                                                    \
-    tile_body<TDT, (1 << (LOG2))>(a, m, t, w, w - a.tile_start[t]);             \
+    tile_body<TDT, (1 << (LOG2))>(a, m, t, w, w - a.tile_start[t], starts);     \
     break;
 
 // Tiles are numbered table by table; with XCD-contiguous workgroup order each
@@ -394,8 +520,10 @@ __global__ __launch_bounds__(kBlock) void eb_bwd_tiles_kernel(BwdArgs a) {
   const int32_t t = table_of_tile(a, w);
   const TableMeta m = a.meta[t];
   if (m.kind / 8 != TDT) return;
+  __shared__ int run_starts[kWavesPerBlock][kWave + 1];
+  int *starts = run_starts[threadIdx.x / kWave];
   if constexpr (LOG2 >= 0) {
-    tile_body<TDT, (1 << LOG2)>(a, m, t, w, w - a.tile_start[t]);
+    tile_body<TDT, (1 << LOG2)>(a, m, t, w, w - a.tile_start[t], starts);
   } else {
     switch (log2_lanes_per_row(4 * m.dim)) {
       EB_BWD_LPR(0) EB_BWD_LPR(1) EB_BWD_LPR(2) EB_BWD_LPR(3) EB_BWD_LPR(4) EB_BWD_LPR(5) EB_BWD_LPR(6)
