@@ -5,8 +5,8 @@ bench.py may import this package.  The product path (libeb and its binding)
 never does.  The arithmetic lives in eb_oracle.c (plain C, fp64
 accumulation); this module only marshals numpy arrays into it.
 """
-from .oracle import (OracleError, OracleTable, build, double_to_half, ebo_backward_update, ebo_forward,
+from .oracle import (OracleError, OracleTable, build, double_to_half, ebo_backward_update, ebo_fm, ebo_forward,
                      half_to_double, lib_path, max_threads)
 
-__all__ = ["OracleError", "OracleTable", "build", "double_to_half", "ebo_backward_update", "ebo_forward",
+__all__ = ["OracleError", "OracleTable", "build", "double_to_half", "ebo_backward_update", "ebo_fm", "ebo_forward",
            "half_to_double", "lib_path", "max_threads"]

@@ -457,3 +457,57 @@ int ebo_backward_update(const ebo_table *tables, int32_t num_tables, const void 
   }
   return EBO_OK;
 }
+
+/* ========================================================================
+ * Factorization-machine cross term over the pooled embeddings (test
+ * infrastructure).
+ *
+ * The paper's DLRM is DeepFM-based; its inter_arch.fm submodule computes the
+ * factorization-machine cross term over the embeddings that sparse_arch
+ * produces (Sec. IV-A.2, inter_arch zoom-in), the second-order term of the
+ * factorization machine the Introduction cites (Rendle, 2010).  With each
+ * categorical feature (field) f of example b represented by its pooled
+ * embedding e_{b,f} (D values, all fields the same D), the term is the sum of
+ * the inner products of every unordered pair of distinct fields:
+ *
+ *   y_b = sum_{f < f'} sum_d e_{b,f,d} * e_{b,f',d}
+ *
+ * pooled is [B, ld] with field f in columns [f*D, f*D + D) (the pooled
+ * output's layout).  Every product of two fp32 values is exact in fp64; the
+ * pairs are summed in fp64 in (f, f', d) order and returned unrounded.
+ *
+ * scale (optional): M_b = sum_d (sum_f A_{b,f,d})^2 with A the per-element
+ * error scale of the pooled values (asum of ebo_forward), the quantity a
+ * computed y_b's rounding error is bounded against.
+ * ======================================================================== */
+int ebo_fm(const float *pooled, int64_t ld, int32_t num_fields, int32_t dim, int64_t num_examples,
+           const double *asum, double *y, double *scale, int32_t num_threads) {
+  if (!pooled || !y || num_fields < 1 || dim < 1 || num_examples < 0) return EBO_ERR_INVALID_ARG;
+  if (ld < (int64_t)num_fields * dim) return EBO_ERR_SHAPE;
+  int nthreads = 1;
+#ifdef _OPENMP
+  nthreads = num_threads > 0 ? num_threads : omp_get_max_threads();
+#endif
+  (void)nthreads;
+#pragma omp parallel for schedule(dynamic, 16) num_threads(nthreads)
+  for (int64_t b = 0; b < num_examples; ++b) {
+    const float *e = pooled + b * ld;
+    double acc = 0.0;
+    for (int32_t f = 0; f < num_fields; ++f)
+      for (int32_t g = f + 1; g < num_fields; ++g)
+        for (int32_t d = 0; d < dim; ++d)
+          acc += (double)e[(int64_t)f * dim + d] * (double)e[(int64_t)g * dim + d];
+    y[b] = acc;
+    if (scale) {
+      const double *a = asum + b * ld;
+      double m = 0.0;
+      for (int32_t d = 0; d < dim; ++d) {
+        double col = 0.0;
+        for (int32_t f = 0; f < num_fields; ++f) col += a[(int64_t)f * dim + d];
+        m += col * col;
+      }
+      scale[b] = m;
+    }
+  }
+  return EBO_OK;
+}

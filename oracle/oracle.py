@@ -84,6 +84,9 @@ def _load():
             ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
             ctypes.c_float, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
         ]
+        lib.ebo_fm.restype = ctypes.c_int
+        lib.ebo_fm.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
+                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]
         _lib = lib
     return _lib
 
@@ -263,3 +266,31 @@ def ebo_backward_update(
         n = int(reps[t].num_rows)
         out[t] = (rows[:n], g[:n], s[:n], c[:n])
     return out
+
+
+def ebo_fm(pooled: np.ndarray, num_fields: int, dim: int, asum: Optional[np.ndarray] = None,
+           num_threads: int = 0):
+    """Factorization-machine cross term of each example over its pooled field
+    embeddings: y[b] = sum_{f<f'} <e_{b,f}, e_{b,f'}> in fp64 (see eb_oracle.c).
+
+    pooled: fp32 [B, ld >= num_fields * dim], field f in columns [f*dim, (f+1)*dim).
+    Returns y (fp64 [B]), or (y, scale) when asum (fp64, pooled's shape) is given.
+    """
+    lib = _load()
+    pooled = np.ascontiguousarray(pooled, dtype=np.float32)
+    if pooled.ndim != 2:
+        raise ValueError("pooled must be 2-D")
+    B, ld = pooled.shape
+    y = np.empty(B, np.float64)
+    scale = None
+    if asum is not None:
+        asum = np.ascontiguousarray(asum, dtype=np.float64)
+        if asum.shape != pooled.shape:
+            raise ValueError("asum must have pooled's shape")
+        scale = np.empty(B, np.float64)
+    rc = lib.ebo_fm(pooled.ctypes.data, ld, int(num_fields), int(dim), B,
+                    asum.ctypes.data if asum is not None else None, y.ctypes.data,
+                    scale.ctypes.data if scale is not None else None, int(num_threads))
+    if rc != 0:
+        raise OracleError(rc)
+    return y if scale is None else (y, scale)
