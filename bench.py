@@ -2,7 +2,9 @@
 """Benchmark: pooled EmbeddingBag forward on one MI355X.
 
 One step = one eb_forward over one batch of the workload (all tables, all
-bags).  Three independently seeded index batches over the same tables are
+bags); with --mode fm, one eb_forward_fm (the same lookup with the FM cross
+term fused into the store); with --mode backward, one eb_backward_update with
+row-wise Adagrad.  Three independently seeded index batches over the same tables are
 rotated so consecutive steps do not replay identical lookups.  Tables,
 indices and offsets are resident in HBM before the timed region starts.
 
@@ -18,7 +20,6 @@ Algorithmic bytes per step = gathered row bytes (every lookup, duplicates
 counted) + index bytes + offset bytes + weight bytes + output bytes.
 """
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -31,38 +32,8 @@ PEAK_HBM_GBS = 8000.0
 METRIC = "EmbeddingBag fwd achieved HBM GB/s (% of peak) + pooled lookups/sec, 1 GPU"
 METRIC_BACKWARD = ("EmbeddingBag bwd + fused row-wise Adagrad update achieved HBM GB/s (% of peak) + "
                    "lookups/sec, 1 GPU")
-KERNEL_NAME = "eb_pool_kernel"
+METRIC_FM = ("EmbeddingBag fwd + fused FM cross term achieved HBM GB/s (% of peak) + pooled lookups/sec, 1 GPU")
 SAMPLE = 7
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_30656_amd", "csrc", f) for f in ("eb_device.h", "eb_forward.hip")]
-
-
-def kernel_source_hash() -> str:
-    """Hash of the sources the forward kernel is built from."""
-    h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()[:16]
-
-
-def counter_traffic(config: str, index_law: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", f"eb_pool_kernel_{config}_{index_law}_pmc.txt")
-    if not os.path.exists(path):
-        return None
-    vals = {}
-    with open(path) as f:
-        for line in f:
-            if "=" in line and not line.startswith("#"):
-                k, v = line.split("=", 1)
-                vals[k.strip()] = v.strip()
-    if vals.get("kernel_source_sha256_16") != kernel_source_hash():
-        return None
-    try:
-        return float(vals["hbm_bytes_per_launch"])
-    except (KeyError, ValueError):
-        return None
 
 
 def backward_algorithmic_bytes(w) -> int:
@@ -93,10 +64,12 @@ def cpu_cores() -> int:
         return os.cpu_count() or 1
 
 
-def run_cpu_baseline(w, budget_s: float, host_bytes_cap: float = 3e9):
+def run_cpu_baseline(w, budget_s: float, host_bytes_cap: float = 3e9, fm: bool = False):
     """Time the oracle (as it stands) on the bags of the first tables of `w`
     whose rows fit in `host_bytes_cap` bytes of host memory (all tables for the
-    smaller workloads), repeated until `budget_s` seconds have passed.
+    smaller workloads), repeated until `budget_s` seconds have passed.  With
+    fm, each pass also runs the oracle's FM cross term over those tables'
+    pooled fields.
     Returns (reps, seconds, threads, lookups per rep, algorithmic bytes per rep,
     tables used)."""
     import numpy as np
@@ -123,9 +96,16 @@ def run_cpu_baseline(w, budget_s: float, host_bytes_cap: float = 3e9):
     esz = w.indices.element_size()
     nbytes = sum(int(lens[t]) * w.tables[t].row_bytes + B * w.tables[t].dim * 4 for t in range(use))
     nbytes += look * (esz + (4 if wt is not None else 0)) + (use * B + 1) * esz
+    if fm:
+        nbytes += 4 * B
+    D = w.tables[0].dim
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.ebo_forward(tabs, idx, off, wt, w.pooling, bags=bags, num_threads=threads)
+        out = oracle.ebo_forward(tabs, idx, off, wt, w.pooling, bags=bags, num_threads=threads)
+        if fm:
+            if bags is not None:  # bag k = (table k // B, example k % B): fields side by side per example
+                out = out[:, :D].reshape(use, B, D).transpose(1, 0, 2).reshape(B, use * D)
+            oracle.ebo_fm(out, use, D, num_threads=threads)
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s:
@@ -144,8 +124,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing (0 = skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (to scale rocprofv3 byte counters)")
-    ap.add_argument("--mode", default="forward", choices=["forward", "backward"],
-                    help="backward: eb_backward_update with row-wise Adagrad instead of eb_forward")
+    ap.add_argument("--mode", default="forward", choices=["forward", "fm", "backward"],
+                    help="fm: eb_forward_fm (FM cross term fused into the store); "
+                         "backward: eb_backward_update with row-wise Adagrad")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -156,6 +137,7 @@ def main():
     import torch
 
     from paper_2609_30656_amd import eb
+    from paper_2609_30656_amd.profiling import KERNELS, counter_traffic
     from paper_2609_30656_amd.workload import CONFIGS, make_workload
 
     dev = torch.device("cuda:0")
@@ -171,6 +153,8 @@ def main():
     out = torch.empty((w0.batch, w0.sum_dim), dtype=torch.float32, device=dev)
     if args.mode == "forward":
         algo = [b.algorithmic_bytes() for b in batches]
+    elif args.mode == "fm":
+        algo = [b.algorithmic_bytes() + 4 * b.batch for b in batches]
     else:
         algo = [backward_algorithmic_bytes(b) for b in batches]
     nlook = [b.num_indices for b in batches]
@@ -183,12 +167,23 @@ def main():
               eb.POOLING[b.pooling]) for b in batches]
     o = eb._as_tensor(out)
 
+    def forward_step(k):
+        i, f, wt, mode = calls[k % 3]
+        st = lib.eb_forward(h.ptr, i, f, wt, mode, o)
+        if st != eb.EB_OK:
+            raise eb.EBError(st, "eb_forward")
+
     if args.mode == "forward":
+        step = forward_step
+    elif args.mode == "fm":
+        fm_out = torch.empty(w0.batch, dtype=torch.float32, device=dev)
+        fm_t = eb._as_tensor(fm_out)
+
         def step(k):
             i, f, wt, mode = calls[k % 3]
-            st = lib.eb_forward(h.ptr, i, f, wt, mode, o)
+            st = lib.eb_forward_fm(h.ptr, i, f, wt, mode, o, fm_t)
             if st != eb.EB_OK:
-                raise eb.EBError(st, "eb_forward")
+                raise eb.EBError(st, "eb_forward_fm")
     else:
         gen = torch.Generator(device=dev)
         gen.manual_seed(5)
@@ -237,7 +232,30 @@ def main():
     look_total = sum(nlook[k % 3] for k in range(args.steps))
     value = bytes_total / wall / 1e9
     achieved = kern_bytes / kern_avg_s / 1e9
-    traffic = counter_traffic(args.config, args.index_law) if args.mode == "forward" else None
+    traffic = counter_traffic(args.config, args.index_law, args.mode) if args.mode == "forward" else None
+
+    fm_pass = None
+    if args.mode == "fm":
+        # the plain lookup on the same batches, timed the same way: the step's
+        # extra time is the FM pass over the pooled output
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in sample]
+        for k in range(args.warmup):
+            forward_step(k)
+        for (a, b), k in zip(ev, sample):
+            a.record(stream)
+            forward_step(k)
+            b.record(stream)
+        torch.cuda.synchronize()
+        fwd_ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+        pass_bytes = w0.batch * w0.sum_dim * 4 + w0.batch * 4
+        pass_ms = kern_avg_s * 1e3 - fwd_ms
+        fm_pass = {
+            "step_kernels_ms": round(kern_avg_s * 1e3, 5),
+            "forward_only_ms": round(fwd_ms, 5),
+            "pass_ms_by_difference": round(pass_ms, 5),
+            "pass_bytes": pass_bytes,
+            "pass_GBps": round(pass_bytes / (pass_ms * 1e-3) / 1e9, 1) if pass_ms > 0 else None,
+        }
 
     if args.copy_calibration:
         n = 1 << 28  # 1 GiB of fp32
@@ -251,10 +269,13 @@ def main():
     eb.eb_destroy(h)
 
     cpu = None
-    if args.cpu_budget > 0 and args.mode == "forward":
+    if args.cpu_budget > 0 and args.mode in ("forward", "fm"):
         print(f"[bench] CPU oracle baseline ({args.cpu_budget:.0f} s budget)", file=sys.stderr, flush=True)
-        reps, el, threads, look, nbytes, use = run_cpu_baseline(w0, args.cpu_budget)
+        fm = args.mode == "fm"
+        reps, el, threads, look, nbytes, use = run_cpu_baseline(w0, args.cpu_budget, fm=fm)
         what = "the whole batch" if use == w0.num_tables else f"the bags of tables 0..{use - 1} of {w0.num_tables}"
+        if fm:
+            what += " plus the FM cross term over those fields"
         cpu = {
             "value": round(nbytes * reps / el / 1e9, 4),
             "unit": "GB/s",
@@ -267,7 +288,7 @@ def main():
 
     dtypes = sorted({t.dtype for t in w0.tables})
     line = {
-        "metric": METRIC if args.mode == "forward" else METRIC_BACKWARD,
+        "metric": {"forward": METRIC, "fm": METRIC_FM, "backward": METRIC_BACKWARD}[args.mode],
         "value": round(value, 2),
         "unit": "GB/s",
         "pct_of_peak_hbm": round(100.0 * value / PEAK_HBM_GBS, 2),
@@ -295,7 +316,8 @@ def main():
         "mode": args.mode,
         "roofline": {
             "bound": "hbm",
-            "kernel": KERNEL_NAME if args.mode == "forward" else "eb_backward_update (all its kernels)",
+            "kernel": {"forward": KERNELS["forward"][0], "fm": "eb_forward_fm (eb_pool_kernel, then eb_fm_kernel)",
+                       "backward": "eb_backward_update (all its kernels)"}[args.mode],
             "achieved": round(achieved, 2),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
@@ -306,6 +328,8 @@ def main():
         },
         "cpu_baseline": cpu,
     }
+    if fm_pass is not None:
+        line["fm_pass"] = fm_pass
     print(json.dumps(line), flush=True)
 
 

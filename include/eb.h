@@ -170,6 +170,36 @@ eb_status eb_forward(const eb_tables *tables, eb_tensor indices,
                      eb_pooling pooling, eb_tensor out);
 
 /*
+ * The factorization-machine cross term of each example over its pooled
+ * embeddings.  The DeepFM-based DLRM of the paper feeds sparse_arch's pooled
+ * embeddings to inter_arch.fm, which computes the FM cross term (Sec. IV-A.2,
+ * inter_arch zoom-in); with field f (table f) of example b represented by its
+ * pooled embedding e_{b,f} (the FM second-order term over fields, Rendle 2010):
+ *   fm_out[b] = sum_{f < f'} <e_{b,f}, e_{b,f'}>
+ *             = 1/2 sum_d [ (sum_f e_{b,f,d})^2 - sum_f e_{b,f,d}^2 ]
+ * evaluated in fp32 in one pass over the pooled values (each read once).  The
+ * result does not depend on thread scheduling; a handle with one table gives
+ * exactly +0.0.  Every table of the handle must have the same dim (else
+ * EB_ERR_SHAPE); storage types may differ.
+ *   pooled:  EB_T_F32 [B * T * D], row-major [B, T*D] as eb_forward writes it,
+ *            16-byte aligned; B = numel / (T*D) must be an integer >= 1
+ *            (else EB_ERR_SHAPE).
+ *   fm_out:  EB_T_F32 [B], 4-byte aligned (EB_ERR_SHAPE if numel != B,
+ *            EB_ERR_INVALID_ARG if NULL).  Every element is written.
+ * Asynchronous on the handle's stream; allocates nothing.
+ */
+eb_status eb_fm_cross(const eb_tables *tables, eb_tensor pooled, eb_tensor fm_out);
+
+/*
+ * eb_forward followed by eb_fm_cross on its output, on the handle's stream.
+ * out receives exactly what eb_forward writes; fm_out is as for eb_fm_cross.
+ * Checked mode as for eb_forward.  Argument errors are those of both calls.
+ */
+eb_status eb_forward_fm(const eb_tables *tables, eb_tensor indices,
+                        eb_tensor offsets, eb_tensor per_sample_weights,
+                        eb_pooling pooling, eb_tensor out, eb_tensor fm_out);
+
+/*
  * Training: backward of eb_forward with a fused row-wise optimizer update.
  *
  * The paper profiles each submodule's forward and backward pass (Sec. III-A).

@@ -179,6 +179,42 @@ struct Chunk {
   int n;         // positions in the chunk (wave-uniform)
 };
 
+// Positions [c, min(c + 64, hi)) of the index stream, one per lane, with
+// their weights.  Indices outside [0, num_rows) become kBadRow.  Indices and
+// weights are read once, so they are streamed past the caches.
+template <bool W>
+__device__ __forceinline__ Chunk load_chunk(int32_t num_rows, const void *indices, const float *weights, int idx64,
+                                            int64_t c, int64_t hi) {
+  const int lane = threadIdx.x & (kWave - 1);
+  Chunk k;
+  k.n = (int)((hi - c) < kWave ? (hi - c) : kWave);
+  k.row = kBadRow;
+  k.w = 0.0f;
+  if (lane < k.n) {
+    const int64_t r = idx64 ? __builtin_nontemporal_load(static_cast<const int64_t *>(indices) + c + lane)
+                            : (int64_t)__builtin_nontemporal_load(static_cast<const int32_t *>(indices) + c + lane);
+    if (r >= 0 && r < num_rows) k.row = (uint32_t)r;
+    if constexpr (W) k.w = __builtin_nontemporal_load(weights + c + lane);
+  }
+  return k;
+}
+
+// Store KEEP consecutive pooled values (16-, 8- or 4-byte non-temporal stores:
+// the output is written once and not read back by the lookup).
+template <int KEEP>
+__device__ __forceinline__ void store_slice(float *dst, const float (&v)[KEEP]) {
+  if constexpr (KEEP % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < KEEP; i += 4)
+      __builtin_nontemporal_store(f32x4{v[i], v[i + 1], v[i + 2], v[i + 3]}, reinterpret_cast<f32x4 *>(dst + i));
+  } else if constexpr (KEEP == 2) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    __builtin_nontemporal_store(f32x2{v[0], v[1]}, reinterpret_cast<f32x2 *>(dst));
+  } else {
+    __builtin_nontemporal_store(v[0], dst);
+  }
+}
+
 // Gather steps [s0, s0 + N) of one chunk (RPL rows per step) and add them into
 // this lane's accumulators.  Straight-line code: a lane whose row does not
 // exist (past the chunk's end, outside the table, or a slice past the row's
@@ -380,6 +416,27 @@ __host__ __device__ inline int log2_lanes_per_row(int code_bytes) {
   return l;
 }
 
+// Host side, shared by the entry points that pool (defined in eb_forward.hip;
+// hidden: the library exports only the C ABI).
+#define EB_INTERNAL __attribute__((visibility("hidden")))
+struct FwdShape {
+  int64_t num_bags;
+  int64_t batch;
+  bool weighted;
+};
+// The argument checks of eb_forward (every host-detectable error, before
+// anything is enqueued).
+EB_INTERNAL eb_status check_forward_args(const struct ::eb_tables *h, const eb_tensor &indices, const eb_tensor &offsets,
+                             const eb_tensor &weights, eb_pooling pooling, const eb_tensor &out, FwdShape *sh);
+// Enqueue the pooled lookup (arguments already checked).
+EB_INTERNAL hipError_t launch_forward(const struct ::eb_tables *h, const eb_tensor &indices, const eb_tensor &offsets,
+                                      const eb_tensor &weights, eb_pooling pooling, const eb_tensor &out,
+                                      const FwdShape &sh);
+// Checked mode: clear the device error word before the launches, then read it
+// back (after a stream sync) and turn it into a status.
+EB_INTERNAL hipError_t begin_checked(const struct ::eb_tables *h);
+EB_INTERNAL eb_status end_checked(const struct ::eb_tables *h, hipError_t e);
+
 }  // namespace eb
 
 struct eb_tables {
@@ -396,6 +453,7 @@ struct eb_tables {
   int32_t bwd_tile_chunks;  // 0: chosen per call; else backward tiles of this many 64-position chunks
   int32_t bwd_xcd_remap;    // backward tiles in XCD-contiguous order
   int32_t max_dim;
+  int32_t uniform_dim;    // the dim every table shares, or 0 if they differ
   int64_t total_rows;     // sum of the tables' row counts (optimizer-state length)
   eb::TableMeta *d_meta;  // device: descriptors, then the error word, then the zero row
   eb::TableMeta *h_meta;  // host copy of the descriptors

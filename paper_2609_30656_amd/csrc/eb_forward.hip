@@ -46,23 +46,6 @@ struct FwdArgs {
   int32_t xcd_remap;         // renumber workgroups XCD-contiguously
 };
 
-template <bool W>
-__device__ __forceinline__ Chunk load_chunk(const TableMeta &m, const FwdArgs &a, int64_t c, int64_t hi) {
-  const int lane = threadIdx.x & (kWave - 1);
-  Chunk k;
-  k.n = (int)((hi - c) < kWave ? (hi - c) : kWave);
-  k.row = kBadRow;
-  k.w = 0.0f;
-  if (lane < k.n) {
-    // indices and weights are read once: stream them past the caches
-    const int64_t r = a.idx64 ? __builtin_nontemporal_load(static_cast<const int64_t *>(a.indices) + c + lane)
-                              : (int64_t)__builtin_nontemporal_load(static_cast<const int32_t *>(a.indices) + c + lane);
-    if (r >= 0 && r < m.num_rows) k.row = (uint32_t)r;
-    if constexpr (W) k.w = __builtin_nontemporal_load(a.weights + c + lane);
-  }
-  return k;
-}
-
 // Pool bags [g0, g0 + nb) of one table (batch rows b0 ..) over the 1 KiB column
 // window starting at byte col_base.  The bags' index positions are walked as
 // one stream of chunks of up to 64; the next chunk's indices are loaded before
@@ -108,7 +91,7 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
   int64_t blo, bhi;
   bag_range(0, blo, bhi);
   int64_t c = blo;
-  Chunk cur = load_chunk<W>(m, a, c, bhi);
+  Chunk cur = load_chunk<W>(m.num_rows, a.indices, a.weights, a.idx64, c, bhi);
   while (true) {
     const bool last = c + kWave >= bhi;
     int jn = j;
@@ -122,7 +105,7 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
     }
     const bool more = !last || jn < nb;
     Chunk nxt;
-    if (more) nxt = load_chunk<W>(m, a, cn, nhi);
+    if (more) nxt = load_chunk<W>(m.num_rows, a.indices, a.weights, a.idx64, cn, nhi);
 
     gather_chunk<DT, LPR, W, SPLIT>(m, a.ctx, cur, acc, cb, colb, colok);
 
@@ -144,18 +127,7 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
 #pragma unroll
           for (int i = 0; i < R::KEEP; ++i) outv[i] = outv[i] / fl;
         }
-        float *dst = a.out + (int64_t)(b0 + j) * a.out_ld + m.out_col + colb / Vals<DT>::esize + f;
-        if constexpr (R::KEEP % 4 == 0) {
-#pragma unroll
-          for (int i = 0; i < R::KEEP; i += 4)
-            __builtin_nontemporal_store(f32x4{outv[i], outv[i + 1], outv[i + 2], outv[i + 3]},
-                                        reinterpret_cast<f32x4 *>(dst + i));
-        } else if constexpr (R::KEEP == 2) {
-          typedef float f32x2 __attribute__((ext_vector_type(2)));
-          __builtin_nontemporal_store(f32x2{outv[0], outv[1]}, reinterpret_cast<f32x2 *>(dst));
-        } else {
-          __builtin_nontemporal_store(outv[0], dst);
-        }
+        store_slice<R::KEEP>(a.out + (int64_t)(b0 + j) * a.out_ld + m.out_col + colb / Vals<DT>::esize + f, outv);
       }
 #pragma unroll
       for (int i = 0; i < V; ++i) acc[i] = 0.0f;
@@ -238,6 +210,102 @@ KernelFn pick_kernel(int dt, int log2, bool weighted) {
 }
 
 }  // namespace
+}  // namespace eb
+
+namespace eb {
+
+eb_status check_forward_args(const eb_tables *h, const eb_tensor &indices, const eb_tensor &offsets,
+                             const eb_tensor &weights, eb_pooling pooling, const eb_tensor &out, FwdShape *sh) {
+  if (!h) return EB_ERR_INVALID_ARG;
+  if (indices.elem_type != EB_I32 && indices.elem_type != EB_I64) return EB_ERR_DTYPE;
+  if (offsets.elem_type != indices.elem_type) return EB_ERR_DTYPE;
+  if (out.elem_type != EB_T_F32) return EB_ERR_DTYPE;
+  if (pooling != EB_POOL_SUM && pooling != EB_POOL_MEAN) return EB_ERR_INVALID_ARG;
+  if (!offsets.data || !out.data) return EB_ERR_INVALID_ARG;
+  if (indices.numel < 0 || (indices.numel > 0 && !indices.data)) return EB_ERR_INVALID_ARG;
+  const bool weighted = weights.data != nullptr;
+  if (weighted) {
+    if (weights.elem_type != EB_T_F32) return EB_ERR_DTYPE;
+    if (pooling == EB_POOL_MEAN) return EB_ERR_INVALID_ARG;
+    if (weights.numel != indices.numel) return EB_ERR_SHAPE;
+  }
+  if (offsets.numel < 2 || (offsets.numel - 1) % h->num_tables != 0) return EB_ERR_SHAPE;
+  const int64_t num_bags = offsets.numel - 1;
+  const int64_t batch = num_bags / h->num_tables;
+  if (num_bags > INT32_MAX) return EB_ERR_SHAPE;
+  if (out.numel != batch * h->sum_dim) return EB_ERR_SHAPE;
+  const size_t isz = indices.elem_type == EB_I64 ? 8 : 4;
+  if (reinterpret_cast<uintptr_t>(out.data) % 16 != 0 || reinterpret_cast<uintptr_t>(offsets.data) % isz != 0 ||
+      reinterpret_cast<uintptr_t>(indices.data) % isz != 0 ||
+      (weighted && reinterpret_cast<uintptr_t>(weights.data) % 4 != 0))
+    return EB_ERR_UNSUPPORTED;
+  sh->num_bags = num_bags;
+  sh->batch = batch;
+  sh->weighted = weighted;
+  return EB_OK;
+}
+
+hipError_t launch_forward(const eb_tables *h, const eb_tensor &indices, const eb_tensor &offsets,
+                          const eb_tensor &weights, eb_pooling pooling, const eb_tensor &out, const FwdShape &sh) {
+  FwdArgs a;
+  a.meta = h->d_meta;
+  a.indices = indices.data;
+  a.offsets = offsets.data;
+  a.weights = static_cast<const float *>(weights.data);
+  a.out = static_cast<float *>(const_cast<void *>(out.data));
+  a.ctx.err = h->d_err;
+  a.ctx.zero = h->d_zero;
+  a.ctx.one = 1.0f;
+  a.xcd_remap = h->xcd_remap;
+  a.num_indices = indices.numel;
+  a.out_ld = h->sum_dim;
+  a.num_bags = (int32_t)sh.num_bags;
+  a.batch = (int32_t)sh.batch;
+  a.idx64 = indices.elem_type == EB_I64;
+  a.mean = pooling == EB_POOL_MEAN;
+  int64_t k = h->bags_per_wave;
+  if (k == 0) {
+    // More bags per wavefront hide more latency (each bag's indices arrive
+    // while the previous bag's rows are in flight); fewer leave more
+    // wavefronts to balance the load.  Measured optimum on MI355X: about
+    // sqrt(bags / resident wavefronts).
+    const int64_t per_slot = sh.num_bags / kResidentWaves;
+    k = 1;
+    while ((k + 1) * (k + 1) <= per_slot) ++k;
+    k = k > kMaxBagsPerWave ? kMaxBagsPerWave : k;
+  }
+  a.bags_per_wave = (int32_t)k;
+  a.groups_per_table = (int32_t)((sh.batch + k - 1) / k);
+  const int64_t num_waves = (int64_t)a.groups_per_table * h->num_tables;
+  a.num_waves = (int32_t)num_waves;
+
+  hipError_t e = hipSuccess;
+  const unsigned grid = (unsigned)((num_waves + kWavesPerBlock - 1) / kWavesPerBlock);
+  // one launch per storage type present (one in the usual case)
+  for (int dt = 0; dt < 3 && e == hipSuccess; ++dt) {
+    if (!(h->dtype_mask & (1 << dt))) continue;
+    hipLaunchKernelGGL(pick_kernel(dt, h->single_log2, sh.weighted), dim3(grid), dim3(kBlock), 0, h->stream, a);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+hipError_t begin_checked(const eb_tables *h) {
+  return h->checked ? hipMemsetAsync(h->d_err, 0, sizeof(int), h->stream) : hipSuccess;
+}
+
+eb_status end_checked(const eb_tables *h, hipError_t e) {
+  eb_status st = EB_OK;
+  if (e == hipSuccess && h->checked) {
+    int herr = 0;
+    e = hipMemcpyAsync(&herr, h->d_err, sizeof(int), hipMemcpyDeviceToHost, h->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
+    if (e == hipSuccess && (herr & kErrOffsets)) st = EB_ERR_OFFSETS;
+    else if (e == hipSuccess && (herr & kErrIndex)) st = EB_ERR_INDEX_OOB;
+  }
+  return e != hipSuccess ? EB_ERR_HIP : st;
+}
+
 }  // namespace eb
 
 using namespace eb;
@@ -328,6 +396,7 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   h->dtype_mask = 0;
   h->single_log2 = meta[0].kind % 8;
   h->max_dim = 0;
+  h->uniform_dim = meta[0].dim;
   h->total_rows = rows_before;
   // the backward sorts (table, row) as one 32-bit key: sum of (rows + 1) must fit
   h->backward_ok = key_before <= (uint64_t)UINT32_MAX;
@@ -335,6 +404,7 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
     h->dtype_mask |= 1 << (meta[t].kind / 8);
     if (meta[t].kind != meta[0].kind) h->single_log2 = -1;
     if (meta[t].dim > h->max_dim) h->max_dim = meta[t].dim;
+    if (meta[t].dim != meta[0].dim) h->uniform_dim = 0;
     if (meta[t].kind / 8 == kU8 || meta[t].dim > kMaxBackwardDim) h->backward_ok = 0;
   }
   h->sum_dim = col;
@@ -380,86 +450,16 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
 
 eb_status eb_forward(const eb_tables *h, eb_tensor indices, eb_tensor offsets, eb_tensor per_sample_weights,
                      eb_pooling pooling, eb_tensor out) {
-  if (!h) return EB_ERR_INVALID_ARG;
-  if (indices.elem_type != EB_I32 && indices.elem_type != EB_I64) return EB_ERR_DTYPE;
-  if (offsets.elem_type != indices.elem_type) return EB_ERR_DTYPE;
-  if (out.elem_type != EB_T_F32) return EB_ERR_DTYPE;
-  if (pooling != EB_POOL_SUM && pooling != EB_POOL_MEAN) return EB_ERR_INVALID_ARG;
-  if (!offsets.data || !out.data) return EB_ERR_INVALID_ARG;
-  if (indices.numel < 0 || (indices.numel > 0 && !indices.data)) return EB_ERR_INVALID_ARG;
-  const bool weighted = per_sample_weights.data != nullptr;
-  if (weighted) {
-    if (per_sample_weights.elem_type != EB_T_F32) return EB_ERR_DTYPE;
-    if (pooling == EB_POOL_MEAN) return EB_ERR_INVALID_ARG;
-    if (per_sample_weights.numel != indices.numel) return EB_ERR_SHAPE;
-  }
-  if (offsets.numel < 2 || (offsets.numel - 1) % h->num_tables != 0) return EB_ERR_SHAPE;
-  const int64_t num_bags = offsets.numel - 1;
-  const int64_t batch = num_bags / h->num_tables;
-  if (num_bags > INT32_MAX) return EB_ERR_SHAPE;
-  if (out.numel != batch * h->sum_dim) return EB_ERR_SHAPE;
-  const size_t isz = indices.elem_type == EB_I64 ? 8 : 4;
-  if (reinterpret_cast<uintptr_t>(out.data) % 16 != 0 || reinterpret_cast<uintptr_t>(offsets.data) % isz != 0 ||
-      reinterpret_cast<uintptr_t>(indices.data) % isz != 0 ||
-      (weighted && reinterpret_cast<uintptr_t>(per_sample_weights.data) % 4 != 0))
-    return EB_ERR_UNSUPPORTED;
+  FwdShape sh;
+  const eb_status chk = check_forward_args(h, indices, offsets, per_sample_weights, pooling, out, &sh);
+  if (chk != EB_OK) return chk;
 
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return EB_ERR_HIP;
   if (cur != h->device && hipSetDevice(h->device) != hipSuccess) return EB_ERR_HIP;
-
-  FwdArgs a;
-  a.meta = h->d_meta;
-  a.indices = indices.data;
-  a.offsets = offsets.data;
-  a.weights = static_cast<const float *>(per_sample_weights.data);
-  a.out = static_cast<float *>(const_cast<void *>(out.data));
-  a.ctx.err = h->d_err;
-  a.ctx.zero = h->d_zero;
-  a.ctx.one = 1.0f;
-  a.xcd_remap = h->xcd_remap;
-  a.num_indices = indices.numel;
-  a.out_ld = h->sum_dim;
-  a.num_bags = (int32_t)num_bags;
-  a.batch = (int32_t)batch;
-  a.idx64 = indices.elem_type == EB_I64;
-  a.mean = pooling == EB_POOL_MEAN;
-  int64_t k = h->bags_per_wave;
-  if (k == 0) {
-    // More bags per wavefront hide more latency (each bag's indices arrive
-    // while the previous bag's rows are in flight); fewer leave more
-    // wavefronts to balance the load.  Measured optimum on MI355X: about
-    // sqrt(bags / resident wavefronts).
-    const int64_t per_slot = num_bags / kResidentWaves;
-    k = 1;
-    while ((k + 1) * (k + 1) <= per_slot) ++k;
-    k = k > kMaxBagsPerWave ? kMaxBagsPerWave : k;
-  }
-  a.bags_per_wave = (int32_t)k;
-  a.groups_per_table = (int32_t)((batch + k - 1) / k);
-  const int64_t num_waves = (int64_t)a.groups_per_table * h->num_tables;
-  a.num_waves = (int32_t)num_waves;
-
-  eb_status st = EB_OK;
-  hipError_t e = hipSuccess;
-  if (h->checked) e = hipMemsetAsync(h->d_err, 0, sizeof(int), h->stream);
-  if (e == hipSuccess) {
-    const unsigned grid = (unsigned)((num_waves + kWavesPerBlock - 1) / kWavesPerBlock);
-    // one launch per storage type present (one in the usual case)
-    for (int dt = 0; dt < 3 && e == hipSuccess; ++dt) {
-      if (!(h->dtype_mask & (1 << dt))) continue;
-      hipLaunchKernelGGL(pick_kernel(dt, h->single_log2, weighted), dim3(grid), dim3(kBlock), 0, h->stream, a);
-      e = hipGetLastError();
-    }
-  }
-  if (e == hipSuccess && h->checked) {
-    int herr = 0;
-    e = hipMemcpyAsync(&herr, h->d_err, sizeof(int), hipMemcpyDeviceToHost, h->stream);
-    if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
-    if (e == hipSuccess && (herr & kErrOffsets)) st = EB_ERR_OFFSETS;
-    else if (e == hipSuccess && (herr & kErrIndex)) st = EB_ERR_INDEX_OOB;
-  }
-  if (e != hipSuccess) st = EB_ERR_HIP;
+  hipError_t e = begin_checked(h);
+  if (e == hipSuccess) e = launch_forward(h, indices, offsets, per_sample_weights, pooling, out, sh);
+  const eb_status st = end_checked(h, e);
   if (cur != h->device) (void)hipSetDevice(cur);
   return st;
 }

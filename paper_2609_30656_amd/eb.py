@@ -39,8 +39,8 @@ EB_OPT_SGD, EB_OPT_ROWWISE_ADAGRAD = 0, 1
 TABLE_DTYPES = {"f32": EB_F32, "f16": EB_F16, "int8_rowwise": EB_INT8_ROWWISE}
 POOLING = {"sum": EB_POOL_SUM, "mean": EB_POOL_MEAN}
 OPTIMIZERS = {"sgd": EB_OPT_SGD, "rowwise_adagrad": EB_OPT_ROWWISE_ADAGRAD}
-EXPORTED = ("eb_create_tables", "eb_forward", "eb_destroy", "eb_status_string", "eb_backward_workspace_size",
-            "eb_backward_update")
+EXPORTED = ("eb_create_tables", "eb_forward", "eb_fm_cross", "eb_forward_fm", "eb_destroy", "eb_status_string",
+            "eb_backward_workspace_size", "eb_backward_update")
 
 
 class EBError(RuntimeError):
@@ -79,6 +79,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                          ctypes.POINTER(ctypes.c_void_p)]
         lib.eb_forward.restype = ctypes.c_int
         lib.eb_forward.argtypes = [ctypes.c_void_p, eb_tensor, eb_tensor, eb_tensor, ctypes.c_int, eb_tensor]
+        lib.eb_forward_fm.restype = ctypes.c_int
+        lib.eb_forward_fm.argtypes = [ctypes.c_void_p, eb_tensor, eb_tensor, eb_tensor, ctypes.c_int, eb_tensor,
+                                      eb_tensor]
+        lib.eb_fm_cross.restype = ctypes.c_int
+        lib.eb_fm_cross.argtypes = [ctypes.c_void_p, eb_tensor, eb_tensor]
         lib.eb_destroy.restype = ctypes.c_int
         lib.eb_destroy.argtypes = [ctypes.c_void_p]
         lib.eb_status_string.restype = ctypes.c_char_p
@@ -169,6 +174,27 @@ def eb_forward(tables: EbTables, indices: torch.Tensor, offsets: torch.Tensor,
     if st != EB_OK:
         raise EBError(st, "eb_forward")
     return out
+
+
+def eb_fm_cross(tables: EbTables, pooled: torch.Tensor, fm_out: torch.Tensor) -> torch.Tensor:
+    """FM cross term of each example of a pooled output [B, T*D] into fm_out [B]; returns fm_out."""
+    st = load_library().eb_fm_cross(tables.ptr, _as_tensor(pooled), _as_tensor(fm_out))
+    if st != EB_OK:
+        raise EBError(st, "eb_fm_cross")
+    return fm_out
+
+
+def eb_forward_fm(tables: EbTables, indices: torch.Tensor, offsets: torch.Tensor,
+                  per_sample_weights: Optional[torch.Tensor], pooling, out: torch.Tensor,
+                  fm_out: torch.Tensor) -> torch.Tensor:
+    """eb_forward, then eb_fm_cross on its output into fm_out [B]; returns fm_out."""
+    lib = load_library()
+    mode = POOLING[pooling] if isinstance(pooling, str) else int(pooling)
+    st = lib.eb_forward_fm(tables.ptr, _as_tensor(indices), _as_tensor(offsets), _as_tensor(per_sample_weights),
+                           mode, _as_tensor(out), _as_tensor(fm_out))
+    if st != EB_OK:
+        raise EBError(st, "eb_forward_fm")
+    return fm_out
 
 
 def eb_destroy(tables: EbTables) -> None:
