@@ -8,18 +8,20 @@
 // once with 128-bit loads, converted in registers and summed in fp32; there
 // is no matrix-core work because there is no dense contraction.
 //
-// Execution model (one wavefront of 64 lanes per bag):
-//   * a bag's row is split into 16-byte lane slices; LPR = lanes per row
-//     (the next power of two >= row bytes / 16, at most 64), so one wave-wide
-//     load instruction fetches RPL = 64 / LPR rows of the bag at once;
-//   * the bag's indices are read 64 at a time with one coalesced load and
-//     handed to the lanes of each row group by a cross-lane permute;
-//   * each lane accumulates its slice in fp32 registers; the RPL row groups
-//     are then combined by a butterfly over lanes and one group stores the
-//     pooled vector;
-//   * tables of every storage type and width are served by one launch: the
-//     (dtype, LPR) pair of the bag's table selects a specialised body, which
-//     is uniform across the wave.
+// Execution model:
+//   * a wavefront (64 lanes) pools k consecutive bags of one table, walking
+//     their index positions as one stream of chunks of up to 64 indices, one
+//     coalesced load per chunk, the next chunk's load issued before the
+//     current chunk's rows are gathered;
+//   * a row is split into 16-byte lane slices; LPR = lanes per row (the next
+//     power of two >= row bytes / 16, at most 64), so one wave-wide load
+//     fetches RPL = 64 / LPR rows, in straight-line batches of loads;
+//   * each lane accumulates its slice in fp32 registers; at a bag's end the
+//     RPL row groups are combined by a fixed-order reduce-scatter across lanes
+//     and the owning lanes store the pooled vector;
+//   * a handle whose tables share one (storage type, LPR) kind launches a body
+//     specialised for it; otherwise one launch per storage type switches on
+//     each table's LPR.
 // Rows wider than 1 KiB take several 1 KiB column passes.
 
 #include "eb_device.h"
