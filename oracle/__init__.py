@@ -6,7 +6,7 @@ never does.  The arithmetic lives in eb_oracle.c (plain C, fp64
 accumulation); this module only marshals numpy arrays into it.
 """
 from .oracle import (OracleError, OracleTable, build, double_to_half, ebo_backward_update, ebo_fm, ebo_forward,
-                     half_to_double, lib_path, max_threads)
+                     ebo_forward_seq, half_to_double, lib_path, max_threads)
 
 __all__ = ["OracleError", "OracleTable", "build", "double_to_half", "ebo_backward_update", "ebo_fm", "ebo_forward",
-           "half_to_double", "lib_path", "max_threads"]
+           "ebo_forward_seq", "half_to_double", "lib_path", "max_threads"]

@@ -511,3 +511,81 @@ int ebo_fm(const float *pooled, int64_t ld, int32_t num_fields, int32_t dim, int
   }
   return EBO_OK;
 }
+
+/* ========================================================================
+ * Un-pooled (sequence) lookup (test infrastructure).
+ *
+ * Sequence recommenders (the Introduction names HSTU among the architectures
+ * the paper's profiling targets) consume the embedding of every position of a
+ * jagged feature instead of a pooled sum.  For every table t and position i
+ * in [start_t, end_t) = [offsets[t*B], offsets[(t+1)*B]):
+ *
+ *   out[base_t + (i - start_t) * D_t + d] = x(t, idx[i], d)
+ *
+ * with base_t = sum_{s<t} N_s * D_s, N_s = end_s - start_s: table t's
+ * positions form a [N_t, D_t] row-major block, the blocks in table order
+ * ([N, D] when every table has the same D).  x is the fp32 element value of
+ * the pooled lookup (the stored value, the exact widening of a binary16, or
+ * fp32(s*q + c) for int8 row-wise rows).
+ * out_numel must equal sum_t N_t * D_t (else EBO_ERR_SHAPE).
+ * ======================================================================== */
+int ebo_forward_seq(const ebo_table *tables, int32_t num_tables, const void *indices,
+                    const void *offsets, int32_t index_type, int64_t num_indices,
+                    int64_t num_offsets, float *out, int64_t out_numel, int32_t num_threads) {
+  if (!tables || num_tables < 1 || !offsets || (!out && out_numel > 0)) return EBO_ERR_INVALID_ARG;
+  if (num_indices < 0 || (num_indices > 0 && !indices)) return EBO_ERR_INVALID_ARG;
+  if (index_type != EBO_IDX_I32 && index_type != EBO_IDX_I64) return EBO_ERR_DTYPE;
+  if (num_offsets < 2 || (num_offsets - 1) % num_tables != 0) return EBO_ERR_SHAPE;
+  const int64_t B = (num_offsets - 1) / num_tables;
+  const int64_t nbags = num_offsets - 1;
+  for (int32_t t = 0; t < num_tables; ++t) {
+    const ebo_table *tb = &tables[t];
+    if (tb->dtype != EBO_ROW_F32 && tb->dtype != EBO_ROW_F16 && tb->dtype != EBO_ROW_U8)
+      return EBO_ERR_DTYPE;
+    if (tb->dim < 1 || tb->num_rows < 1 || !tb->data) return EBO_ERR_INVALID_ARG;
+  }
+  if (ebo_read_index(offsets, index_type, 0) != 0) return EBO_ERR_OFFSETS;
+  for (int64_t g = 0; g < nbags; ++g)
+    if (ebo_read_index(offsets, index_type, g + 1) < ebo_read_index(offsets, index_type, g))
+      return EBO_ERR_OFFSETS;
+  if (ebo_read_index(offsets, index_type, nbags) != num_indices) return EBO_ERR_OFFSETS;
+
+  int64_t *base = (int64_t *)malloc(sizeof(int64_t) * (size_t)(num_tables + 1));
+  if (!base) return EBO_ERR_INVALID_ARG;
+  base[0] = 0;
+  for (int32_t t = 0; t < num_tables; ++t) {
+    int64_t lo = ebo_read_index(offsets, index_type, (int64_t)t * B);
+    int64_t hi = ebo_read_index(offsets, index_type, (int64_t)(t + 1) * B);
+    for (int64_t i = lo; i < hi; ++i) {
+      int64_t r = ebo_read_index(indices, index_type, i);
+      if (r < 0 || r >= tables[t].num_rows) {
+        free(base);
+        return EBO_ERR_INDEX_OOB;
+      }
+    }
+    base[t + 1] = base[t] + (hi - lo) * tables[t].dim;
+  }
+  if (base[num_tables] != out_numel) {
+    free(base);
+    return EBO_ERR_SHAPE;
+  }
+
+  int nthreads = 1;
+#ifdef _OPENMP
+  nthreads = num_threads > 0 ? num_threads : omp_get_max_threads();
+#endif
+  (void)nthreads;
+  for (int32_t t = 0; t < num_tables; ++t) {
+    const ebo_table *tb = &tables[t];
+    const int64_t lo = ebo_read_index(offsets, index_type, (int64_t)t * B);
+    const int64_t hi = ebo_read_index(offsets, index_type, (int64_t)(t + 1) * B);
+#pragma omp parallel for schedule(static) num_threads(nthreads)
+    for (int64_t i = lo; i < hi; ++i) {
+      const int64_t r = ebo_read_index(indices, index_type, i);
+      float *dst = out + base[t] + (i - lo) * tb->dim;
+      for (int32_t d = 0; d < tb->dim; ++d) dst[d] = ebo_element(tb, r, d);
+    }
+  }
+  free(base);
+  return EBO_OK;
+}

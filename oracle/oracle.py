@@ -84,6 +84,11 @@ def _load():
             ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
             ctypes.c_float, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
         ]
+        lib.ebo_forward_seq.restype = ctypes.c_int
+        lib.ebo_forward_seq.argtypes = [
+            ctypes.POINTER(_CTable), ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+            ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+        ]
         lib.ebo_fm.restype = ctypes.c_int
         lib.ebo_fm.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]
@@ -294,3 +299,35 @@ def ebo_fm(pooled: np.ndarray, num_fields: int, dim: int, asum: Optional[np.ndar
     if rc != 0:
         raise OracleError(rc)
     return y if scale is None else (y, scale)
+
+
+def ebo_forward_seq(tables: Sequence[OracleTable], indices: np.ndarray, offsets: np.ndarray,
+                    out_numel: Optional[int] = None, num_threads: int = 0) -> np.ndarray:
+    """Un-pooled lookup: every position's row as fp32, table t's positions as a
+    [N_t, D_t] block, blocks in table order (see eb_oracle.c).  Returns the flat
+    fp32 array; out_numel defaults to sum_t N_t * D_t."""
+    lib = _load()
+    offsets = np.ascontiguousarray(offsets)
+    indices = np.ascontiguousarray(indices)
+    if offsets.dtype not in (np.int32, np.int64) or indices.dtype != offsets.dtype:
+        raise TypeError("indices and offsets must share an int32 or int64 dtype")
+    T = len(tables)
+    ct = (_CTable * T)()
+    for i, tb in enumerate(tables):
+        if not tb.rows.flags["C_CONTIGUOUS"]:
+            raise ValueError("table rows must be C-contiguous")
+        ct[i].data = tb.rows.ctypes.data
+        ct[i].num_rows = tb.rows.shape[0]
+        ct[i].row_stride_bytes = tb.rows.strides[0]
+        ct[i].dim = int(tb.dim)
+        ct[i].dtype = _ROW_CODES[tb.dtype]
+    if out_numel is None:
+        B = (offsets.size - 1) // T
+        out_numel = sum(int(offsets[(t + 1) * B] - offsets[t * B]) * int(tables[t].dim) for t in range(T))
+    out = np.empty(max(int(out_numel), 0), np.float32)
+    rc = lib.ebo_forward_seq(ct, T, indices.ctypes.data if indices.size else None, offsets.ctypes.data,
+                             1 if offsets.dtype == np.int64 else 0, indices.size, offsets.size,
+                             out.ctypes.data if out.size else None, int(out_numel), int(num_threads))
+    if rc != 0:
+        raise OracleError(rc)
+    return out
