@@ -33,28 +33,8 @@ METRIC = "EmbeddingBag fwd achieved HBM GB/s (% of peak) + pooled lookups/sec, 1
 METRIC_BACKWARD = ("EmbeddingBag bwd + fused row-wise Adagrad update achieved HBM GB/s (% of peak) + "
                    "lookups/sec, 1 GPU")
 METRIC_FM = ("EmbeddingBag fwd + fused FM cross term achieved HBM GB/s (% of peak) + pooled lookups/sec, 1 GPU")
+METRIC_SEQ = "Un-pooled (sequence) embedding lookup achieved HBM GB/s (% of peak) + lookups/sec, 1 GPU"
 SAMPLE = 7
-
-
-def backward_algorithmic_bytes(w) -> int:
-    """Bytes one backward + row-wise Adagrad step must move at minimum: the
-    gathered gradient rows (4*D per lookup), each touched table row read and
-    written once, its optimizer state read and written once, and the indices,
-    offsets and weights."""
-    import torch
-
-    esz = w.indices.element_size()
-    B = w.batch
-    total = w.num_indices * esz + int(w.offsets.numel()) * esz
-    if w.weights is not None:
-        total += w.num_indices * 4
-    off = w.offsets.cpu()
-    for t, tb in enumerate(w.tables):
-        lo, hi = int(off[t * B]), int(off[(t + 1) * B])
-        n = hi - lo
-        u = int(torch.unique(w.indices[lo:hi]).numel()) if n else 0
-        total += n * 4 * tb.dim + u * (2 * tb.row_bytes + 8)
-    return total
 
 
 def cpu_cores() -> int:
@@ -62,6 +42,39 @@ def cpu_cores() -> int:
         return len(os.sched_getaffinity(0))
     except AttributeError:
         return os.cpu_count() or 1
+
+
+def run_cpu_baseline_seq(w, budget_s: float, host_bytes_cap: float = 3e9):
+    """Time the oracle's un-pooled lookup (as it stands) on the positions of
+    the first tables of `w` whose rows fit in `host_bytes_cap` bytes, repeated
+    until `budget_s` seconds have passed.  Returns (reps, seconds, threads,
+    lookups per rep, algorithmic bytes per rep, tables used)."""
+    import oracle
+
+    threads = min(cpu_cores(), int(os.environ.get("OMP_NUM_THREADS", cpu_cores())))
+    use, acc = 0, 0
+    for t in w.tables:
+        nbytes = t.rows.numel() * t.rows.element_size()
+        if use and acc + nbytes > host_bytes_cap:
+            break
+        acc += nbytes
+        use += 1
+    B = w.batch
+    off = w.offsets[:use * B + 1].cpu().numpy()
+    idx = w.indices[:int(off[-1])].cpu().numpy()
+    tabs = [oracle.OracleTable(t.rows.cpu().numpy(), t.dim, t.dtype) for t in w.tables[:use]]
+    esz = w.indices.element_size()
+    look = int(off[-1])
+    nbytes = (use + 1) * esz + sum(int(off[(t + 1) * B] - off[t * B]) * (w.tables[t].row_bytes + esz + 4 * w.tables[t].dim)
+                                   for t in range(use))
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.ebo_forward_seq(tabs, idx, off, num_threads=threads)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return reps, el, threads, look, nbytes, use
 
 
 def run_cpu_baseline(w, budget_s: float, host_bytes_cap: float = 3e9, fm: bool = False):
@@ -124,9 +137,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing (0 = skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (to scale rocprofv3 byte counters)")
-    ap.add_argument("--mode", default="forward", choices=["forward", "fm", "backward"],
-                    help="fm: eb_forward_fm (FM cross term fused into the store); "
-                         "backward: eb_backward_update with row-wise Adagrad")
+    ap.add_argument("--mode", default="forward", choices=["forward", "fm", "seq", "backward"],
+                    help="fm: eb_forward_fm (the lookup, then the FM cross term); seq: eb_forward_seq "
+                         "(un-pooled lookup); backward: eb_backward_update with row-wise Adagrad")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -150,13 +163,19 @@ def main():
     for s in (1, 2):
         batches.append(make_workload(args.config, dev, batch_seed=s, index_law=law, tables=batches[0].tables))
     w0 = batches[0]
-    out = torch.empty((w0.batch, w0.sum_dim), dtype=torch.float32, device=dev)
+    if args.mode == "seq":
+        # every position's row; sized for the largest of the three batches
+        out = torch.empty(max(b.seq_output_numel() for b in batches), dtype=torch.float32, device=dev)
+    else:
+        out = torch.empty((w0.batch, w0.sum_dim), dtype=torch.float32, device=dev)
     if args.mode == "forward":
         algo = [b.algorithmic_bytes() for b in batches]
     elif args.mode == "fm":
         algo = [b.algorithmic_bytes() + 4 * b.batch for b in batches]
+    elif args.mode == "seq":
+        algo = [b.seq_algorithmic_bytes() for b in batches]
     else:
-        algo = [backward_algorithmic_bytes(b) for b in batches]
+        algo = [b.backward_algorithmic_bytes() for b in batches]
     nlook = [b.num_indices for b in batches]
     torch.cuda.synchronize()
 
@@ -175,6 +194,14 @@ def main():
 
     if args.mode == "forward":
         step = forward_step
+    elif args.mode == "seq":
+        seq_outs = [eb._as_tensor(out[:b.seq_output_numel()]) for b in batches]
+
+        def step(k):
+            i, f, _, _ = calls[k % 3]
+            st = lib.eb_forward_seq(h.ptr, i, f, seq_outs[k % 3])
+            if st != eb.EB_OK:
+                raise eb.EBError(st, "eb_forward_seq")
     elif args.mode == "fm":
         fm_out = torch.empty(w0.batch, dtype=torch.float32, device=dev)
         fm_t = eb._as_tensor(fm_out)
@@ -232,7 +259,7 @@ def main():
     look_total = sum(nlook[k % 3] for k in range(args.steps))
     value = bytes_total / wall / 1e9
     achieved = kern_bytes / kern_avg_s / 1e9
-    traffic = counter_traffic(args.config, args.index_law, args.mode) if args.mode == "forward" else None
+    traffic = counter_traffic(args.config, args.index_law, args.mode) if args.mode in ("forward", "seq") else None
 
     fm_pass = None
     if args.mode == "fm":
@@ -269,10 +296,13 @@ def main():
     eb.eb_destroy(h)
 
     cpu = None
-    if args.cpu_budget > 0 and args.mode in ("forward", "fm"):
+    if args.cpu_budget > 0 and args.mode in ("forward", "fm", "seq"):
         print(f"[bench] CPU oracle baseline ({args.cpu_budget:.0f} s budget)", file=sys.stderr, flush=True)
         fm = args.mode == "fm"
-        reps, el, threads, look, nbytes, use = run_cpu_baseline(w0, args.cpu_budget, fm=fm)
+        if args.mode == "seq":
+            reps, el, threads, look, nbytes, use = run_cpu_baseline_seq(w0, args.cpu_budget)
+        else:
+            reps, el, threads, look, nbytes, use = run_cpu_baseline(w0, args.cpu_budget, fm=fm)
         what = "the whole batch" if use == w0.num_tables else f"the bags of tables 0..{use - 1} of {w0.num_tables}"
         if fm:
             what += " plus the FM cross term over those fields"
@@ -288,7 +318,7 @@ def main():
 
     dtypes = sorted({t.dtype for t in w0.tables})
     line = {
-        "metric": {"forward": METRIC, "fm": METRIC_FM, "backward": METRIC_BACKWARD}[args.mode],
+        "metric": {"forward": METRIC, "fm": METRIC_FM, "seq": METRIC_SEQ, "backward": METRIC_BACKWARD}[args.mode],
         "value": round(value, 2),
         "unit": "GB/s",
         "pct_of_peak_hbm": round(100.0 * value / PEAK_HBM_GBS, 2),
@@ -317,7 +347,7 @@ def main():
         "roofline": {
             "bound": "hbm",
             "kernel": {"forward": KERNELS["forward"][0], "fm": "eb_forward_fm (eb_pool_kernel, then eb_fm_kernel)",
-                       "backward": "eb_backward_update (all its kernels)"}[args.mode],
+                       "seq": KERNELS["seq"][0], "backward": "eb_backward_update (all its kernels)"}[args.mode],
             "achieved": round(achieved, 2),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",

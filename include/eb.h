@@ -51,8 +51,9 @@
  * Checked mode is for debugging; it blocks the calling thread.
  *
  * Tuning.  EB_BAGS_PER_WAVE=k (1..32), read when a handle is created, fixes
- * how many consecutive bags of one table a wavefront pools; without it the
- * count is chosen per call from the number of bags.  EB_XCD_REMAP=0|1, read
+ * how many consecutive bags of one table a wavefront pools (and how many
+ * 64-position chunks a wavefront of eb_forward_seq copies); without it the
+ * count is chosen per call from the number of bags (positions).  EB_XCD_REMAP=0|1, read
  * at the same time, forces how workgroups map onto the GPU's XCDs (default:
  * XCD-contiguous for handles of up to 32 tables, round-robin otherwise).
  * EB_BWD_TILE_CHUNKS=c (1..16) fixes the backward's tiles at 64*c sorted
@@ -168,6 +169,32 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables,
 eb_status eb_forward(const eb_tables *tables, eb_tensor indices,
                      eb_tensor offsets, eb_tensor per_sample_weights,
                      eb_pooling pooling, eb_tensor out);
+
+/*
+ * Un-pooled (sequence) lookup: the embedding of every position, for
+ * sequence recommenders (the Introduction names HSTU among the architectures
+ * the paper's profiling targets), which consume each position of a jagged
+ * feature instead of a pooled sum.  For table t and each position i in
+ * [start_t, end_t) = [offsets[t*B], offsets[(t+1)*B]):
+ *   out[base_t + (i - start_t) * D_t + d] = x(t, indices[i], d),
+ *   base_t = sum_{s<t} (end_s - start_s) * D_s,
+ * i.e. table t's positions form a [N_t, D_t] row-major block and the blocks
+ * follow in table order ([N, D] when every table has the same D).  x is the
+ * element's fp32 value as for eb_forward, so the output is exact (one
+ * rounding for int8 row-wise rows).
+ *   indices, offsets: as for eb_forward; only the table starts offsets[t*B]
+ *            (and offsets[T*B] = N) are read.
+ *   out:     EB_T_F32 [sum_t N_t * D_t], 16-byte aligned.  With one D for
+ *            every table numel must be N * D (else EB_ERR_SHAPE); otherwise
+ *            it must lie in [N * min D, N * max D] (else EB_ERR_SHAPE), and a
+ *            numel that does not match the offsets leaves the rows that do
+ *            not fit unwritten (reported as EB_ERR_SHAPE in checked mode).
+ * Positions whose index is outside its table get zeros (EB_ERR_INDEX_OOB in
+ * checked mode).  Asynchronous on the handle's stream; allocates nothing;
+ * N = 0 enqueues nothing.
+ */
+eb_status eb_forward_seq(const eb_tables *tables, eb_tensor indices,
+                         eb_tensor offsets, eb_tensor out);
 
 /*
  * The factorization-machine cross term of each example over its pooled

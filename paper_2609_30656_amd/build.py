@@ -11,7 +11,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
-SOURCES = [os.path.join(CSRC, f) for f in ("eb_forward.hip", "eb_fm.hip", "eb_backward.hip") if os.path.exists(os.path.join(CSRC, f))]
+SOURCES = [os.path.join(CSRC, f) for f in ("eb_forward.hip", "eb_fm.hip", "eb_seq.hip", "eb_backward.hip") if os.path.exists(os.path.join(CSRC, f))]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libeb.so")
 

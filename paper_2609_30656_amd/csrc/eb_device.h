@@ -43,6 +43,7 @@ constexpr int32_t kRemapMaxTables = 32;
 // error bits raised by the kernel, reported in checked mode
 constexpr int kErrIndex = 1;
 constexpr int kErrOffsets = 2;
+constexpr int kErrOutSize = 4;  // an output row would fall outside the output
 
 enum : int32_t { kF32 = 0, kF16 = 1, kU8 = 2 };
 

@@ -304,6 +304,7 @@ eb_status end_checked(const eb_tables *h, hipError_t e) {
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
     if (e == hipSuccess && (herr & kErrOffsets)) st = EB_ERR_OFFSETS;
     else if (e == hipSuccess && (herr & kErrIndex)) st = EB_ERR_INDEX_OOB;
+    else if (e == hipSuccess && (herr & kErrOutSize)) st = EB_ERR_SHAPE;
   }
   return e != hipSuccess ? EB_ERR_HIP : st;
 }

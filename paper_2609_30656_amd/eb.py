@@ -39,8 +39,8 @@ EB_OPT_SGD, EB_OPT_ROWWISE_ADAGRAD = 0, 1
 TABLE_DTYPES = {"f32": EB_F32, "f16": EB_F16, "int8_rowwise": EB_INT8_ROWWISE}
 POOLING = {"sum": EB_POOL_SUM, "mean": EB_POOL_MEAN}
 OPTIMIZERS = {"sgd": EB_OPT_SGD, "rowwise_adagrad": EB_OPT_ROWWISE_ADAGRAD}
-EXPORTED = ("eb_create_tables", "eb_forward", "eb_fm_cross", "eb_forward_fm", "eb_destroy", "eb_status_string",
-            "eb_backward_workspace_size", "eb_backward_update")
+EXPORTED = ("eb_create_tables", "eb_forward", "eb_forward_seq", "eb_fm_cross", "eb_forward_fm", "eb_destroy",
+            "eb_status_string", "eb_backward_workspace_size", "eb_backward_update")
 
 
 class EBError(RuntimeError):
@@ -82,6 +82,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.eb_forward_fm.restype = ctypes.c_int
         lib.eb_forward_fm.argtypes = [ctypes.c_void_p, eb_tensor, eb_tensor, eb_tensor, ctypes.c_int, eb_tensor,
                                       eb_tensor]
+        lib.eb_forward_seq.restype = ctypes.c_int
+        lib.eb_forward_seq.argtypes = [ctypes.c_void_p, eb_tensor, eb_tensor, eb_tensor]
         lib.eb_fm_cross.restype = ctypes.c_int
         lib.eb_fm_cross.argtypes = [ctypes.c_void_p, eb_tensor, eb_tensor]
         lib.eb_destroy.restype = ctypes.c_int
@@ -173,6 +175,15 @@ def eb_forward(tables: EbTables, indices: torch.Tensor, offsets: torch.Tensor,
                         mode, _as_tensor(out))
     if st != EB_OK:
         raise EBError(st, "eb_forward")
+    return out
+
+
+def eb_forward_seq(tables: EbTables, indices: torch.Tensor, offsets: torch.Tensor, out: torch.Tensor) -> torch.Tensor:
+    """Un-pooled lookup: every position's row as fp32 into out (table t's
+    positions as a [N_t, D_t] block, blocks in table order); returns out."""
+    st = load_library().eb_forward_seq(tables.ptr, _as_tensor(indices), _as_tensor(offsets), _as_tensor(out))
+    if st != EB_OK:
+        raise EBError(st, "eb_forward_seq")
     return out
 
 

@@ -35,6 +35,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 KERNELS = {
     "forward": ("eb_pool_kernel", ("eb_device.h", "eb_forward.hip")),
     "fm": ("eb_fm_kernel", ("eb_device.h", "eb_fm.hip")),
+    "seq": ("eb_seq_kernel", ("eb_device.h", "eb_seq.hip")),
     "backward": ("eb_bwd_tiles_kernel", ("eb_device.h", "eb_backward.hip")),
 }
 

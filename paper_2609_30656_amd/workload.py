@@ -100,6 +100,41 @@ class Workload:
         out = self.batch * self.sum_dim * 4
         return row + idx + off + w + out
 
+    def table_lookups(self) -> List[int]:
+        """Number of index positions of each table."""
+        return [int(n) for n in self.lengths.view(self.num_tables, self.batch).sum(dim=1).cpu().tolist()]
+
+    def seq_output_numel(self) -> int:
+        """fp32 elements of the un-pooled lookup's output (a D_t row per position)."""
+        return sum(n * t.dim for n, t in zip(self.table_lookups(), self.tables))
+
+    def seq_algorithmic_bytes(self) -> int:
+        """Bytes one un-pooled lookup must move at minimum: each position's row
+        read, its index read and its fp32 row written, plus the T + 1 table
+        starts of the offsets."""
+        esz = self.indices.element_size()
+        total = (self.num_tables + 1) * esz
+        for n, t in zip(self.table_lookups(), self.tables):
+            total += n * (t.row_bytes + esz + 4 * t.dim)
+        return total
+
+    def backward_algorithmic_bytes(self) -> int:
+        """Bytes one backward + row-wise Adagrad step must move at minimum: the
+        gathered gradient rows (4*D per lookup), each touched table row read and
+        written once, its optimizer state read and written once, and the
+        indices, offsets and weights."""
+        esz = self.indices.element_size()
+        total = self.num_indices * esz + int(self.offsets.numel()) * esz
+        if self.weights is not None:
+            total += self.num_indices * 4
+        off = self.offsets.cpu()
+        B = self.batch
+        for t, tb in enumerate(self.tables):
+            lo, hi = int(off[t * B]), int(off[(t + 1) * B])
+            u = int(torch.unique(self.indices[lo:hi]).numel()) if hi > lo else 0
+            total += (hi - lo) * 4 * tb.dim + u * (2 * tb.row_bytes + 8)
+        return total
+
 
 def _seed(*parts: int) -> int:
     """63-bit torch seed derived from a tuple of small integers."""

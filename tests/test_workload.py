@@ -79,3 +79,22 @@ def test_algorithmic_bytes_counts_every_term():
     N = w.num_indices
     expect = N * 256 + N * 8 + (2 * 16 + 1) * 8 + N * 4 + 16 * 256 * 4
     assert w.algorithmic_bytes() == expect
+
+
+def test_sequence_and_backward_byte_counts():
+    from oracle import ebo_forward_seq
+    from conftest import oracle_tables
+
+    w = make_workload("c4", "cpu", rows_cap=300, batch=6, num_tables=5)
+    seq = ebo_forward_seq(oracle_tables(w), w.indices.numpy(), w.offsets.numpy())
+    assert w.seq_output_numel() == seq.size
+    off, B, esz = w.offsets.numpy(), w.batch, w.indices.element_size()
+    n = [int(off[(t + 1) * B] - off[t * B]) for t in range(w.num_tables)]
+    assert w.table_lookups() == n
+    expect = (w.num_tables + 1) * esz + sum(n[t] * (tb.row_bytes + esz + 4 * tb.dim) for t, tb in enumerate(w.tables))
+    assert w.seq_algorithmic_bytes() == expect
+    idx = w.indices.numpy()
+    uniq = [np.unique(idx[off[t * B]:off[(t + 1) * B]]).size for t in range(w.num_tables)]
+    expect = w.num_indices * esz + off.size * esz + sum(
+        n[t] * 4 * tb.dim + uniq[t] * (2 * tb.row_bytes + 8) for t, tb in enumerate(w.tables))
+    assert w.backward_algorithmic_bytes() == expect
