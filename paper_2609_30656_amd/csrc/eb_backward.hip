@@ -53,7 +53,7 @@ struct BwdArgs {
   uint32_t *keys;         // [N] sort keys by position
   int32_t *bag_of;        // [N] bag id by position
   const uint32_t *skeys;  // [N] sorted keys
-  const uint32_t *spos;   // [N] positions in sorted order
+  const uint32_t *spos;   // [N] in sorted order: positions, or bag ids when sorted_bags
   int32_t *tile_start;    // [T + 1] first tile of each table; [T] = number of tiles
   uint8_t *tile_flags;    // [tiles] kTileContinues | kTileOwnsRun
   float *carry;           // [2 * tiles * max_dim]: slot 2w = head run partial, 2w+1 = tail run partial
@@ -64,6 +64,7 @@ struct BwdArgs {
   int32_t num_tables;
   int32_t idx64;
   int32_t coef;           // 0: c = 1, 1: c = w_i, 2: c = 1 / L
+  int32_t sorted_bags;    // spos holds bag ids (no per-sample weights to look up)
   int32_t opt;
   float lr;
   float eps;
@@ -438,8 +439,11 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
     ch.n = n;
     if (lane < n) {
       key = a.skeys[c + lane];
-      const uint32_t pos = a.spos[c + lane];
-      const int32_t g = a.bag_of[pos];
+      // unweighted pooling sorts bag ids with the keys; weighted pooling sorts
+      // positions (the weight is per position) and looks the bag up
+      const uint32_t sv = a.spos[c + lane];
+      const uint32_t pos = sv;
+      const int32_t g = a.sorted_bags ? (int32_t)sv : a.bag_of[pos];
       const int64_t b = (int64_t)g - (int64_t)t * a.batch;
       if (key >= kmin && key < sentinel && b >= 0 && b < a.batch) {
         ch.row = (uint32_t)b;
@@ -648,11 +652,18 @@ eb_status layout(const eb_tables *h, int64_t n, BwdLayout *L) {
   L->tiles_ub = (n + L->tile_size - 1) / L->tile_size + h->num_tables;
   size_t sort_bytes = 0;
   if (n > 0) {
-    hipError_t e = rocprim::radix_sort_pairs(nullptr, sort_bytes, static_cast<const uint32_t *>(nullptr),
+    // scratch for either kind of value sorted with the keys (positions, or bag ids)
+    size_t by_pos = 0, by_bag = 0;
+    hipError_t e = rocprim::radix_sort_pairs(nullptr, by_pos, static_cast<const uint32_t *>(nullptr),
                                              static_cast<uint32_t *>(nullptr), rocprim::counting_iterator<uint32_t>(0),
                                              static_cast<uint32_t *>(nullptr), (unsigned int)n, 0, key_bits(h),
                                              h->stream);
+    if (e == hipSuccess)
+      e = rocprim::radix_sort_pairs(nullptr, by_bag, static_cast<const uint32_t *>(nullptr),
+                                    static_cast<uint32_t *>(nullptr), static_cast<const uint32_t *>(nullptr),
+                                    static_cast<uint32_t *>(nullptr), (unsigned int)n, 0, key_bits(h), h->stream);
     if (e != hipSuccess) return EB_ERR_HIP;
+    sort_bytes = by_pos > by_bag ? by_pos : by_bag;
   }
   L->sort_bytes = sort_bytes;
   size_t off = 0;
@@ -764,6 +775,7 @@ eb_status eb_backward_update(const eb_tables *h, eb_tensor indices, eb_tensor of
   a.num_tables = h->num_tables;
   a.idx64 = indices.elem_type == EB_I64;
   a.coef = pooling == EB_POOL_MEAN ? 2 : (weighted ? 1 : 0);
+  a.sorted_bags = weighted ? 0 : 1;
   a.opt = optimizer;
   a.lr = learning_rate;
   a.eps = eps;
@@ -788,13 +800,19 @@ eb_status eb_backward_update(const eb_tables *h, eb_tensor indices, eb_tensor of
     hipLaunchKernelGGL(eb_bwd_keys_kernel, dim3(grid), dim3(kBlock), 0, h->stream, a);
     e = hipGetLastError();
   }
-  // 2. sort (key, position) pairs on the bits the largest key needs
+  // 2. sort (key, bag id) pairs, or (key, position) pairs when the weights
+  //    (per position) are needed, on the bits the largest key needs
   if (e == hipSuccess) {
     const unsigned end_bit = key_bits(h);
     size_t tmp = L.sort_bytes;
-    e = rocprim::radix_sort_pairs(ws + L.sort_tmp, tmp, a.keys, const_cast<uint32_t *>(a.skeys),
-                                  rocprim::counting_iterator<uint32_t>(0), const_cast<uint32_t *>(a.spos),
-                                  (unsigned int)n, 0, end_bit, h->stream);
+    if (a.sorted_bags)
+      e = rocprim::radix_sort_pairs(ws + L.sort_tmp, tmp, a.keys, const_cast<uint32_t *>(a.skeys),
+                                    reinterpret_cast<const uint32_t *>(a.bag_of), const_cast<uint32_t *>(a.spos),
+                                    (unsigned int)n, 0, end_bit, h->stream);
+    else
+      e = rocprim::radix_sort_pairs(ws + L.sort_tmp, tmp, a.keys, const_cast<uint32_t *>(a.skeys),
+                                    rocprim::counting_iterator<uint32_t>(0), const_cast<uint32_t *>(a.spos),
+                                    (unsigned int)n, 0, end_bit, h->stream);
   }
   // 3. tiles: first tile per table, then pool and update
   if (e == hipSuccess) {
