@@ -2,18 +2,22 @@
 """Benchmark: pooled EmbeddingBag forward on one MI355X.
 
 One step = one eb_forward over one batch of the workload (all tables, all
-bags); with --mode fm, one eb_forward_fm (the same lookup with the FM cross
-term fused into the store); with --mode backward, one eb_backward_update with
-row-wise Adagrad.  Three independently seeded index batches over the same tables are
-rotated so consecutive steps do not replay identical lookups.  Tables,
-indices and offsets are resident in HBM before the timed region starts.
+bags).  Other modes: --mode fm, one eb_forward_fm (the lookup, then the FM
+cross term over its output); --mode seq, one eb_forward_seq (the un-pooled
+lookup); --mode backward, one eb_backward_update with row-wise Adagrad.  Three
+independently seeded index batches over the same tables are rotated so
+consecutive steps do not replay identical lookups.  Tables, indices and
+offsets are resident in HBM before the timed region starts.
 
 Prints one JSON line:
   value            algorithmic GB/s over the K timed steps (wall clock)
   lookups_per_s    pooled lookups per second over the same steps
   roofline         eb_pool_kernel's algorithmic bytes per launch / its mean
                    launch time from HIP events on the library's stream,
-                   against 8 TB/s HBM3E; traffic from rocprofv3 counters
+                   against 8 TB/s HBM3E; traffic from rocprofv3 counters;
+                   p10/median/p90 of the launch times; and `cold`: the same
+                   calls each preceded (outside the events) by a 1 GiB write
+                   that evicts L2 and the Infinity Cache
   cpu_baseline     the CPU oracle on a bounded sample of the same workload
 
 Algorithmic bytes per step = gathered row bytes (every lookup, duplicates
@@ -135,6 +139,9 @@ def main():
     ap.add_argument("--index-law", default="zipf", choices=["zipf", "uniform"],
                     help="uniform = no-reuse control at the same shapes")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing (0 = skip)")
+    ap.add_argument("--cold-reps", type=int, default=15,
+                    help="after the timed loop, time this many calls each preceded (outside the events) by a "
+                         "1 GiB write that evicts L2 and the Infinity Cache (0 = skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (to scale rocprofv3 byte counters)")
     ap.add_argument("--mode", default="forward", choices=["forward", "fm", "seq", "backward"],
@@ -255,6 +262,35 @@ def main():
     kern_avg_s = sum(kern_ms) / len(kern_ms) / 1e3
     kern_bytes = sum(algo[k % 3] for k in sample) / len(sample)
 
+    def quantiles(xs):
+        xs = sorted(xs)
+        pick = lambda f: xs[min(len(xs) - 1, int(f * (len(xs) - 1) + 0.5))]
+        return pick(0.1), pick(0.5), pick(0.9)
+
+    cold = None
+    if args.cold_reps > 0:
+        # every call starts with nothing of its inputs in L2 or the Infinity
+        # Cache: a 1 GiB write on the same stream, outside the events, first
+        print(f"[bench] {args.cold_reps} cold calls", file=sys.stderr, flush=True)
+        scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        cold_ms, cold_bytes = [], 0
+        for k in range(args.cold_reps):
+            with torch.cuda.stream(stream):
+                scratch.fill_(k & 0xFF)
+            a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a_ev.record(stream)
+            step(k)
+            b_ev.record(stream)
+            b_ev.synchronize()
+            cold_ms.append(a_ev.elapsed_time(b_ev))
+            cold_bytes += algo[k % 3]
+        del scratch
+        c10, c50, c90 = quantiles(cold_ms)
+        cold = {"reps": args.cold_reps, "kernel_ms_p10": round(c10, 5), "kernel_ms_median": round(c50, 5),
+                "kernel_ms_p90": round(c90, 5),
+                "achieved": round(cold_bytes / args.cold_reps / (c50 * 1e-3) / 1e9, 2)}
+    w10, w50, w90 = quantiles(kern_ms)
+
     bytes_total = sum(algo[k % 3] for k in range(args.steps))
     look_total = sum(nlook[k % 3] for k in range(args.steps))
     value = bytes_total / wall / 1e9
@@ -354,6 +390,10 @@ def main():
             "frac": round(achieved / PEAK_HBM_GBS, 4),
             "traffic": None if traffic is None else round(traffic),
             "kernel_ms_avg": round(kern_avg_s * 1e3, 5),
+            "kernel_ms_p10": round(w10, 5),
+            "kernel_ms_median": round(w50, 5),
+            "kernel_ms_p90": round(w90, 5),
+            "cold": cold,
             "timed_launches": len(sample),
         },
         "cpu_baseline": cpu,
