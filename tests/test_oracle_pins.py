@@ -396,3 +396,41 @@ def test_oracle_matches_frozen_record():
         out = ebo_forward(tabs, np.array(case["indices"], np.int64), np.array(case["offsets"], np.int64), w,
                           case["pooling"])
         assert np.array_equal(out.view(np.uint32), np.array(case["out_bits"], np.uint32))
+
+
+def test_oracle_seq_fm_and_backward_match_frozen_record():
+    import json
+    import os
+
+    from oracle import ebo_backward_update, ebo_fm, ebo_forward_seq
+
+    path = os.path.join(os.path.dirname(__file__), "golden", "oracle_regression.json")
+    with open(path) as f:
+        doc = json.load(f)
+    for case in doc["cases"]:
+        tabs = []
+        for k in ("f32", "f16", "int8_rowwise"):
+            raw = np.array(case["tables"][k], dtype=np.uint8)
+            arr = raw.view({"f32": np.float32, "f16": np.float16, "int8_rowwise": np.uint8}[k])
+            tabs.append(OracleTable(np.ascontiguousarray(arr), case["dim"], k))
+        idx, off = np.array(case["indices"], np.int64), np.array(case["offsets"], np.int64)
+        seq = ebo_forward_seq(tabs, idx, off)
+        assert np.array_equal(seq.view(np.uint32), np.array(case["seq_bits"], np.uint32))
+        pooled = np.array(case["out_bits"], np.uint32).view(np.float32).reshape(6, 24)
+        fm = ebo_fm(pooled, 3, case["dim"])
+        assert np.array_equal(fm.view(np.uint64), np.array(case["fm_bits"], np.uint64))
+    tables = doc["cases"][0]["tables"]
+    f32 = np.array(tables["f32"], np.uint8).view(np.float32)
+    f16 = np.array(tables["f16"], np.uint8).view(np.float16)
+    assert doc["backward"]
+    for case in doc["backward"]:
+        tabs = [OracleTable(np.ascontiguousarray(f32.copy()), 8, "f32"),
+                OracleTable(np.ascontiguousarray(f16.copy()), 8, "f16")]
+        state = np.array(case["state_in_bits"], np.uint32).view(np.float32).copy()
+        w = None if case["weights"] is None else np.array(case["weights"], np.uint32).view(np.float32)
+        grad = np.array(case["grad_bits"], np.uint32).view(np.float32).reshape(6, 16)
+        ebo_backward_update(tabs, np.array(case["indices"], np.int64), np.array(case["offsets"], np.int64), w,
+                            case["pooling"], grad, case["optimizer"], lr=case["lr"], eps=case["eps"], state=state)
+        assert np.array_equal(tabs[0].rows.view(np.uint32), np.array(case["f32_bits"], np.uint32))
+        assert np.array_equal(tabs[1].rows.view(np.uint16), np.array(case["f16_bits"], np.uint16))
+        assert np.array_equal(state.view(np.uint32), np.array(case["state_bits"], np.uint32))
