@@ -16,7 +16,7 @@ Prints one JSON line:
                    launch time from HIP events on the library's stream,
                    against 8 TB/s HBM3E; traffic from rocprofv3 counters;
                    p10/median/p90 of the launch times; and `cold`: the same
-                   calls each preceded (outside the events) by a 1 GiB write
+                   calls each preceded (outside the events) by a 1 GiB read
                    that evicts L2 and the Infinity Cache
   cpu_baseline     the CPU oracle on a bounded sample of the same workload
 
@@ -141,7 +141,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing (0 = skip)")
     ap.add_argument("--cold-reps", type=int, default=15,
                     help="after the timed loop, time this many calls each preceded (outside the events) by a "
-                         "1 GiB write that evicts L2 and the Infinity Cache (0 = skip)")
+                         "1 GiB read that evicts L2 and the Infinity Cache (0 = skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (to scale rocprofv3 byte counters)")
     ap.add_argument("--mode", default="forward", choices=["forward", "fm", "seq", "backward"],
@@ -270,13 +270,16 @@ def main():
     cold = None
     if args.cold_reps > 0:
         # every call starts with nothing of its inputs in L2 or the Infinity
-        # Cache: a 1 GiB write on the same stream, outside the events, first
+        # Cache: a 1 GiB read on the same stream, outside the events, first (a
+        # read, so no dirty lines are still being written back when it starts)
         print(f"[bench] {args.cold_reps} cold calls", file=sys.stderr, flush=True)
-        scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        scratch = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        sink = torch.empty((), dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
         cold_ms, cold_bytes = [], 0
         for k in range(args.cold_reps):
             with torch.cuda.stream(stream):
-                scratch.fill_(k & 0xFF)
+                torch.sum(scratch, dim=0, out=sink)
             a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a_ev.record(stream)
             step(k)
@@ -284,7 +287,7 @@ def main():
             b_ev.synchronize()
             cold_ms.append(a_ev.elapsed_time(b_ev))
             cold_bytes += algo[k % 3]
-        del scratch
+        del scratch, sink
         c10, c50, c90 = quantiles(cold_ms)
         cold = {"reps": args.cold_reps, "kernel_ms_p10": round(c10, 5), "kernel_ms_median": round(c50, 5),
                 "kernel_ms_p90": round(c90, 5),
