@@ -59,7 +59,13 @@
  * EB_BWD_TILE_CHUNKS=c (1..16) fixes the backward's tiles at 64*c sorted
  * positions (default: 64 to 256, from the number of lookups), and
  * EB_BWD_XCD_REMAP=0|1 its workgroup order (default as for the forward).
- * Results do not depend on any of these.
+ * EB_LONG_BAG=n (n > 0) makes the handle's lookups pool every bag of more
+ * than n lookups with all four wavefronts of a workgroup (each a contiguous
+ * quarter, partial sums added in a fixed order): for inputs with very long
+ * bags.  Without it each bag is pooled by one wavefront, which is faster when
+ * bags are short (the split path costs 7-10% on such inputs even unused).
+ * Results do not depend on any of these, except that splitting a bag changes
+ * the order of its sum (within the same error bound).
  */
 #ifndef EB_H_
 #define EB_H_

@@ -446,6 +446,7 @@ struct eb_tables {
   int32_t num_tables;
   int32_t checked;
   int32_t bags_per_wave;  // 0: chosen per call from the bag count
+  int64_t long_bag_len;   // > 0: the lookup splits bags with more lookups over a workgroup's wavefronts
   int32_t dtype_mask;     // bit d set: some table has storage type d
   int32_t single_log2;    // lanes-per-row log2 shared by every table of one type, else -1
   int32_t xcd_remap;      // see xcd_contiguous

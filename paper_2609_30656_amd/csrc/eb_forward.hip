@@ -46,6 +46,7 @@ struct FwdArgs {
   int32_t groups_per_table;  // ceil(batch / bags_per_wave)
   int32_t num_waves;         // num_tables * groups_per_table
   int32_t xcd_remap;         // renumber workgroups XCD-contiguously
+  int64_t long_len;          // bags with more lookups are split over the workgroup's wavefronts
 };
 
 // Pool bags [g0, g0 + nb) of one table (batch rows b0 ..) over the 1 KiB column
@@ -56,6 +57,7 @@ struct FwdArgs {
 template <int DT, int LPR, bool W>
 __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, int32_t g0, int nb, int32_t b0,
                                           int col_base) {
+  // (bags longer than a.long_len are pooled by pool_long_bags: skipped here)
   using R = Reduce<DT, LPR>;
   constexpr int V = Vals<DT>::n;
   const int lane = threadIdx.x & (kWave - 1);
@@ -70,7 +72,7 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
   }
   // bag j's index range, clamped into [0, N) so nothing is read outside the
   // index array whatever the offsets hold (a broken partition is reported)
-  auto bag_range = [&](int j, int64_t &lo, int64_t &hi) {
+  auto bag_range = [&](int j, int64_t &lo, int64_t &hi, bool &skip) {
     lo = readlane64(my_off, j);
     hi = readlane64(my_off, j + 1);
     const int32_t g = g0 + j;
@@ -81,6 +83,8 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
       lo = lo < 0 ? 0 : (lo > a.num_indices ? a.num_indices : lo);
       hi = hi < lo ? lo : (hi > a.num_indices ? a.num_indices : hi);
     }
+    skip = hi - lo > a.long_len;
+    if (skip) hi = lo;
   };
 
   constexpr bool SPLIT = EB_INT8_SPLIT_BIAS && DT == kU8 && !W;
@@ -91,17 +95,19 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
 
   int j = 0;
   int64_t blo, bhi;
-  bag_range(0, blo, bhi);
+  bool bskip;
+  bag_range(0, blo, bhi, bskip);
   int64_t c = blo;
   Chunk cur = load_chunk<W>(m.num_rows, a.indices, a.weights, a.idx64, c, bhi);
   while (true) {
     const bool last = c + kWave >= bhi;
     int jn = j;
     int64_t cn = c + kWave, nlo = blo, nhi = bhi;
+    bool nskip = bskip;
     if (last) {
       jn = j + 1;
       if (jn < nb) {
-        bag_range(jn, nlo, nhi);
+        bag_range(jn, nlo, nhi, nskip);
         cn = nlo;
       }
     }
@@ -118,7 +124,7 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
         cb = 0.0f;
       }
       R::run(acc);
-      if (R::stores(lane) && colok) {
+      if (R::stores(lane) && colok && !bskip) {
         const int64_t L = bhi - blo;
         const int f = R::first_value(lane);
         float outv[R::KEEP];
@@ -139,7 +145,86 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
     c = cn;
     blo = nlo;
     bhi = nhi;
+    bskip = nskip;
     cur = nxt;
+  }
+}
+
+// Pool positions [lo, hi) of one table over the column window at col_base
+// into acc, reduced across the wave (the values the lanes for which
+// Reduce::stores() holds keep).
+template <int DT, int LPR, bool W>
+__device__ __forceinline__ void pool_range(const TableMeta &m, const FwdArgs &a, int64_t lo, int64_t hi, int col_base,
+                                           float (&acc)[Vals<DT>::n]) {
+  constexpr int V = Vals<DT>::n;
+  constexpr bool SPLIT = EB_INT8_SPLIT_BIAS && DT == kU8 && !W;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int colb = col_base + (lane % LPR) * 16;
+  const bool colok = colb < m.code_bytes;
+  float cb = 0.0f;
+#pragma unroll
+  for (int i = 0; i < V; ++i) acc[i] = 0.0f;
+  if (lo < hi) {
+    int64_t c = lo;
+    Chunk cur = load_chunk<W>(m.num_rows, a.indices, a.weights, a.idx64, c, hi);
+    while (true) {
+      const int64_t cn = c + kWave;
+      const bool more = cn < hi;
+      Chunk nxt;
+      if (more) nxt = load_chunk<W>(m.num_rows, a.indices, a.weights, a.idx64, cn, hi);
+      gather_chunk<DT, LPR, W, SPLIT>(m, a.ctx, cur, acc, cb, colb, colok);
+      if (!more) break;
+      c = cn;
+      cur = nxt;
+    }
+  }
+  if constexpr (SPLIT) {
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] += cb;
+  }
+  Reduce<DT, LPR>::run(acc);
+}
+
+// One long bag (global id g, table m, batch row b, positions [lo, hi)), pooled
+// by all the workgroup's wavefronts: wave w takes the w-th contiguous quarter
+// of its positions; the partial vectors meet in LDS and wave 0 adds them in
+// wave order (so the result is deterministic) and stores the sum.  Every wave
+// of the workgroup calls this with the same arguments.
+template <int DT, int LPR, bool W>
+__device__ __forceinline__ void pool_long_bag(const TableMeta &m, const FwdArgs &a, int32_t b, int64_t lo, int64_t hi,
+                                              float (*part)[kPassBytes / Vals<DT>::esize]) {
+  using R = Reduce<DT, LPR>;
+  constexpr int V = Vals<DT>::n;
+  constexpr int WIN = kPassBytes / Vals<DT>::esize;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int64_t L = hi - lo;
+  const int64_t piece = (L + kWavesPerBlock - 1) / kWavesPerBlock;
+  const int64_t plo = lo + piece * wave < hi ? lo + piece * wave : hi;
+  const int64_t phi = plo + piece < hi ? plo + piece : hi;
+  const int e0 = (lane % LPR) * V + R::first_value(lane);
+  const int passes = LPR == kWave ? m.passes : 1;
+  for (int p = 0; p < passes; ++p) {
+    float acc[V];
+    pool_range<DT, LPR, W>(m, a, plo, phi, p * kPassBytes, acc);
+    if (R::stores(lane)) {
+#pragma unroll
+      for (int i = 0; i < R::KEEP; ++i) part[wave][e0 + i] = acc[i];
+    }
+    __syncthreads();
+    if (wave == 0) {
+      const int rest = (m.code_bytes - p * kPassBytes) / Vals<DT>::esize;
+      const int n = rest < WIN ? rest : WIN;
+      float *dst = a.out + (int64_t)b * a.out_ld + m.out_col + p * WIN;
+      for (int e = lane; e < n; e += kWave) {
+        float v = part[0][e];
+#pragma unroll
+        for (int w = 1; w < kWavesPerBlock; ++w) v += part[w][e];
+        if (a.mean && L > 0) v = v / (float)L;
+        __builtin_nontemporal_store(v, dst + e);
+      }
+    }
+    __syncthreads();  // the next pass or bag reuses the buffers
   }
 }
 
@@ -158,31 +243,129 @@ __device__ __forceinline__ void pool_all_passes(const TableMeta &m, const FwdArg
     pool_all_passes<DT, (1 << (LOG2)), W>(m, a, g0, nb, b0);                  \
     break;
 
-// One wavefront per run of bags.  DT is the storage type the launch serves
-// (wavefronts of other tables return at once).  LOG2 >= 0 fixes the lanes
-// per row for handles whose tables all share one kind; LOG2 < 0 switches on
-// each table's lanes per row.  Specialising keeps the register count (and so
-// the occupancy) at what that kind needs.
+// The workgroup's bags [G0, G1) and the offsets at both ends (clamped into
+// [0, N]).  Loaded when the kernel starts, with the wavefront's own offsets,
+// and used only after its own bags are done, so the check costs no extra
+// memory round trip.
+struct BlockBags {
+  int64_t G0, G1;
+  int64_t o;  // lane 0: the offset at G0, lane 1: at G1 (a vector load, so it
+              // returns with the wavefront's own offsets and delays no scalar load)
+};
+
+__device__ __forceinline__ int64_t clamped_offset(const FwdArgs &a, int64_t g) {
+  const int64_t v = a.idx64 ? static_cast<const int64_t *>(a.offsets)[g]
+                            : (int64_t) static_cast<const int32_t *>(a.offsets)[g];
+  return v < 0 ? 0 : (v > a.num_indices ? a.num_indices : v);
+}
+
+__device__ __forceinline__ BlockBags block_bags(const FwdArgs &a, uint32_t blk) {
+  const int32_t w0 = (int32_t)blk * kWavesPerBlock;
+  const int32_t w1 = (w0 + kWavesPerBlock < a.num_waves ? w0 + kWavesPerBlock : a.num_waves) - 1;
+  auto bag = [&](int32_t w, bool end) -> int64_t {
+    const int32_t t = w / a.groups_per_table;
+    const int32_t b0 = (w - t * a.groups_per_table) * a.bags_per_wave;
+    const int32_t nb = (a.batch - b0) < a.bags_per_wave ? (a.batch - b0) : a.bags_per_wave;
+    return (int64_t)t * a.batch + b0 + (end ? nb : 0);
+  };
+  BlockBags r;
+  r.G0 = bag(w0, false);
+  r.G1 = bag(w1, true);
+  const int lane = threadIdx.x & (kWave - 1);
+  r.o = lane < 2 ? clamped_offset(a, lane == 0 ? r.G0 : r.G1) : 0;
+  return r;
+}
+
+// Bags of the workgroup longer than a.long_len lookups are pooled, after the
+// wavefronts' own (shorter) bags, by all its wavefronts together
+// (pool_long_bag).  Every wavefront derives the same list from the offsets,
+// so all of them meet the same barriers; when the workgroup's bags hold no
+// more than a.long_len lookups in all (the usual case) no barrier is reached.
 template <int DT, int LOG2, bool W>
+__device__ __forceinline__ void pool_block_long_bags(const FwdArgs &a, const BlockBags &bb,
+                                                     float (*part)[kPassBytes / Vals<DT>::esize]) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t G0 = bb.G0, G1 = bb.G1;
+  auto off = [&](int64_t g) -> int64_t { return clamped_offset(a, g); };
+  if (readlane64(bb.o, 1) - readlane64(bb.o, 0) <= a.long_len) return;  // no bag can be long
+  for (int64_t gb = G0; gb < G1; gb += kWave) {
+    uint64_t mask;
+    {
+      const int64_t g = gb + lane;
+      int64_t lo = 0, hi = 0;
+      if (g < G1) {
+        lo = off(g);
+        hi = off(g + 1);
+        hi = hi < lo ? lo : hi;
+      }
+      mask = __ballot(g < G1 && hi - lo > a.long_len);
+    }
+    while (mask) {
+      const int j = __builtin_ctzll(mask);
+      mask &= mask - 1;
+      const int64_t gl = gb + j;
+      // re-read (uniform): nothing per lane stays live across the pooling
+      const int64_t blo = off(gl);
+      int64_t bhi = off(gl + 1);
+      bhi = bhi < blo ? blo : bhi;
+      const int32_t t = (int32_t)(gl / a.batch);
+      const int32_t b = (int32_t)(gl - (int64_t)t * a.batch);
+      const TableMeta m = a.meta[t];
+      if (m.kind / 8 != DT) continue;  // served by the launch for its storage type
+      if constexpr (LOG2 >= 0) {
+        pool_long_bag<DT, (1 << (LOG2 >= 0 ? LOG2 : 0)), W>(m, a, b, blo, bhi, part);
+      } else {
+        switch (m.kind % 8) {
+          case 0: pool_long_bag<DT, 1, W>(m, a, b, blo, bhi, part); break;
+          case 1: pool_long_bag<DT, 2, W>(m, a, b, blo, bhi, part); break;
+          case 2: pool_long_bag<DT, 4, W>(m, a, b, blo, bhi, part); break;
+          case 3: pool_long_bag<DT, 8, W>(m, a, b, blo, bhi, part); break;
+          case 4: pool_long_bag<DT, 16, W>(m, a, b, blo, bhi, part); break;
+          case 5: pool_long_bag<DT, 32, W>(m, a, b, blo, bhi, part); break;
+          case 6: pool_long_bag<DT, 64, W>(m, a, b, blo, bhi, part); break;
+          default: break;
+        }
+      }
+    }
+  }
+}
+
+// One wavefront per run of bags; with LONG, then the workgroup's long bags
+// together.  DT is the storage type the launch serves (wavefronts of other
+// tables skip their own bags).  LOG2 >= 0 fixes the lanes per row for handles
+// whose tables all share one kind; LOG2 < 0 switches on each table's lanes per
+// row.  Specialising keeps the register count (and so the occupancy) at what
+// that kind needs.  LONG is a specialisation of its own because the split
+// path's LDS and barriers slowed the common path by 7-10% on MI355X even when
+// no bag took it.
+template <int DT, int LOG2, bool W, bool LONG>
 __global__ __launch_bounds__(kBlock) void eb_pool_kernel(FwdArgs a) {
   const uint32_t blk = a.xcd_remap ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x;
+  BlockBags bb;
+  if constexpr (LONG) bb = block_bags(a, blk);
   const int32_t wid = (int32_t)blk * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  if (wid >= a.num_waves) return;
-  const int32_t t = wid / a.groups_per_table;
-  const int32_t b0 = (wid - t * a.groups_per_table) * a.bags_per_wave;
-  const int nb = (a.batch - b0) < a.bags_per_wave ? (a.batch - b0) : a.bags_per_wave;
-  const int32_t g0 = t * a.batch + b0;
-  const TableMeta m = a.meta[t];
-  if (m.kind / 8 != DT) return;
-
-  if constexpr (LOG2 >= 0) {
-    pool_all_passes<DT, (1 << LOG2), W>(m, a, g0, nb, b0);
-  } else {
-    switch (m.kind % 8) {
-      EB_LPR(0) EB_LPR(1) EB_LPR(2) EB_LPR(3) EB_LPR(4) EB_LPR(5) EB_LPR(6)
-      default:
-        break;
+  if (wid < a.num_waves) {
+    const int32_t t = wid / a.groups_per_table;
+    const int32_t b0 = (wid - t * a.groups_per_table) * a.bags_per_wave;
+    const int nb = (a.batch - b0) < a.bags_per_wave ? (a.batch - b0) : a.bags_per_wave;
+    const int32_t g0 = t * a.batch + b0;
+    const TableMeta m = a.meta[t];
+    if (m.kind / 8 == DT) {
+      if constexpr (LOG2 >= 0) {
+        pool_all_passes<DT, (1 << (LOG2 >= 0 ? LOG2 : 0)), W>(m, a, g0, nb, b0);
+      } else {
+        switch (m.kind % 8) {
+          EB_LPR(0) EB_LPR(1) EB_LPR(2) EB_LPR(3) EB_LPR(4) EB_LPR(5) EB_LPR(6)
+          default:
+            break;
+        }
+      }
     }
+  }
+  if constexpr (LONG) {
+    // every wavefront of the workgroup, its own bags done or not
+    __shared__ float long_part[kWavesPerBlock][kPassBytes / Vals<DT>::esize];
+    pool_block_long_bags<DT, LOG2, W>(a, bb, long_part);
   }
 }
 
@@ -190,25 +373,30 @@ __global__ __launch_bounds__(kBlock) void eb_pool_kernel(FwdArgs a) {
 
 typedef void (*KernelFn)(FwdArgs);
 
-// kernel for (storage type, log2 lanes per row or -1, weighted)
-template <int DT, bool W>
+// kernel for (storage type, log2 lanes per row or -1, weighted, long-bag split)
+template <int DT, bool W, bool LONG>
 KernelFn pick_kernel(int log2) {
   switch (log2) {
-    case 0: return eb_pool_kernel<DT, 0, W>;
-    case 1: return eb_pool_kernel<DT, 1, W>;
-    case 2: return eb_pool_kernel<DT, 2, W>;
-    case 3: return eb_pool_kernel<DT, 3, W>;
-    case 4: return eb_pool_kernel<DT, 4, W>;
-    case 5: return eb_pool_kernel<DT, 5, W>;
-    case 6: return eb_pool_kernel<DT, 6, W>;
-    default: return eb_pool_kernel<DT, -1, W>;
+    case 0: return eb_pool_kernel<DT, 0, W, LONG>;
+    case 1: return eb_pool_kernel<DT, 1, W, LONG>;
+    case 2: return eb_pool_kernel<DT, 2, W, LONG>;
+    case 3: return eb_pool_kernel<DT, 3, W, LONG>;
+    case 4: return eb_pool_kernel<DT, 4, W, LONG>;
+    case 5: return eb_pool_kernel<DT, 5, W, LONG>;
+    case 6: return eb_pool_kernel<DT, 6, W, LONG>;
+    default: return eb_pool_kernel<DT, -1, W, LONG>;
   }
 }
 
+template <bool LONG>
 KernelFn pick_kernel(int dt, int log2, bool weighted) {
-  if (dt == kF32) return weighted ? pick_kernel<kF32, true>(log2) : pick_kernel<kF32, false>(log2);
-  if (dt == kF16) return weighted ? pick_kernel<kF16, true>(log2) : pick_kernel<kF16, false>(log2);
-  return weighted ? pick_kernel<kU8, true>(log2) : pick_kernel<kU8, false>(log2);
+  if (dt == kF32) return weighted ? pick_kernel<kF32, true, LONG>(log2) : pick_kernel<kF32, false, LONG>(log2);
+  if (dt == kF16) return weighted ? pick_kernel<kF16, true, LONG>(log2) : pick_kernel<kF16, false, LONG>(log2);
+  return weighted ? pick_kernel<kU8, true, LONG>(log2) : pick_kernel<kU8, false, LONG>(log2);
+}
+
+KernelFn pick_kernel(int dt, int log2, bool weighted, bool split_long) {
+  return split_long ? pick_kernel<true>(dt, log2, weighted) : pick_kernel<false>(dt, log2, weighted);
 }
 
 }  // namespace
@@ -259,6 +447,7 @@ hipError_t launch_forward(const eb_tables *h, const eb_tensor &indices, const eb
   a.ctx.zero = h->d_zero;
   a.ctx.one = 1.0f;
   a.xcd_remap = h->xcd_remap;
+  a.long_len = h->long_bag_len > 0 ? h->long_bag_len : INT64_MAX;  // 0: no split
   a.num_indices = indices.numel;
   a.out_ld = h->sum_dim;
   a.num_bags = (int32_t)sh.num_bags;
@@ -286,7 +475,8 @@ hipError_t launch_forward(const eb_tables *h, const eb_tensor &indices, const eb
   // one launch per storage type present (one in the usual case)
   for (int dt = 0; dt < 3 && e == hipSuccess; ++dt) {
     if (!(h->dtype_mask & (1 << dt))) continue;
-    hipLaunchKernelGGL(pick_kernel(dt, h->single_log2, sh.weighted), dim3(grid), dim3(kBlock), 0, h->stream, a);
+    hipLaunchKernelGGL(pick_kernel(dt, h->single_log2, sh.weighted, h->long_bag_len > 0), dim3(grid), dim3(kBlock), 0,
+                       h->stream, a);
     e = hipGetLastError();
   }
   return e;
@@ -420,6 +610,10 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   const char *btc = getenv("EB_BWD_TILE_CHUNKS");
   h->bwd_tile_chunks = btc ? atoi(btc) : 0;
   if (h->bwd_tile_chunks < 0 || h->bwd_tile_chunks > 16) h->bwd_tile_chunks = 0;
+  const char *lb = getenv("EB_LONG_BAG");
+  h->long_bag_len = lb ? atoll(lb) : 0;
+  if (h->long_bag_len < 0) h->long_bag_len = 0;
+  if (h->long_bag_len > 0 && h->long_bag_len < kWavesPerBlock) h->long_bag_len = kWavesPerBlock;
   const char *bpw = getenv("EB_BAGS_PER_WAVE");
   h->bags_per_wave = bpw ? atoi(bpw) : 0;
   if (h->bags_per_wave < 0 || h->bags_per_wave > kMaxBagsPerWave) h->bags_per_wave = 0;

@@ -154,6 +154,17 @@ def test_bags_per_wave(dev, monkeypatch, name, k):
     full_check(w, f"k={k} {name}")
 
 
+@pytest.mark.parametrize("long_len", ["4", "16", "64"])
+@pytest.mark.parametrize("name", ["c1", "c2", "c3a", "c3b", "c4", "c5"])
+def test_long_bags_split_over_the_workgroup(dev, monkeypatch, name, long_len):
+    # bags longer than EB_LONG_BAG lookups are pooled by the workgroup's four
+    # wavefronts together; a low threshold sends many bags down that path
+    say(f"[parity] long-bag split at {long_len} {name}")
+    monkeypatch.setenv("EB_LONG_BAG", long_len)
+    w = make_workload(name, dev, **REDUCED[name])
+    full_check(w, f"long>{long_len} {name}")
+
+
 # ----------------------------------------------------------------------------
 # full sizes, in the launch configuration the benchmark times
 
@@ -284,6 +295,31 @@ def test_every_width_in_one_launch(dev, monkeypatch, mode, k):
         l[0], l[1], l[2] = 0, 1, 129  # empty, one row, just over two index chunks
     w = _custom(dev, tables, lens, weighted=(mode == "weighted"), pooling="mean" if mode == "mean" else "sum")
     full_check(w, f"widths {mode}")
+
+
+@pytest.mark.parametrize("mode", ["sum", "mean", "weighted"])
+def test_long_bag_split_every_width(dev, monkeypatch, mode):
+    say(f"[parity] long-bag split, every width, {mode}")
+    monkeypatch.setenv("EB_LONG_BAG", "8")
+    rng = np.random.default_rng(15)
+    tables = [_table(dev, dt, 300 + 7 * i, D, seed=i) for i, (dt, D) in enumerate(WIDTHS)]
+    lens = [rng.integers(0, 40, 13) for _ in tables]
+    for l in lens:
+        l[0], l[1], l[2], l[3] = 0, 1, 9, 8  # empty, one row, just long, just not long
+    w = _custom(dev, tables, lens, weighted=(mode == "weighted"), pooling="mean" if mode == "mean" else "sum")
+    full_check(w, f"long split widths {mode}")
+
+
+@pytest.mark.parametrize("long_len", ["0", "4096"])
+def test_one_very_long_bag(dev, monkeypatch, long_len):
+    # a bag of 300 000 lookups among short ones: one wavefront per bag (the
+    # default), or split over the workgroup above 4096 lookups
+    say(f"[parity] one very long bag, EB_LONG_BAG={long_len}")
+    monkeypatch.setenv("EB_LONG_BAG", long_len)
+    tables = [_table(dev, "f32", 100000, 64), _table(dev, "f16", 50000, 128, seed=1)]
+    lens = [np.array([3, 300000, 0, 7, 4097, 1]), np.array([4096, 2, 200000, 0, 5, 9])]
+    w = _custom(dev, tables, lens)
+    full_check(w, "very long bag")
 
 
 def test_padded_row_strides(dev):
