@@ -153,19 +153,29 @@ __global__ __launch_bounds__(1024) void eb_bwd_tile_start_kernel(BwdArgs a) {
     table_range(a, t, p0, p1);
     sum += (p1 - p0 + a.tile_size - 1) / a.tile_size;
   }
-  part[tid] = sum;
+  // exclusive scan of the per-thread sums: within each wavefront, then over
+  // the 16 wavefronts' totals
+  const int lane = tid & (kWave - 1), wave = tid / kWave;
+  int64_t incl = sum;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int64_t v = __shfl_up(incl, o);
+    if (lane >= o) incl += v;
+  }
+  if (lane == kWave - 1) part[wave] = incl;
   __syncthreads();
-  if (tid == 0) {
-    int64_t run = 0;
-    for (int i = 0; i < 1024; ++i) {
-      const int64_t v = part[i];
-      part[i] = run;
-      run += v;
+  if (wave == 0) {
+    int64_t w = lane < 1024 / kWave ? part[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < 1024 / kWave; o <<= 1) {
+      const int64_t v = __shfl_up(w, o);
+      if (lane >= o) w += v;
     }
-    a.tile_start[T] = (int32_t)run;
+    if (lane < 1024 / kWave) part[kWave + lane] = w;  // inclusive totals of waves 0..lane
   }
   __syncthreads();
-  int64_t run = part[tid];
+  int64_t run = incl - sum + (wave > 0 ? part[kWave + wave - 1] : 0);
+  if (tid == 1023) a.tile_start[T] = (int32_t)(run + sum);
   for (int t = t0; t < t1; ++t) {
     a.tile_start[t] = (int32_t)run;
     int64_t p0, p1;
