@@ -1,6 +1,8 @@
 /*
  * eb.h — C ABI of libeb: the jagged, pooled EmbeddingBag forward on one
- * AMD Instinct MI355X (gfx950).
+ * AMD Instinct MI355X (gfx950), with its backward and fused row-wise
+ * optimizer step, the un-pooled (sequence) lookup, and the
+ * factorization-machine cross term over the pooled output.
  *
  * The operation.  The paper's DLRM study (Sec. IV-A.2, icicle view) splits a
  * recommendation model into sparse_arch, which looks rows up in embedding
@@ -34,8 +36,9 @@
  * into a small device array that it owns.
  *
  * Streams and synchronisation.  The HIP stream is fixed when the handle is
- * created.  eb_forward only enqueues one kernel on it and returns; `out` is
- * valid once that stream has been synchronised.  A handle is immutable after
+ * created.  eb_forward only enqueues its kernel (one per storage type
+ * present) on it and returns; `out` is valid once that stream has been
+ * synchronised.  The other entry points behave the same way.  A handle is immutable after
  * creation, so forwards from several host threads may share it.
  *
  * Errors.  Every error the host can detect from the arguments is returned

@@ -1,6 +1,7 @@
 // eb_device.h — internal to libeb: the table descriptor the kernels read, the
 // 16-byte-slice row gather with its convert/accumulate step, and the
-// cross-lane reduce-scatter, shared by the forward and backward kernels.
+// cross-lane reduce-scatter, shared by the pooled and un-pooled lookups, the
+// FM pass and the backward; and the host-side checks the lookups share.
 // Not part of the C ABI (include/eb.h is).
 #ifndef EB_DEVICE_H_
 #define EB_DEVICE_H_

@@ -21,8 +21,12 @@
 //     and the owning lanes store the pooled vector;
 //   * a handle whose tables share one (storage type, LPR) kind launches a body
 //     specialised for it; otherwise one launch per storage type switches on
-//     each table's LPR.
-// Rows wider than 1 KiB take several 1 KiB column passes.
+//     each table's LPR;
+//   * optionally (EB_LONG_BAG at create time), bags longer than a threshold
+//     are pooled by all four wavefronts of their workgroup together.
+// Rows wider than 1 KiB take several 1 KiB column passes.  This file also
+// holds the C ABI's handle creation and the checks shared by the entry points
+// that pool.
 
 #include "eb_device.h"
 

@@ -2,8 +2,8 @@
 
 Each function has the name of the C entry point it calls (include/eb.h) and
 turns torch tensors into the plain pointers and sizes the C ABI takes.  Every
-step of the pooled lookup runs in libeb's HIP kernels; torch only owns the
-device memory and the stream.  If libeb.so has not been built this module
+step of the lookups, the FM term and the backward runs in libeb's HIP
+kernels; torch only owns the device memory and the stream.  If libeb.so has not been built this module
 raises on first use: there is no other implementation to fall back to.
 """
 from __future__ import annotations
