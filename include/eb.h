@@ -124,7 +124,7 @@ typedef enum { EB_POOL_SUM = 0, EB_POOL_MEAN = 1 } eb_pooling;
  *   EB_ERR_UNSUPPORTED.
  */
 typedef struct {
-  const void *data;         /* device pointer to row 0 */
+  const void *data;         /* pointer to row 0 (memory the device can read) */
   int64_t num_rows;         /* R_t */
   int32_t dim;              /* D_t */
   int32_t dtype;            /* eb_table_dtype */
@@ -148,7 +148,10 @@ typedef struct eb_tables eb_tables;
  * device at this call is the handle's device.  On success *out receives the
  * handle, which the caller releases with eb_destroy.  Synchronous: allocates
  * one small device array (EB_ERR_OOM if that fails) and copies the
- * descriptors into it.  On error *out is set to NULL.
+ * descriptors into it.  Each table's rows must be memory the handle's device
+ * can read in place: its own device memory, managed memory or pinned host
+ * memory; pageable host memory and another device's memory give
+ * EB_ERR_INVALID_ARG.  On error *out is set to NULL.
  * Paper: Sec. IV-A.2 (sparse_arch's embedding tables) and Sec. III-B.1
  * (tables too large for one GPU are shrunk to fit it, so the handle takes
  * tables of any row count that fits in device memory).

@@ -486,6 +486,19 @@ hipError_t launch_forward(const eb_tables *h, const eb_tensor &indices, const eb
   return e;
 }
 
+// Whether kernels on device `dev` can read memory at p: that device's own
+// memory, managed memory or pinned host memory (not pageable host memory, and
+// not another device's memory).
+static bool device_can_read(const void *p, int dev) {
+  hipPointerAttribute_t at;
+  if (hipPointerGetAttributes(&at, p) != hipSuccess) {
+    (void)hipGetLastError();  // an unknown pointer leaves the error behind
+    return false;
+  }
+  if (at.type == hipMemoryTypeDevice) return at.device == dev;
+  return at.type == hipMemoryTypeManaged || at.type == hipMemoryTypeHost || at.type == hipMemoryTypeUnified;
+}
+
 hipError_t begin_checked(const eb_tables *h) {
   return h->checked ? hipMemsetAsync(h->d_err, 0, sizeof(int), h->stream) : hipSuccess;
 }
@@ -587,6 +600,14 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
     free(meta);
     free(h);
     return EB_ERR_HIP;
+  }
+  // the kernels read the rows in place: refuse memory this device cannot reach
+  for (int32_t t = 0; t < num_tables; ++t) {
+    if (!device_can_read(descs[t].data, h->device)) {
+      free(meta);
+      free(h);
+      return EB_ERR_INVALID_ARG;
+    }
   }
   h->stream = static_cast<hipStream_t>(hip_stream);
   h->num_tables = num_tables;

@@ -107,11 +107,12 @@ def eb_status_string(status: int) -> str:
 class EbTables:
     """Handle returned by eb_create_tables; keeps the table tensors alive."""
 
-    def __init__(self, ptr: int, tables, stream, sum_dim: int):
+    def __init__(self, ptr: int, tables, stream, sum_dim: int, device: Optional[torch.device] = None):
         self.ptr = ptr
         self.tables = list(tables)
         self.stream = stream
         self.sum_dim = sum_dim
+        self.device = device
 
     @property
     def num_tables(self) -> int:
@@ -122,6 +123,15 @@ class EbTables:
 
     def __exit__(self, *exc):
         eb_destroy(self)
+
+
+def _torch_stream(stream, device: torch.device) -> torch.cuda.Stream:
+    """The handle's stream as a torch stream (None: the null stream)."""
+    if stream is None or (isinstance(stream, int) and stream == 0):
+        return torch.cuda.default_stream(device)
+    if isinstance(stream, int):
+        return torch.cuda.ExternalStream(stream, device=device)
+    return stream
 
 
 def _stream_handle(stream) -> Optional[int]:
@@ -141,6 +151,9 @@ def eb_create_tables(tables: Sequence, stream=None) -> EbTables:
     for t in tables:
         rows, dim, dtype = (t.rows, t.dim, t.dtype) if hasattr(t, "rows") else t
         norm.append((rows, int(dim), dtype))
+    devices = {r.device for r, _, _ in norm}
+    if any(d.type != "cuda" for d in devices) or len(devices) > 1:
+        raise ValueError(f"eb tables must be device tensors of one GPU, got {sorted(map(str, devices))}")
     descs = (eb_table_desc * len(norm))()
     for i, (rows, dim, dtype) in enumerate(norm):
         descs[i].data = rows.data_ptr() if rows.numel() else None
@@ -152,17 +165,23 @@ def eb_create_tables(tables: Sequence, stream=None) -> EbTables:
     st = lib.eb_create_tables(descs, len(norm), _stream_handle(stream), ctypes.byref(out))
     if st != EB_OK:
         raise EBError(st, "eb_create_tables")
-    return EbTables(out.value, [r for r, _, _ in norm], stream, sum(d for _, d, _ in norm))
+    return EbTables(out.value, [r for r, _, _ in norm], stream, sum(d for _, d, _ in norm),
+                    norm[0][0].device if norm else None)
 
 
 _ELEM = {torch.int32: EB_I32, torch.int64: EB_I64, torch.float32: EB_T_F32}
 
 
-def _as_tensor(t: Optional[torch.Tensor]) -> eb_tensor:
+def _as_tensor(t: Optional[torch.Tensor], device: Optional[torch.device] = None) -> eb_tensor:
+    """The eb_tensor view of a contiguous device tensor (of `device`, the
+    handle's GPU, when given): the kernels read these pointers directly, so a
+    host tensor is refused here rather than handed to the GPU."""
     if t is None:
         return eb_tensor(None, 0, EB_T_F32)
     if not t.is_contiguous():
         raise ValueError("eb tensors must be contiguous")
+    if t.device.type != "cuda" or (device is not None and t.device != device):
+        raise ValueError(f"eb tensors must be on the handle's GPU ({device}), got one on {t.device}")
     return eb_tensor(t.data_ptr() if t.numel() else None, t.numel(), _ELEM.get(t.dtype, 99))
 
 
@@ -171,8 +190,9 @@ def eb_forward(tables: EbTables, indices: torch.Tensor, offsets: torch.Tensor,
     """Enqueue the pooled lookup on the handle's stream; returns `out`."""
     lib = load_library()
     mode = POOLING[pooling] if isinstance(pooling, str) else int(pooling)
-    st = lib.eb_forward(tables.ptr, _as_tensor(indices), _as_tensor(offsets), _as_tensor(per_sample_weights),
-                        mode, _as_tensor(out))
+    d = tables.device
+    st = lib.eb_forward(tables.ptr, _as_tensor(indices, d), _as_tensor(offsets, d),
+                        _as_tensor(per_sample_weights, d), mode, _as_tensor(out, d))
     if st != EB_OK:
         raise EBError(st, "eb_forward")
     return out
@@ -181,7 +201,8 @@ def eb_forward(tables: EbTables, indices: torch.Tensor, offsets: torch.Tensor,
 def eb_forward_seq(tables: EbTables, indices: torch.Tensor, offsets: torch.Tensor, out: torch.Tensor) -> torch.Tensor:
     """Un-pooled lookup: every position's row as fp32 into out (table t's
     positions as a [N_t, D_t] block, blocks in table order); returns out."""
-    st = load_library().eb_forward_seq(tables.ptr, _as_tensor(indices), _as_tensor(offsets), _as_tensor(out))
+    d = tables.device
+    st = load_library().eb_forward_seq(tables.ptr, _as_tensor(indices, d), _as_tensor(offsets, d), _as_tensor(out, d))
     if st != EB_OK:
         raise EBError(st, "eb_forward_seq")
     return out
@@ -189,7 +210,8 @@ def eb_forward_seq(tables: EbTables, indices: torch.Tensor, offsets: torch.Tenso
 
 def eb_fm_cross(tables: EbTables, pooled: torch.Tensor, fm_out: torch.Tensor) -> torch.Tensor:
     """FM cross term of each example of a pooled output [B, T*D] into fm_out [B]; returns fm_out."""
-    st = load_library().eb_fm_cross(tables.ptr, _as_tensor(pooled), _as_tensor(fm_out))
+    d = tables.device
+    st = load_library().eb_fm_cross(tables.ptr, _as_tensor(pooled, d), _as_tensor(fm_out, d))
     if st != EB_OK:
         raise EBError(st, "eb_fm_cross")
     return fm_out
@@ -201,8 +223,9 @@ def eb_forward_fm(tables: EbTables, indices: torch.Tensor, offsets: torch.Tensor
     """eb_forward, then eb_fm_cross on its output into fm_out [B]; returns fm_out."""
     lib = load_library()
     mode = POOLING[pooling] if isinstance(pooling, str) else int(pooling)
-    st = lib.eb_forward_fm(tables.ptr, _as_tensor(indices), _as_tensor(offsets), _as_tensor(per_sample_weights),
-                           mode, _as_tensor(out), _as_tensor(fm_out))
+    d = tables.device
+    st = lib.eb_forward_fm(tables.ptr, _as_tensor(indices, d), _as_tensor(offsets, d),
+                           _as_tensor(per_sample_weights, d), mode, _as_tensor(out, d), _as_tensor(fm_out, d))
     if st != EB_OK:
         raise EBError(st, "eb_forward_fm")
     return fm_out
@@ -232,15 +255,22 @@ def eb_backward_update(tables: EbTables, indices: torch.Tensor, offsets: torch.T
     """Enqueue the backward + optimizer step on the handle's stream.
 
     workspace: a device uint8 tensor of at least eb_backward_workspace_size()
-    bytes; when None one is allocated (torch owns it)."""
+    bytes that stays untouched until the step has run on the handle's stream;
+    when None, one is allocated on that stream (torch's allocator then reuses
+    it only for work ordered after the step on the same stream)."""
     lib = load_library()
+    d = tables.device
+    args = (_as_tensor(indices, d), _as_tensor(offsets, d), _as_tensor(per_sample_weights, d))
+    g, st_t = _as_tensor(grad_out, d), _as_tensor(optimizer_state, d)
     if workspace is None:
         nbytes = eb_backward_workspace_size(tables, indices.numel())
-        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=grad_out.device)
+        with torch.cuda.stream(_torch_stream(tables.stream, d)):
+            workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=d)
+    elif workspace.device != d:
+        raise ValueError(f"the workspace must be on the handle's GPU ({d}), got one on {workspace.device}")
     mode = POOLING[pooling] if isinstance(pooling, str) else int(pooling)
     opt = OPTIMIZERS[optimizer] if isinstance(optimizer, str) else int(optimizer)
-    st = lib.eb_backward_update(tables.ptr, _as_tensor(indices), _as_tensor(offsets), _as_tensor(per_sample_weights),
-                                mode, _as_tensor(grad_out), opt, float(learning_rate), float(eps),
-                                _as_tensor(optimizer_state), workspace.data_ptr(), workspace.numel())
+    st = lib.eb_backward_update(tables.ptr, *args, mode, g, opt, float(learning_rate), float(eps),
+                                st_t, workspace.data_ptr(), workspace.numel())
     if st != EB_OK:
         raise EBError(st, "eb_backward_update")

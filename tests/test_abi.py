@@ -116,3 +116,22 @@ def test_binding_fails_loudly_without_the_library(tmp_path):
             eb.load_library(str(tmp_path / "missing.so"))
         finally:
             eb._lib = saved
+
+
+def test_binding_refuses_host_tensors(lib):
+    # the kernels read these pointers directly: a host tensor must never reach them
+    import torch
+
+    with pytest.raises(ValueError, match="device tensors"):
+        eb.eb_create_tables([(torch.zeros(10, 16), 16, "f32")])
+    h = eb.EbTables(None, [], None, 16, torch.device("cuda:0"))
+    idx, off = torch.zeros(4, dtype=torch.int64), torch.tensor([0, 2, 4])
+    out = torch.empty(2, 16)
+    with pytest.raises(ValueError, match="handle's GPU"):
+        eb.eb_forward(h, idx, off, None, "sum", out)
+    with pytest.raises(ValueError, match="handle's GPU"):
+        eb.eb_forward_seq(h, idx, off, torch.empty(64))
+    with pytest.raises(ValueError, match="handle's GPU"):
+        eb.eb_fm_cross(h, out, torch.empty(2))
+    with pytest.raises(ValueError, match="handle's GPU"):
+        eb.eb_backward_update(h, idx, off, None, "sum", out, workspace=torch.empty(8, dtype=torch.uint8))

@@ -400,6 +400,32 @@ def test_forward_argument_errors(dev):
         assert torch.all(out == 7.0)  # nothing was written
 
 
+def test_create_refuses_memory_the_gpu_cannot_read(dev):
+    # kernels read the rows in place: pageable host memory is refused at
+    # creation; device and pinned host memory are accepted (no lookup is run
+    # on the host rows)
+    say("[parity] table memory the GPU cannot read")
+    import ctypes
+
+    lib = eb.load_library()
+
+    def create(ptr):
+        arr = (eb.eb_table_desc * 1)(eb.eb_table_desc(ptr, 10, 16, eb.EB_F32, 64))
+        h = ctypes.c_void_p(0)
+        st = lib.eb_create_tables(arr, 1, None, ctypes.byref(h))
+        return st, h.value
+
+    host = np.zeros(10 * 16 + 4, np.float32)
+    st, h = create((host.ctypes.data + 15) // 16 * 16)
+    assert st == eb.EB_ERR_INVALID_ARG and h is None
+    for rows in (torch.zeros((10, 16), device=dev), torch.zeros((10, 16), pin_memory=True)):
+        st, h = create(rows.data_ptr())
+        assert st == eb.EB_OK and h
+        assert lib.eb_destroy(h) == eb.EB_OK
+    with pytest.raises(ValueError):
+        eb.eb_create_tables([(torch.zeros(10, 16), 16, "f32")])
+
+
 def test_checked_mode_reports_bad_data(dev, monkeypatch):
     say("[parity] checked mode")
     monkeypatch.setenv("EB_CHECK", "1")
