@@ -39,7 +39,11 @@
  * created.  eb_forward only enqueues its kernel (one per storage type
  * present) on it and returns; `out` is valid once that stream has been
  * synchronised.  The other entry points behave the same way.  A handle is immutable after
- * creation, so forwards from several host threads may share it.
+ * creation, so forwards from several host threads may share it.  eb_forward,
+ * eb_forward_fm and eb_forward_seq allocate nothing and, outside checked
+ * mode, enqueue only kernel launches, so they may be captured into a HIP
+ * graph on the handle's stream and replayed (the captured launches read
+ * whatever the buffers hold at replay time).
  *
  * Errors.  Every error the host can detect from the arguments is returned
  * before anything is enqueued, and `out` is left untouched.  The kernel never
