@@ -58,22 +58,27 @@ struct FwdArgs {
 // one stream of chunks of up to 64; the next chunk's indices are loaded before
 // the current chunk's rows are gathered, so each chunk costs one memory round
 // trip.
+// offsets[g0 .. g0 + nb] of a run of bags, one per lane (lanes past nb hold 0)
+__device__ __forceinline__ int64_t run_offsets(const FwdArgs &a, int32_t g0, int nb) {
+  const int lane = threadIdx.x & (kWave - 1);
+  int64_t o = 0;
+  if (lane <= nb) {
+    o = a.idx64 ? static_cast<const int64_t *>(a.offsets)[g0 + lane]
+                : (int64_t) static_cast<const int32_t *>(a.offsets)[g0 + lane];
+  }
+  return o;
+}
+
 template <int DT, int LPR, bool W>
 __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, int32_t g0, int nb, int32_t b0,
-                                          int col_base) {
+                                          int col_base, int64_t my_off) {
   // (bags longer than a.long_len are pooled by pool_long_bags: skipped here)
+  // my_off: run_offsets(a, g0, nb)
   using R = Reduce<DT, LPR>;
   constexpr int V = Vals<DT>::n;
   const int lane = threadIdx.x & (kWave - 1);
   const int colb = col_base + (lane % LPR) * 16;
   const bool colok = colb < m.code_bytes;
-
-  // offsets[g0 .. g0 + nb]: one per lane
-  int64_t my_off = 0;
-  if (lane <= nb) {
-    my_off = a.idx64 ? static_cast<const int64_t *>(a.offsets)[g0 + lane]
-                     : (int64_t) static_cast<const int32_t *>(a.offsets)[g0 + lane];
-  }
   // bag j's index range, clamped into [0, N) so nothing is read outside the
   // index array whatever the offsets hold (a broken partition is reported)
   auto bag_range = [&](int j, int64_t &lo, int64_t &hi, bool &skip) {
@@ -234,17 +239,17 @@ __device__ __forceinline__ void pool_long_bag(const TableMeta &m, const FwdArgs 
 
 template <int DT, int LPR, bool W>
 __device__ __forceinline__ void pool_all_passes(const TableMeta &m, const FwdArgs &a, int32_t g0, int nb,
-                                                int32_t b0) {
+                                                int32_t b0, int64_t my_off) {
   if constexpr (LPR == kWave) {
-    for (int p = 0; p < m.passes; ++p) pool_bags<DT, LPR, W>(m, a, g0, nb, b0, p * kPassBytes);
+    for (int p = 0; p < m.passes; ++p) pool_bags<DT, LPR, W>(m, a, g0, nb, b0, p * kPassBytes, my_off);
   } else {
-    pool_bags<DT, LPR, W>(m, a, g0, nb, b0, 0);
+    pool_bags<DT, LPR, W>(m, a, g0, nb, b0, 0, my_off);
   }
 }
 
 #define EB_LPR(LOG2)                                                          \
   case LOG2:                                                                  \
-    pool_all_passes<DT, (1 << (LOG2)), W>(m, a, g0, nb, b0);                  \
+    pool_all_passes<DT, (1 << (LOG2)), W>(m, a, g0, nb, b0, my_off);          \
     break;
 
 // The workgroup's bags [G0, G1) and the offsets at both ends (clamped into
@@ -353,10 +358,12 @@ __global__ __launch_bounds__(kBlock) void eb_pool_kernel(FwdArgs a) {
     const int32_t b0 = (wid - t * a.groups_per_table) * a.bags_per_wave;
     const int nb = (a.batch - b0) < a.bags_per_wave ? (a.batch - b0) : a.bags_per_wave;
     const int32_t g0 = t * a.batch + b0;
+    // the offsets' address needs no table descriptor: issue that load first
+    const int64_t my_off = run_offsets(a, g0, nb);
     const TableMeta m = a.meta[t];
     if (m.kind / 8 == DT) {
       if constexpr (LOG2 >= 0) {
-        pool_all_passes<DT, (1 << (LOG2 >= 0 ? LOG2 : 0)), W>(m, a, g0, nb, b0);
+        pool_all_passes<DT, (1 << (LOG2 >= 0 ? LOG2 : 0)), W>(m, a, g0, nb, b0, my_off);
       } else {
         switch (m.kind % 8) {
           EB_LPR(0) EB_LPR(1) EB_LPR(2) EB_LPR(3) EB_LPR(4) EB_LPR(5) EB_LPR(6)
