@@ -23,8 +23,11 @@
 //      forward's 16-byte-slice gather and reduce-scatter (the gradient is an
 //      fp32 "table" of B rows), and updates the run's table row; a run that
 //      crosses a tile boundary leaves a partial sum in a per-tile slot;
-//   4. a fix-up pass sums each crossing run's partials in tile order and
-//      updates its row.
+//   4. a fix-up pass sums each crossing run's partials in a fixed order (set
+//      by the run's length) and updates its row; each tile's info word (its
+//      table, the key of its last run, whether that run goes on and whether
+//      it started there) lets the pass find a run's tiles without the sorted
+//      keys.
 // Long runs (the hottest rows of a Zipf workload appear tens of thousands of
 // times per batch) are thereby spread over as many wavefronts as they have
 // tiles, and no wavefront waits for another.
@@ -55,7 +58,7 @@ struct BwdArgs {
   const uint32_t *skeys;  // [N] sorted keys
   const uint32_t *spos;   // [N] in sorted order: positions, or bag ids when sorted_bags
   int32_t *tile_start;    // [T + 1] first tile of each table; [T] = number of tiles
-  uint8_t *tile_flags;    // [tiles] kTileContinues | kTileOwnsRun
+  uint64_t *tile_info;    // [tiles] flags | table << 8 | key of the tile's last run << 32
   float *carry;           // [2 * tiles * max_dim]: slot 2w = head run partial, 2w+1 = tail run partial
   int64_t num_indices;
   int64_t grad_ld;        // sum D
@@ -388,7 +391,8 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
   if (lane == 0) {
     const bool cont = after != kNoKey && after == key_last;
     const bool owns = cont && key_last != before && key_last < sentinel && key_last >= kmin;
-    a.tile_flags[w] = (uint8_t)((cont ? kTileContinues : 0) | (owns ? kTileOwnsRun : 0));
+    a.tile_info[w] = (uint64_t)((cont ? kTileContinues : 0) | (owns ? kTileOwnsRun : 0)) | ((uint64_t)t << 8) |
+                     ((uint64_t)key_last << 32);
   }
 
   // the gradient rows of this table as an fp32 table of B rows
@@ -559,59 +563,95 @@ __global__ __launch_bounds__(kBlock) void eb_bwd_fixup_kernel(BwdArgs a) {
   const int32_t w = (int32_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int32_t total = a.tile_start[a.num_tables];
   if (w >= total) return;
-  if (!(a.tile_flags[w] & kTileOwnsRun)) return;
-  const int32_t t = table_of_tile(a, w);
+  // every tile below `total` holds at least one position, so its info word
+  // was written by this step's tiles kernel
+  const uint64_t info = a.tile_info[w];
+  if (!(info & kTileOwnsRun)) return;
+  const int32_t t = (int32_t)((info >> 8) & 0xFFFFFFu);
+  const uint32_t key = (uint32_t)(info >> 32);
   const TableMeta m = a.meta[t];
   if (m.kind / 8 != TDT) return;
   const int lane = threadIdx.x & (kWave - 1);
-  int64_t p0, p1;
-  table_range(a, t, p0, p1);
-  const int32_t k0 = w - a.tile_start[t];
-  const int32_t ntiles = a.tile_start[t + 1] - a.tile_start[t];
-  auto tile_last = [&](int32_t kk) {
-    const int64_t e = p0 + (int64_t)(kk + 1) * a.tile_size;
-    return (e < p1 ? e : p1) - 1;
+  // Row columns are held 4 per lane by L lanes (L = the next power of two
+  // >= dim/4); the wavefront's G = 64/L lane groups add the partials of
+  // tiles w+1+gi, w+1+gi+G, ... (group gi), and group 0 then adds the
+  // groups' sums in group order.  The order of the sum is fixed by the run's
+  // length alone, so results are reproducible.
+  int L = 1;
+  while (L < kWave && 4 * L < m.dim) L <<= 1;
+  const int G = kWave / L;
+  const int gi = lane / L;
+  const int col = 4 * (lane % L);
+  const bool cols = col < m.dim;
+  const bool own = cols && gi == 0;
+  constexpr int kBatch = 8;
+  auto head = [&](int32_t tile) {  // partial of the run that enters `tile`
+    return *reinterpret_cast<const f32x4 *>(a.carry + ((int64_t)2 * tile) * a.max_dim + col);
   };
-  const uint32_t key = a.skeys[tile_last(k0)];
-  // last tile of the run: the first tile kk > k0 that the run does not fill
-  // and go on past (the table's last tile never goes on)
-  int32_t kend = ntiles - 1;
-  for (int32_t base = k0 + 1; base < ntiles; base += kWave) {
-    const int32_t kk = base + lane;
-    bool stop = false;
-    if (kk < ntiles) {
-      const int32_t wk = a.tile_start[t] + kk;
-      stop = !((a.tile_flags[wk] & kTileContinues) && a.skeys[tile_last(kk)] == key);
-    }
-    const uint64_t hit = __ballot(kk < ntiles && stop);
-    if (hit) {
-      kend = base + (int32_t)__builtin_ctzll(hit);
+  // Issued before the run's end is known: the row and its state, this
+  // tile's partial and that of tile w + 1, which is always in the run.
+  const RowPrefetch<TDT, 4> pre = prefetch_row<TDT, 4>(m, a, (int64_t)(key - m.key_base), own, col);
+  f32x4 tail = {0.0f, 0.0f, 0.0f, 0.0f}, next = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (own) {
+    tail = *reinterpret_cast<const f32x4 *>(a.carry + ((int64_t)2 * w + 1) * a.max_dim + col);
+    next = head(w + 1);
+  }
+  // The run's last tile kend: every tile of the run but its last goes on
+  // with the same key, and no tile after it does (the keys are sorted, and a
+  // table's last tile never goes on), so it is the first tile after w that
+  // fails the test.  Most runs end within the next 64 tiles (one load per
+  // lane); longer ones are searched coarse to fine: tiles 64 apart, then the
+  // 64 tiles before the first hit.
+  auto ends = [&](int32_t kk) -> bool {
+    if (kk >= total) return true;
+    const uint64_t x = a.tile_info[kk];
+    return !((x & kTileContinues) && (uint32_t)(x >> 32) == key);
+  };
+  int32_t kend = w + 1;
+  const uint64_t near = __ballot(ends(w + 1 + lane));
+  if (near) {
+    kend = w + 1 + (int32_t)__builtin_ctzll(near);
+  } else {
+    const int32_t first = w + 1 + kWave;  // no tile before it ends
+    for (int32_t lo = first;; lo += kWave * kWave) {
+      const uint64_t coarse = __ballot(ends(lo + lane * kWave));
+      if (!coarse) continue;
+      // the first tile that ends lies in (lo + (j-1)*64, lo + j*64]
+      const int j = __builtin_ctzll(coarse);
+      int32_t base = lo + (j - 1) * kWave + 1;
+      base = base > first ? base : first;
+      kend = base + (int32_t)__builtin_ctzll(__ballot(ends(base + lane)));
       break;
     }
   }
-  const int col = 4 * lane;
-  const bool own = col < m.dim;
-  const RowPrefetch<TDT, 4> pre = prefetch_row<TDT, 4>(m, a, (int64_t)(key - m.key_base), own, col);
   float g[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (own) {
-    const f32x4 v = *reinterpret_cast<const f32x4 *>(a.carry + ((int64_t)2 * w + 1) * a.max_dim + col);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) g[i] = v[i];
-    constexpr int kBatch = 8;
-    for (int32_t kk = k0 + 1; kk <= kend; kk += kBatch) {
+    for (int i = 0; i < 4; ++i) g[i] = tail[i] + next[i];
+  }
+  if (cols) {
+    // group 0 has added tile w + 1 already; past kend a load re-reads kk and
+    // is not added
+    for (int32_t kk = w + 1 + gi + (gi == 0 ? G : 0); kk <= kend; kk += kBatch * G) {
       f32x4 v8[kBatch];
 #pragma unroll
-      for (int j = 0; j < kBatch; ++j) {
-        const int32_t kj = kk + j <= kend ? kk + j : kend;  // past the end: re-read the last, not added
-        v8[j] = *reinterpret_cast<const f32x4 *>(a.carry + ((int64_t)2 * (a.tile_start[t] + kj)) * a.max_dim + col);
-      }
+      for (int j = 0; j < kBatch; ++j) v8[j] = head(kk + j * G <= kend ? kk + j * G : kk);
 #pragma unroll
       for (int j = 0; j < kBatch; ++j) {
-        if (kk + j <= kend) {
+        if (kk + j * G <= kend) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) g[i] += v8[j][i];
         }
       }
+    }
+  }
+  for (int q = 1; q < G; ++q) {
+    float o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = __shfl(g[i], (lane % L) + q * L);
+    if (gi == 0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) g[i] += o[i];
     }
   }
   apply_update<TDT, 4>(m, a, (int64_t)(key - m.key_base), g, own, col, pre);
@@ -635,7 +675,7 @@ KernelFn pick_tiles(int log2) {
 
 // Workspace regions (each 256-byte aligned).
 struct BwdLayout {
-  size_t keys, skeys, spos, bag_of, tile_start, tile_flags, carry, sort_tmp, total;
+  size_t keys, skeys, spos, bag_of, tile_start, tile_info, carry, sort_tmp, total;
   size_t sort_bytes;
   int64_t tiles_ub;
   int32_t tile_size;
@@ -687,8 +727,8 @@ eb_status layout(const eb_tables *h, int64_t n, BwdLayout *L) {
   off += align256(4 * (size_t)n);
   L->tile_start = off;
   off += align256(4 * (size_t)(h->num_tables + 1));
-  L->tile_flags = off;
-  off += align256((size_t)L->tiles_ub);
+  L->tile_info = off;
+  off += align256(8 * (size_t)L->tiles_ub);
   L->carry = off;
   off += align256(4 * (size_t)2 * L->tiles_ub * h->max_dim);
   L->sort_tmp = off;
@@ -776,7 +816,7 @@ eb_status eb_backward_update(const eb_tables *h, eb_tensor indices, eb_tensor of
   a.skeys = reinterpret_cast<const uint32_t *>(ws + L.skeys);
   a.spos = reinterpret_cast<const uint32_t *>(ws + L.spos);
   a.tile_start = reinterpret_cast<int32_t *>(ws + L.tile_start);
-  a.tile_flags = reinterpret_cast<uint8_t *>(ws + L.tile_flags);
+  a.tile_info = reinterpret_cast<uint64_t *>(ws + L.tile_info);
   a.carry = reinterpret_cast<float *>(ws + L.carry);
   a.num_indices = n;
   a.grad_ld = h->sum_dim;

@@ -158,6 +158,37 @@ def test_hot_row_spans_many_tiles(dev, monkeypatch, chunks):
     run_and_check(w, dev, "sgd", label="hot row sgd")
 
 
+def test_hot_rows_of_every_lane_grouping(dev, monkeypatch):
+    # The fix-up adds a crossing run's tile partials with 64/L lane groups
+    # (L lanes hold a row's columns 4 at a time): fp16 D32 (8 groups), fp16
+    # D128 (2), fp32 D256 (1) and fp32 D64 (4), each with one row hot enough
+    # to span far more than 64 tiles of 64 positions; the fp32 D64 table's
+    # row spans more than 4160 tiles, past the first coarse step of the
+    # search for the run's last tile.
+    monkeypatch.setenv("EB_BWD_TILE_CHUNKS", "1")
+    g = torch.Generator(device="cpu")
+    g.manual_seed(4)
+    B = 3000
+    specs = [("f16", 32, 400, 12), ("f16", 128, 400, 12), ("f32", 256, 400, 12), ("f32", 64, 500, 100)]
+    tables, lens_all, idx_all = [], [], []
+    for dtype, D, R, L in specs:
+        rows = torch.randn((R, D), generator=g)
+        tables.append(Table((rows * 0.1).half().to(dev) if dtype == "f16" else rows.to(dev), D, dtype))
+        lens = torch.randint(0, 2 * L + 1, (B,), generator=g)
+        n = int(lens.sum())
+        idx = torch.randint(0, R, (n,), generator=g)
+        idx[torch.rand(n, generator=g) < 0.95] = R // 3
+        lens_all.append(lens)
+        idx_all.append(idx)
+    lens = torch.cat(lens_all)
+    off = torch.zeros(lens.numel() + 1, dtype=torch.int64)
+    torch.cumsum(lens, 0, out=off[1:])
+    hot = int((idx_all[-1] == specs[-1][2] // 3).sum())
+    assert hot > 64 * 4160, hot
+    w = Workload("hot rows", tables, B, torch.cat(idx_all).to(dev), off.to(dev), None, "mean", lens.to(dev))
+    run_and_check(w, dev, "rowwise_adagrad", label="hot rows of every lane grouping")
+
+
 def test_mixed_storage_and_widths(dev):
     g = torch.Generator(device="cpu")
     g.manual_seed(2)
