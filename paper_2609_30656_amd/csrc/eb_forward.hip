@@ -346,9 +346,13 @@ __device__ __forceinline__ void pool_block_long_bags(const FwdArgs &a, const Blo
 // row.  Specialising keeps the register count (and so the occupancy) at what
 // that kind needs.  LONG is a specialisation of its own because the split
 // path's LDS and barriers slowed the common path by 7-10% on MI355X even when
-// no bag took it.
+// no bag took it.  The fp16 kernel that switches over every width (without
+// the split) is held to 8 waves per SIMD (64 VGPRs), which it meets without
+// spilling; the others would spill, so they keep the compiler's choice.
 template <int DT, int LOG2, bool W, bool LONG>
-__global__ __launch_bounds__(kBlock) void eb_pool_kernel(FwdArgs a) {
+__global__ __launch_bounds__(kBlock)
+__attribute__((amdgpu_waves_per_eu((LOG2 < 0 && DT == kF16 && !LONG) ? 8 : 1, 8)))
+void eb_pool_kernel(FwdArgs a) {
   const uint32_t blk = a.xcd_remap ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x;
   BlockBags bb;
   if constexpr (LONG) bb = block_bags(a, blk);
