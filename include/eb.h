@@ -261,8 +261,9 @@ typedef enum { EB_OPT_SGD = 0, EB_OPT_ROWWISE_ADAGRAD = 1 } eb_optimizer;
 
 /*
  * Device workspace (bytes) eb_backward_update needs for num_indices lookups
- * on this handle (about 17 bytes per lookup plus per-tile partial sums and
- * the sort's scratch).  Synchronous, host only.
+ * on this handle: 16 bytes per lookup, then per tile of 64 to 256 sorted
+ * lookups an 8-byte descriptor and two partial rows of the widest table
+ * (8 * max dim bytes), and the sort's scratch.  Synchronous, host only.
  */
 eb_status eb_backward_workspace_size(const eb_tables *tables, int64_t num_indices, size_t *bytes);
 
