@@ -183,31 +183,62 @@ struct GatherCtx {
   float one;
 };
 
-// One chunk of up to 64 consecutive index positions of a bag, one per lane.
+// One chunk of up to 64 consecutive index positions of a bag, one per lane,
+// as the gathers use it.
 struct Chunk {
   uint32_t row;  // row number, or kBadRow (no row / outside the table)
-  float w;       // per-sample weight (weighted pooling only)
+  float w;       // per-sample weight (weighted pooling only; 0 past the chunk)
   int n;         // positions in the chunk (wave-uniform)
 };
 
-// Positions [c, min(c + 64, hi)) of the index stream, one per lane, with
-// their weights.  Indices outside [0, num_rows) become kBadRow.  Indices and
-// weights are read once, so they are streamed past the caches.
+// The same chunk as read: each lane's index bits (hi only for 64-bit indices)
+// and weight, with the loads possibly still in flight.  resolve() makes the
+// Chunk where it is used, so a chunk loaded ahead stays in flight until then
+// (checking an index right after its load would make the wave wait for it
+// before the current chunk's rows are even requested).
+struct RawChunk {
+  uint32_t lo, hi;
+  float w;
+  int n;
+};
+
+// Positions [c, min(c + 64, end)) of the index stream, one per lane, with
+// their weights.  Lanes past the chunk re-read its first position, so no
+// branch surrounds the loads.  Indices and weights are read once, so they
+// are streamed past the caches.
 template <bool W>
-__device__ __forceinline__ Chunk load_chunk(int32_t num_rows, const void *indices, const float *weights, int idx64,
-                                            int64_t c, int64_t hi) {
+__device__ __forceinline__ RawChunk load_chunk(const void *indices, const float *weights, int idx64, int64_t c,
+                                               int64_t end) {
   const int lane = threadIdx.x & (kWave - 1);
-  Chunk k;
-  k.n = (int)((hi - c) < kWave ? (hi - c) : kWave);
-  k.row = kBadRow;
+  RawChunk k;
+  k.n = (int)((end - c) < kWave ? (end - c) : kWave);
+  k.lo = 0u;
+  k.hi = 0u;
   k.w = 0.0f;
-  if (lane < k.n) {
-    const int64_t r = idx64 ? __builtin_nontemporal_load(static_cast<const int64_t *>(indices) + c + lane)
-                            : (int64_t)__builtin_nontemporal_load(static_cast<const int32_t *>(indices) + c + lane);
-    if (r >= 0 && r < num_rows) k.row = (uint32_t)r;
-    if constexpr (W) k.w = __builtin_nontemporal_load(weights + c + lane);
+  if (k.n > 0) {
+    const int64_t p = c + (lane < k.n ? lane : 0);
+    if (idx64) {
+      const uint64_t v = __builtin_nontemporal_load(static_cast<const uint64_t *>(indices) + p);
+      k.lo = (uint32_t)v;
+      k.hi = (uint32_t)(v >> 32);
+    } else {
+      k.lo = __builtin_nontemporal_load(static_cast<const uint32_t *>(indices) + p);
+    }
+    if constexpr (W) k.w = __builtin_nontemporal_load(weights + p);
   }
   return k;
+}
+
+// The rows of a chunk of a table of num_rows rows: an index outside
+// [0, num_rows) and a lane past the chunk give kBadRow (and weight 0).
+__device__ __forceinline__ Chunk resolve(const RawChunk &k, int32_t num_rows, int idx64) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t r = idx64 ? (int64_t)(((uint64_t)k.hi << 32) | k.lo) : (int64_t)(int32_t)k.lo;
+  Chunk c;
+  c.n = k.n;
+  c.row = (lane < k.n && r >= 0 && r < num_rows) ? (uint32_t)r : kBadRow;
+  c.w = lane < k.n ? k.w : 0.0f;
+  return c;
 }
 
 // Store KEEP consecutive pooled values (16-, 8- or 4-byte non-temporal stores:

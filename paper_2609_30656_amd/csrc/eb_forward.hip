@@ -107,7 +107,7 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
   bool bskip;
   bag_range(0, blo, bhi, bskip);
   int64_t c = blo;
-  Chunk cur = load_chunk<W>(m.num_rows, a.indices, a.weights, a.idx64, c, bhi);
+  RawChunk cur = load_chunk<W>(a.indices, a.weights, a.idx64, c, bhi);
   while (true) {
     const bool last = c + kWave >= bhi;
     int jn = j;
@@ -121,10 +121,10 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
       }
     }
     const bool more = !last || jn < nb;
-    Chunk nxt;
-    if (more) nxt = load_chunk<W>(m.num_rows, a.indices, a.weights, a.idx64, cn, nhi);
+    RawChunk nxt;
+    if (more) nxt = load_chunk<W>(a.indices, a.weights, a.idx64, cn, nhi);
 
-    gather_chunk<DT, LPR, W, SPLIT>(m, a.ctx, cur, acc, cb, colb, colok);
+    gather_chunk<DT, LPR, W, SPLIT>(m, a.ctx, resolve(cur, m.num_rows, a.idx64), acc, cb, colb, colok);
 
     if (last) {
       if constexpr (SPLIT) {
@@ -175,13 +175,13 @@ __device__ __forceinline__ void pool_range(const TableMeta &m, const FwdArgs &a,
   for (int i = 0; i < V; ++i) acc[i] = 0.0f;
   if (lo < hi) {
     int64_t c = lo;
-    Chunk cur = load_chunk<W>(m.num_rows, a.indices, a.weights, a.idx64, c, hi);
+    RawChunk cur = load_chunk<W>(a.indices, a.weights, a.idx64, c, hi);
     while (true) {
       const int64_t cn = c + kWave;
       const bool more = cn < hi;
-      Chunk nxt;
-      if (more) nxt = load_chunk<W>(m.num_rows, a.indices, a.weights, a.idx64, cn, hi);
-      gather_chunk<DT, LPR, W, SPLIT>(m, a.ctx, cur, acc, cb, colb, colok);
+      RawChunk nxt;
+      if (more) nxt = load_chunk<W>(a.indices, a.weights, a.idx64, cn, hi);
+      gather_chunk<DT, LPR, W, SPLIT>(m, a.ctx, resolve(cur, m.num_rows, a.idx64), acc, cb, colb, colok);
       if (!more) break;
       c = cn;
       cur = nxt;

@@ -204,7 +204,7 @@ __device__ __forceinline__ void copy_chunk(const SeqArgs &a, const TableMeta &m,
 
 #define EB_SEQ_LPR(LOG2)                                  \
   case LOG2:                                              \
-    copy_chunk<DT, (1 << (LOG2))>(a, m, cur, rowbase);    \
+    copy_chunk<DT, (1 << (LOG2))>(a, m, ck, rowbase);     \
     break;
 
 // DT: the storage type this launch serves (chunks of other tables are
@@ -256,7 +256,7 @@ __global__ __launch_bounds__(kBlock) void eb_seq_kernel(SeqArgs a) {
   int64_t c = p0;
   int64_t hi = en < p1 ? en : p1;
   hi = (c + kWave) < hi ? (c + kWave) : hi;
-  Chunk cur = load_chunk<false>(m.num_rows, a.indices, nullptr, a.idx64, c, hi);
+  RawChunk cur = load_chunk<false>(a.indices, nullptr, a.idx64, c, hi);
   while (true) {
     // the next chunk: the rest of this table's part of the span, or the next
     // non-empty table's first positions
@@ -281,17 +281,18 @@ __global__ __launch_bounds__(kBlock) void eb_seq_kernel(SeqArgs a) {
       }
     }
     int64_t hin = 0;
-    Chunk nxt;
+    RawChunk nxt;
     if (more) {
       hin = enn < p1 ? enn : p1;
       hin = (cn + kWave) < hin ? (cn + kWave) : hin;
-      nxt = load_chunk<false>(a.meta[tn].num_rows, a.indices, nullptr, a.idx64, cn, hin);
+      nxt = load_chunk<false>(a.indices, nullptr, a.idx64, cn, hin);
     }
 
     if (m.kind / 8 == DT) {
       const int64_t rowbase = base + (c - st) * m.dim;
+      const Chunk ck = resolve(cur, m.num_rows, a.idx64);
       if constexpr (LOG2 >= 0) {
-        copy_chunk<DT, (1 << (LOG2 >= 0 ? LOG2 : 0))>(a, m, cur, rowbase);
+        copy_chunk<DT, (1 << (LOG2 >= 0 ? LOG2 : 0))>(a, m, ck, rowbase);
       } else {
         switch (m.kind % 8) {
           EB_SEQ_LPR(0) EB_SEQ_LPR(1) EB_SEQ_LPR(2) EB_SEQ_LPR(3) EB_SEQ_LPR(4) EB_SEQ_LPR(5) EB_SEQ_LPR(6)
