@@ -238,6 +238,41 @@ def test_full_size(dev, name):
     run_and_check(w, dev, "rowwise_adagrad", check_tables=sorted({0, T // 2, T - 1}), label=f"full {name}")
 
 
+def test_checked_mode_reports_bad_data(dev, monkeypatch):
+    # An index outside its table gets the table's sentinel key and updates
+    # nothing; offsets that are not a partition are clamped.  Checked mode
+    # reports both, and a valid call afterwards reports nothing (the error word
+    # is cleared).  The broken offsets here still cover every position.
+    monkeypatch.setenv("EB_CHECK", "1")
+    g = torch.Generator(device="cpu")
+    g.manual_seed(9)
+    rows = torch.randn((10, 16), generator=g).to(dev)
+    grad = torch.randn((3, 16), generator=g).to(dev)
+    ok_idx = torch.tensor([1, 2, 3, 4], device=dev)
+    off = torch.tensor([0, 2, 2, 4], device=dev)
+    with eb.eb_create_tables([Table(rows, 16, "f32")]) as h:
+        eb.eb_backward_update(h, ok_idx, off, None, "sum", grad, "sgd", 0.1)
+        for bad_idx in ([1, 10, 3, 4], [1, -1, 3, 4]):
+            with pytest.raises(eb.EBError) as e:
+                eb.eb_backward_update(h, torch.tensor(bad_idx, device=dev), off, None, "sum", grad, "sgd", 0.1)
+            assert e.value.status == eb.EB_ERR_INDEX_OOB
+        for bad_off in ([0, 3, 2, 4], [0, 2, 2, 9]):
+            with pytest.raises(eb.EBError) as e:
+                eb.eb_backward_update(h, ok_idx, torch.tensor(bad_off, device=dev), None, "sum", grad, "sgd", 0.1)
+            assert e.value.status == eb.EB_ERR_OFFSETS
+        before = rows.cpu().numpy().copy()
+        eb.eb_backward_update(h, ok_idx, off, None, "sum", grad, "sgd", 0.1)  # no error left over
+        torch.cuda.synchronize()
+    # that last step, against the oracle
+    tabs = [OracleTable(before, 16, "f32", 10)]
+    ebo_backward_update(tabs, np.array([1, 2, 3, 4]), np.array([0, 2, 2, 4]), None, "sum", grad.cpu().numpy(), "sgd",
+                        0.1, 0.0, None, report=[0])
+    got = rows.cpu().numpy()
+    np.testing.assert_allclose(got, tabs[0].rows, rtol=0, atol=1e-6)
+    untouched = [0, 5, 6, 7, 8, 9]  # rows no index reads keep their bits
+    assert np.array_equal(got[untouched].view(np.uint32), before[untouched].view(np.uint32))
+
+
 def test_backward_argument_errors(dev):
     g = torch.Generator(device="cpu")
     g.manual_seed(3)
