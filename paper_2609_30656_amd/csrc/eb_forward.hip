@@ -348,7 +348,8 @@ __device__ __forceinline__ void pool_block_long_bags(const FwdArgs &a, const Blo
 // path's LDS and barriers slowed the common path by 7-10% on MI355X even when
 // no bag took it.  The fp16 kernel that switches over every width (without
 // the split) is held to 8 waves per SIMD (64 VGPRs), which it meets without
-// spilling; the others would spill, so they keep the compiler's choice.
+// spilling; the int8 one and the split variants would spill, so they keep the
+// compiler's choice (the fp32 one needs 64 anyway).
 template <int DT, int LOG2, bool W, bool LONG>
 __global__ __launch_bounds__(kBlock)
 __attribute__((amdgpu_waves_per_eu((LOG2 < 0 && DT == kF16 && !LONG) ? 8 : 1, 8)))
