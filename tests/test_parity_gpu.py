@@ -375,6 +375,45 @@ def test_side_stream(dev):
 # argument errors through the ABI (host-side: nothing is enqueued)
 
 
+def test_threads_share_a_handle(dev):
+    # The handle is immutable after creation, so host threads may call the
+    # lookup on it at once (ctypes releases the GIL during the call).  Each
+    # thread writes its own output; every result equals a single-threaded call.
+    import threading
+
+    say("[parity] four host threads on one handle")
+    w = make_workload("c2", dev, **REDUCED["c2"])
+    ws = [w] + [make_workload("c2", dev, batch_seed=s, tables=w.tables, **REDUCED["c2"]) for s in (1, 2, 3)]
+    with eb.eb_create_tables(w.tables) as h:
+        ref = []
+        for x in ws:
+            o = torch.empty((x.batch, x.sum_dim), device=dev)
+            eb.eb_forward(h, x.indices, x.offsets, x.weights, x.pooling, o)
+            ref.append(o)
+        torch.cuda.synchronize()
+        outs = [[torch.full((x.batch, x.sum_dim), float("nan"), device=dev) for _ in range(20)] for x in ws]
+        errors = []
+
+        def work(i):
+            try:
+                x = ws[i]
+                for o in outs[i]:
+                    eb.eb_forward(h, x.indices, x.offsets, x.weights, x.pooling, o)
+            except Exception as e:  # reported below
+                errors.append(e)
+
+        threads = [threading.Thread(target=work, args=(i,)) for i in range(len(ws))]
+        for th in threads:
+            th.start()
+        for th in threads:
+            th.join()
+        torch.cuda.synchronize()
+    assert not errors, errors
+    for i in range(len(ws)):
+        for o in outs[i]:
+            assert torch.equal(o.view(torch.int32), ref[i].view(torch.int32))
+
+
 def test_forward_argument_errors(dev):
     say("[parity] argument errors")
     w = _custom(dev, [_table(dev, "f32", 10, 16), _table(dev, "f16", 10, 16)], [np.array([1, 2]), np.array([0, 3])])
