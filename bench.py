@@ -13,11 +13,14 @@ Prints one JSON line:
   value            algorithmic GB/s over the K timed steps (wall clock)
   lookups_per_s    pooled lookups per second over the same steps
   roofline         eb_pool_kernel's algorithmic bytes per launch / its mean
-                   launch time from HIP events on the library's stream,
-                   against 8 TB/s HBM3E; traffic from rocprofv3 counters;
-                   p10/median/p90 of the launch times; and `cold`: the same
-                   calls each preceded (outside the events) by a 1 GiB read
-                   that evicts L2 and the Infinity Cache
+                   launch time: the K timed steps between one pair of HIP
+                   events on the library's stream, divided by K; against
+                   8 TB/s HBM3E; traffic from rocprofv3 counters;
+                   p10/median/p90 of single launches (a second pass with an
+                   event pair around every 7th launch, which also times the
+                   events and the launch's dispatch); and `cold`: calls each
+                   preceded (outside their events) by a 1 GiB read that
+                   evicts L2 and the Infinity Cache
   cpu_baseline     the CPU oracle on a bounded sample of the same workload
 
 Algorithmic bytes per step = gathered row bytes (every lookup, duplicates
@@ -239,16 +242,33 @@ def main():
         step(k)
     torch.cuda.synchronize()
 
-    # Kernel durations come from HIP events on the library's stream around every
-    # SAMPLE-th launch of the timed loop (7 is coprime with the 3 rotating
-    # batches, so all three are sampled); events around every launch would add
-    # their own command-processor packets to each step of the timed loop.
+    # The timed loop: K back-to-back steps between one pair of HIP events on
+    # the library's stream (so the kernels' GPU time per step, with no event
+    # packets between them) and the host clock (`value`).
+    def timed_region(fn):
+        r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        r0.record(stream)
+        for k in range(args.steps):
+            fn(k)
+        r1.record(stream)
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0, r0.elapsed_time(r1) / 1e3
+
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    wall, region_s = timed_region(step)
+    kern_avg_s = region_s / args.steps
+    kern_bytes = sum(algo[k % 3] for k in range(args.steps)) / args.steps
+
+    # Then the spread of single launches: a second pass with an event pair
+    # around every SAMPLE-th step (7 is coprime with the 3 rotating batches,
+    # so all three are sampled).  Each such pair also times its own event
+    # packets and the launch's dispatch, so these read a little longer than
+    # the steady-state average above.
     sample = [k for k in range(args.steps) if k % SAMPLE == 0]
     starts = {k: torch.cuda.Event(enable_timing=True) for k in sample}
     ends = {k: torch.cuda.Event(enable_timing=True) for k in sample}
-    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
     for k in range(args.steps):
         if k in starts:
             starts[k].record(stream)
@@ -257,10 +277,7 @@ def main():
         else:
             step(k)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     kern_ms = [starts[k].elapsed_time(ends[k]) for k in sample]
-    kern_avg_s = sum(kern_ms) / len(kern_ms) / 1e3
-    kern_bytes = sum(algo[k % 3] for k in sample) / len(sample)
 
     def quantiles(xs):
         xs = sorted(xs)
@@ -304,15 +321,10 @@ def main():
     if args.mode == "fm":
         # the plain lookup on the same batches, timed the same way: the step's
         # extra time is the FM pass over the pooled output
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in sample]
         for k in range(args.warmup):
             forward_step(k)
-        for (a, b), k in zip(ev, sample):
-            a.record(stream)
-            forward_step(k)
-            b.record(stream)
-        torch.cuda.synchronize()
-        fwd_ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+        _, fwd_region_s = timed_region(forward_step)
+        fwd_ms = fwd_region_s / args.steps * 1e3
         pass_bytes = w0.batch * w0.sum_dim * 4 + w0.batch * 4
         pass_ms = kern_avg_s * 1e3 - fwd_ms
         fm_pass = {
@@ -393,11 +405,12 @@ def main():
             "frac": round(achieved / PEAK_HBM_GBS, 4),
             "traffic": None if traffic is None else round(traffic),
             "kernel_ms_avg": round(kern_avg_s * 1e3, 5),
+            "timed_launches": args.steps,
             "kernel_ms_p10": round(w10, 5),
             "kernel_ms_median": round(w50, 5),
             "kernel_ms_p90": round(w90, 5),
+            "sampled_launches": len(sample),
             "cold": cold,
-            "timed_launches": len(sample),
         },
         "cpu_baseline": cpu,
     }
