@@ -404,6 +404,11 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4),
             "traffic": None if traffic is None else round(traffic),
+            # the counter traffic per launch over the mean launch time: the
+            # fabric's actual rate, which Zipf reuse in L2 keeps below the
+            # algorithmic one
+            "traffic_gbs": None if traffic is None else round(traffic / kern_avg_s / 1e9, 1),
+            "traffic_frac": None if traffic is None else round(traffic / kern_avg_s / 1e9 / PEAK_HBM_GBS, 4),
             "kernel_ms_avg": round(kern_avg_s * 1e3, 5),
             "timed_launches": args.steps,
             "kernel_ms_p10": round(w10, 5),
