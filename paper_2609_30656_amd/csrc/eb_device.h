@@ -297,10 +297,26 @@ __device__ __forceinline__ void gather_steps(const TableMeta &m, const GatherCtx
   for (int u = 0; u < N; ++u) accumulate<DT, W, SPLIT>(acc, cb, v[u], sb[u], w[u], a.one);
 }
 
-// Gather all rows of one chunk: full batches of U steps, then one batch of
-// the smallest power-of-two size that covers the remaining steps (its
-// missing steps read the zero row), so a chunk of up to U steps costs one
-// memory round trip.
+// One straight-line batch of exactly `rem` steps (1 <= rem <= N).
+template <int DT, int LPR, bool W, bool SPLIT, int N>
+__device__ __forceinline__ void gather_exact(int rem, const TableMeta &m, const GatherCtx &a, const Chunk &k, int s,
+                                             float (&acc)[Vals<DT>::n], float &cb, int colb, bool colok) {
+  if constexpr (N > 0) {
+    if (rem == N) {
+      gather_steps<DT, LPR, W, SPLIT, N>(m, a, k, s, acc, cb, colb, colok);
+      return;
+    }
+    gather_exact<DT, LPR, W, SPLIT, N - 1>(rem, m, a, k, s, acc, cb, colb, colok);
+  }
+}
+
+// Gather all rows of one chunk: full batches of U steps, then one batch for
+// the rest, so a chunk of up to U steps costs one memory round trip.  With
+// batches of 8 the last one has exactly the remaining steps: padding it to a
+// power of two spent up to 3 of every 8 loads on the zero row (a 20-row bag
+// of 4 rows per load takes 5 steps), which cost c2 7%.  With batches of 4 it
+// is padded to 2 or 4 steps (at most one padded load): exact sizes there were
+// no faster and took more registers.
 template <int DT, int LPR, bool W, bool SPLIT>
 __device__ __forceinline__ void gather_chunk(const TableMeta &m, const GatherCtx &a, const Chunk &k,
                                              float (&acc)[Vals<DT>::n], float &cb, int colb, bool colok) {
@@ -312,21 +328,20 @@ __device__ __forceinline__ void gather_chunk(const TableMeta &m, const GatherCtx
   }
   const int steps = (k.n + RPL - 1) / RPL;
   int s = 0;
-  for (; steps - s > U / 2; s += U) gather_steps<DT, LPR, W, SPLIT, U>(m, a, k, s, acc, cb, colb, colok);
-  const int rem = steps - s;  // 0 .. U/2
   if constexpr (U >= 8) {
-    if (rem > 2) {
-      gather_steps<DT, LPR, W, SPLIT, 4>(m, a, k, s, acc, cb, colb, colok);
-      return;
+    for (; steps - s >= U; s += U) gather_steps<DT, LPR, W, SPLIT, U>(m, a, k, s, acc, cb, colb, colok);
+    if (steps > s) gather_exact<DT, LPR, W, SPLIT, U - 1>(steps - s, m, a, k, s, acc, cb, colb, colok);
+  } else {
+    for (; steps - s > U / 2; s += U) gather_steps<DT, LPR, W, SPLIT, U>(m, a, k, s, acc, cb, colb, colok);
+    const int rem = steps - s;  // 0 .. U/2
+    if constexpr (U >= 4) {
+      if (rem > 1) {
+        gather_steps<DT, LPR, W, SPLIT, 2>(m, a, k, s, acc, cb, colb, colok);
+        return;
+      }
     }
+    if (rem > 0) gather_steps<DT, LPR, W, SPLIT, 1>(m, a, k, s, acc, cb, colb, colok);
   }
-  if constexpr (U >= 4) {
-    if (rem > 1) {
-      gather_steps<DT, LPR, W, SPLIT, 2>(m, a, k, s, acc, cb, colb, colok);
-      return;
-    }
-  }
-  if (rem > 0) gather_steps<DT, LPR, W, SPLIT, 1>(m, a, k, s, acc, cb, colb, colok);
 }
 
 // Gather entries [base, base + n) of a chunk (n <= 64 - base) and accumulate
