@@ -496,7 +496,8 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
       const int z = heads ? (int)__builtin_ctzll(heads) : n;
       const uint32_t rkey = __builtin_amdgcn_readlane(key, 0);
       if (!pending) start_run(rkey);
-      gather_range<kF32, LPR, true>(gm, a.ctx, ch, 0, z, acc, colb, colok);
+      if (a.coef == 0) gather_range<kF32, LPR, false>(gm, a.ctx, ch, 0, z, acc, colb, colok);
+      else gather_range<kF32, LPR, true>(gm, a.ctx, ch, 0, z, acc, colb, colok);
       if (z < n || last_chunk) {
         finish(rkey, z == n);
         pending = false;
@@ -518,7 +519,8 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
       const int hl = 63 - __builtin_clzll(hs);
       const uint32_t rkey = __builtin_amdgcn_readlane(key, hl);
       start_run(rkey);
-      gather_range<kF32, LPR, true>(gm, a.ctx, ch, hl, n - hl, acc, colb, colok);
+      if (a.coef == 0) gather_range<kF32, LPR, false>(gm, a.ctx, ch, hl, n - hl, acc, colb, colok);
+      else gather_range<kF32, LPR, true>(gm, a.ctx, ch, hl, n - hl, acc, colb, colok);
       if (last_chunk) {
         finish(rkey, true);
         pending = false;

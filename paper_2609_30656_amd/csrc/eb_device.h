@@ -344,6 +344,20 @@ __device__ __forceinline__ void gather_chunk(const TableMeta &m, const GatherCtx
   }
 }
 
+// One straight-line batch of exactly `rem` steps of entries from `base` on.
+template <int DT, int LPR, bool W, int N>
+__device__ __forceinline__ void gather_exact_at(int rem, const TableMeta &m, const GatherCtx &a, const Chunk &k, int s,
+                                                float (&acc)[Vals<DT>::n], float &cb, int colb, bool colok,
+                                                int base) {
+  if constexpr (N > 0) {
+    if (rem == N) {
+      gather_steps<DT, LPR, W, false, N>(m, a, k, s, acc, cb, colb, colok, base);
+      return;
+    }
+    gather_exact_at<DT, LPR, W, N - 1>(rem, m, a, k, s, acc, cb, colb, colok, base);
+  }
+}
+
 // Gather entries [base, base + n) of a chunk (n <= 64 - base) and accumulate
 // them: the same batching as gather_chunk, for a run that covers only part
 // of the chunk.
@@ -356,6 +370,11 @@ __device__ __forceinline__ void gather_range(const TableMeta &m, const GatherCtx
   k.n = n;
   const int steps = (n + RPL - 1) / RPL;
   int s = 0;
+  if constexpr (U >= 8) {
+    for (; steps - s >= U; s += U) gather_steps<DT, LPR, W, false, U>(m, a, k, s, acc, cb, colb, colok, base);
+    if (steps > s) gather_exact_at<DT, LPR, W, U - 1>(steps - s, m, a, k, s, acc, cb, colb, colok, base);
+    return;
+  }
   for (; steps - s > U / 2; s += U) gather_steps<DT, LPR, W, false, U>(m, a, k, s, acc, cb, colb, colok, base);
   const int rem = steps - s;
   if constexpr (U >= 8) {
