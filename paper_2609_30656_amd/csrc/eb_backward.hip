@@ -216,6 +216,81 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// Table rows, the optimizer state and the carry slots are plain device
+// memory, addressed in the global address space so that their accesses compile
+// to global instructions.  A flat access also counts as an LDS access: the wait
+// before the next cross-lane shuffle would wait for it too, and a row read
+// ahead of a gradient gather would no longer overlap the gather.
+typedef EB_GLOBAL unsigned char growb;
+typedef EB_GLOBAL float gf32;
+typedef EB_GLOBAL _Float16 gf16;
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ growb *row_bytes(const TableMeta &m, int64_t row) {
+  return (growb *)m.data + (uint64_t)row * m.row_stride;
+}
+
+__device__ __forceinline__ gf32 *state_of(const BwdArgs &a, const TableMeta &m, int64_t row) {
+  return (gf32 *)a.state + m.state_base + row;
+}
+
+// K = 1, 2 or 4 consecutive values of a row of type TDT from column col (a
+// multiple of K, so the access is aligned to its size), in one access.
+template <int TDT, int K>
+__device__ __forceinline__ void load_vals(growb *base, int col, float (&w)[K]) {
+  static_assert(K == 1 || K == 2 || K == 4, "one access holds 1, 2 or 4 values");
+  if constexpr (TDT == kF32) {
+    gf32 *p = (gf32 *)base + col;
+    if constexpr (K == 4) {
+      const f32x4 v = *(EB_GLOBAL f32x4 *)p;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = v[i];
+    } else if constexpr (K == 2) {
+      const f32x2 v = *(EB_GLOBAL f32x2 *)p;
+      w[0] = v[0];
+      w[1] = v[1];
+    } else {
+      w[0] = *p;
+    }
+  } else {
+    gf16 *p = (gf16 *)base + col;
+    if constexpr (K == 4) {
+      const f16x4 v = *(EB_GLOBAL f16x4 *)p;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = (float)v[i];
+    } else if constexpr (K == 2) {
+      const f16x2 v = *(EB_GLOBAL f16x2 *)p;
+      w[0] = (float)v[0];
+      w[1] = (float)v[1];
+    } else {
+      w[0] = (float)*p;
+    }
+  }
+}
+
+// The store matching load_vals (fp16 rows round to nearest).
+template <int TDT, int K>
+__device__ __forceinline__ void store_vals(growb *base, int col, const float (&w)[K]) {
+  static_assert(K == 1 || K == 2 || K == 4, "one access holds 1, 2 or 4 values");
+  if constexpr (TDT == kF32) {
+    gf32 *p = (gf32 *)base + col;
+    if constexpr (K == 4) *(EB_GLOBAL f32x4 *)p = f32x4{w[0], w[1], w[2], w[3]};
+    else if constexpr (K == 2) *(EB_GLOBAL f32x2 *)p = f32x2{w[0], w[1]};
+    else *p = w[0];
+  } else {
+    gf16 *p = (gf16 *)base + col;
+    if constexpr (K == 4) {
+      *(EB_GLOBAL f16x4 *)p = f16x4{(_Float16)w[0], (_Float16)w[1], (_Float16)w[2], (_Float16)w[3]};
+    } else if constexpr (K == 2) {
+      *(EB_GLOBAL f16x2 *)p = f16x2{(_Float16)w[0], (_Float16)w[1]};
+    } else {
+      *p = (_Float16)w[0];
+    }
+  }
+}
+
 // The values a row update reads, loaded ahead of the gather that produces
 // the row's gradient: the lane's K table values and the Adagrad state.
 template <int TDT, int K>
@@ -228,21 +303,10 @@ template <int TDT, int K>
 __device__ __forceinline__ RowPrefetch<TDT, K> prefetch_row(const TableMeta &m, const BwdArgs &a, int64_t row, bool own,
                                                            int col) {
   RowPrefetch<TDT, K> p;
-  p.s = a.opt == kOptRowwiseAdagrad ? a.state[m.state_base + row] : 0.0f;
+  p.s = a.opt == kOptRowwiseAdagrad ? *state_of(a, m, row) : 0.0f;
 #pragma unroll
   for (int i = 0; i < K; ++i) p.w[i] = 0.0f;
-  if (own) {
-    const unsigned char *base = m.data + (uint64_t)row * m.row_stride;
-    if constexpr (TDT == kF32) {
-      const float *wp = reinterpret_cast<const float *>(base) + col;
-#pragma unroll
-      for (int i = 0; i < K; ++i) p.w[i] = wp[i];
-    } else {
-      const _Float16 *wp = reinterpret_cast<const _Float16 *>(base) + col;
-#pragma unroll
-      for (int i = 0; i < K; ++i) p.w[i] = (float)wp[i];
-    }
-  }
+  if (own) load_vals<TDT, K>(row_bytes(m, row), col, p.w);
   return p;
 }
 
@@ -262,19 +326,13 @@ __device__ __forceinline__ void apply_update(const TableMeta &m, const BwdArgs &
     sq = wave_sum(sq);
     const float s_new = p.s + sq / (float)m.dim;
     scale = a.lr / (sqrtf(s_new) + a.eps);
-    if ((threadIdx.x & (kWave - 1)) == 0) a.state[m.state_base + row] = s_new;
+    if ((threadIdx.x & (kWave - 1)) == 0) *state_of(a, m, row) = s_new;
   }
   if (own) {
-    unsigned char *base = const_cast<unsigned char *>(m.data) + (uint64_t)row * m.row_stride;
-    if constexpr (TDT == kF32) {
-      float *wp = reinterpret_cast<float *>(base) + col;
+    float nw[K];
 #pragma unroll
-      for (int i = 0; i < K; ++i) wp[i] = fmaf(-scale, g[i], p.w[i]);
-    } else {
-      _Float16 *wp = reinterpret_cast<_Float16 *>(base) + col;
-#pragma unroll
-      for (int i = 0; i < K; ++i) wp[i] = (_Float16)fmaf(-scale, g[i], p.w[i]);
-    }
+    for (int i = 0; i < K; ++i) nw[i] = fmaf(-scale, g[i], p.w[i]);
+    store_vals<TDT, K>(row_bytes(m, row), col, nw);
   }
 }
 
@@ -317,13 +375,16 @@ __device__ __forceinline__ void short_runs(const BwdArgs &a, const TableMeta &m,
     for (int i = 0; i < NV; ++i) wv[i] = 0.0f;
     const int col0 = colb0 / 4;
     if (valid) {
-      if (a.opt == kOptRowwiseAdagrad) s_old = a.state[m.state_base + row];
-      const unsigned char *base = m.data + (uint64_t)row * m.row_stride;
+      if (a.opt == kOptRowwiseAdagrad) s_old = *state_of(a, m, row);
+      growb *base = row_bytes(m, row);
 #pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        if (col0 + i < m.dim) {
-          if constexpr (TDT == kF32) wv[i] = reinterpret_cast<const float *>(base)[col0 + i];
-          else wv[i] = (float)reinterpret_cast<const _Float16 *>(base)[col0 + i];
+      for (int pp = 0; pp < P; ++pp) {
+        // dim is a multiple of 4: four columns are all in the row or all past it
+        if (col0 + 4 * pp < m.dim) {
+          float t4[4];
+          load_vals<TDT, 4>(base, col0 + 4 * pp, t4);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) wv[4 * pp + i] = t4[i];
         }
       }
     }
@@ -364,16 +425,17 @@ __device__ __forceinline__ void short_runs(const BwdArgs &a, const TableMeta &m,
       for (int o = 1; o < LPRS; o <<= 1) sq += __shfl_xor(sq, o);
       const float s_new = s_old + sq / (float)m.dim;
       scale = a.lr / (sqrtf(s_new) + a.eps);
-      if (valid && sub == 0) a.state[m.state_base + row] = s_new;
+      if (valid && sub == 0) *state_of(a, m, row) = s_new;
     }
     if (valid) {
-      unsigned char *base = const_cast<unsigned char *>(m.data) + (uint64_t)row * m.row_stride;
+      growb *base = row_bytes(m, row);
 #pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        if (col0 + i < m.dim) {
-          const float nw = fmaf(-scale, acc[i], wv[i]);
-          if constexpr (TDT == kF32) reinterpret_cast<float *>(base)[col0 + i] = nw;
-          else reinterpret_cast<_Float16 *>(base)[col0 + i] = (_Float16)nw;
+      for (int pp = 0; pp < P; ++pp) {
+        if (col0 + 4 * pp < m.dim) {
+          float t4[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) t4[i] = fmaf(-scale, acc[4 * pp + i], wv[4 * pp + i]);
+          store_vals<TDT, 4>(base, col0 + 4 * pp, t4);
         }
       }
     }
@@ -441,9 +503,8 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
       if (!started_before && !continues_after) {
         apply_update<TDT, KEEP>(m, a, (int64_t)(rkey - kmin), gk, own, col, pre);
       } else if (own) {
-        float *slot = a.carry + ((int64_t)2 * w + (started_before ? 0 : 1)) * a.max_dim + col;
-#pragma unroll
-        for (int i = 0; i < KEEP; ++i) slot[i] = gk[i];
+        gf32 *slot = (gf32 *)a.carry + ((int64_t)2 * w + (started_before ? 0 : 1)) * a.max_dim;
+        store_vals<kF32, KEEP>((growb *)slot, col, gk);
       }
     }
     first_run = false;
@@ -598,14 +659,14 @@ __global__ __launch_bounds__(kBlock) void eb_bwd_fixup_kernel(BwdArgs a) {
   const bool own = cols && gi == 0;
   constexpr int kBatch = 8;
   auto head = [&](int32_t tile) {  // partial of the run that enters `tile`
-    return *reinterpret_cast<const f32x4 *>(a.carry + ((int64_t)2 * tile) * a.max_dim + col);
+    return *(EB_GLOBAL const f32x4 *)((gf32 *)a.carry + ((int64_t)2 * tile) * a.max_dim + col);
   };
   // Issued before the run's end is known: the row and its state, this
   // tile's partial and that of tile w + 1, which is always in the run.
   const RowPrefetch<TDT, 4> pre = prefetch_row<TDT, 4>(m, a, (int64_t)(key - m.key_base), own, col);
   f32x4 tail = {0.0f, 0.0f, 0.0f, 0.0f}, next = {0.0f, 0.0f, 0.0f, 0.0f};
   if (own) {
-    tail = *reinterpret_cast<const f32x4 *>(a.carry + ((int64_t)2 * w + 1) * a.max_dim + col);
+    tail = *(EB_GLOBAL const f32x4 *)((gf32 *)a.carry + ((int64_t)2 * w + 1) * a.max_dim + col);
     next = head(w + 1);
   }
   // The run's last tile kend: every tile of the run but its last goes on
