@@ -342,10 +342,13 @@ __device__ __forceinline__ void apply_update(const TableMeta &m, const BwdArgs &
 // group walks its run's entries in order (P 16-byte loads per lane per
 // gradient row), then applies the optimizer step to the run's row itself:
 // no cross-group reduction, and one memory round trip per round of G runs.
+// A gradient row of 16 or more 16-byte slices is held by half as many lanes,
+// two slices each: twice the runs per round, for the same registers that the
+// widest row already takes.
 template <int TDT, int LPR_NAT>
 __device__ __forceinline__ void short_runs(const BwdArgs &a, const TableMeta &m, const TableMeta &gm, const Chunk &ch,
                                            uint32_t key, uint64_t hs, int nruns, int *starts) {
-  constexpr int LPRS = LPR_NAT < 32 ? LPR_NAT : 32;
+  constexpr int LPRS = LPR_NAT >= 16 ? LPR_NAT / 2 : LPR_NAT;
   constexpr int P = LPR_NAT / LPRS;
   constexpr int G = kWave / LPRS;
   constexpr int US = P >= 2 ? 2 : 4;
