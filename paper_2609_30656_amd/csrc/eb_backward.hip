@@ -40,14 +40,16 @@
 namespace eb {
 namespace {
 
-// The (key, value) sort: onesweep passes of 8 bits with 1024-thread blocks of
+// The (key, value) sort: onesweep passes of 9 bits with 1024-thread blocks of
 // 8 items each.  rocPRIM's own choice for 32-bit pairs on this GPU takes 16
 // items per thread, so a 1 M-pair sort runs as only 65 blocks per pass; with 8
 // the backward step was 12% faster on 1 M lookups, 4% on 15 M and the same on
-// 3 M (smaller blocks or fewer items were slower on the larger inputs).
+// 3 M (smaller blocks or fewer items were slower on the larger inputs).  Keys
+// of up to 27 bits (tens of millions of rows) take three 9-bit passes instead
+// of four 8-bit ones: 7-10% off the step there; 10-bit digits were slower.
 using SortConfig = rocprim::radix_sort_config<
     rocprim::default_config, rocprim::default_config,
-    rocprim::radix_sort_onesweep_config<rocprim::kernel_config<1024, 8>, rocprim::kernel_config<1024, 8>, 8,
+    rocprim::radix_sort_onesweep_config<rocprim::kernel_config<1024, 8>, rocprim::kernel_config<1024, 8>, 9,
                                         rocprim::block_radix_rank_algorithm::match>>;
 
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;  // larger than any key (keys fit below it)
@@ -602,19 +604,26 @@ __device__ __forceinline__ void tile_body(const BwdArgs &a, const TableMeta &m, 
     tile_body<TDT, (1 << (LOG2))>(a, m, t, w, w - a.tile_start[t], starts);     \
     break;
 
+// Wavefronts per tiles-kernel workgroup.  A tile's time varies several-fold
+// with its runs (a chunk of single-occurrence rows takes many rounds, a piece
+// of a hot row's run one gather); one-wavefront workgroups let a finished
+// wavefront's slot take the next tile at once, where a four-wavefront
+// workgroup waits for a free slot on every SIMD (measured 3-5% faster).
+constexpr int kTileWaves = 1;
+
 // Tiles are numbered table by table; with XCD-contiguous workgroup order each
 // XCD walks one eighth of the tables, so its L2 keeps those tables' gradient
 // rows (B x D fp32 per table, re-read by every run of the table) instead of
 // all eight XCDs pulling the same table's gradient through the fabric.
 template <int TDT, int LOG2>
-__global__ __launch_bounds__(kBlock) void eb_bwd_tiles_kernel(BwdArgs a) {
+__global__ __launch_bounds__(kWave * kTileWaves) void eb_bwd_tiles_kernel(BwdArgs a) {
   const uint32_t blk = a.xcd_remap ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x;
-  const int32_t w = (int32_t)blk * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int32_t w = (int32_t)blk * kTileWaves + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if (w >= a.tile_start[a.num_tables]) return;
   const int32_t t = table_of_tile(a, w);
   const TableMeta m = a.meta[t];
   if (m.kind / 8 != TDT) return;
-  __shared__ int run_starts[kWavesPerBlock][kWave + 1];
+  __shared__ int run_starts[kTileWaves][kWave + 1];
   int *starts = run_starts[threadIdx.x / kWave];
   if constexpr (LOG2 >= 0) {
     tile_body<TDT, (1 << LOG2)>(a, m, t, w, w - a.tile_start[t], starts);
@@ -946,21 +955,23 @@ eb_status eb_backward_update(const eb_tables *h, eb_tensor indices, eb_tensor of
     hipLaunchKernelGGL(eb_bwd_tile_start_kernel, dim3(1), dim3(1024), 0, h->stream, a);
     e = hipGetLastError();
   }
-  const unsigned tgrid = (unsigned)((L.tiles_ub + kWavesPerBlock - 1) / kWavesPerBlock);
+  const unsigned tgrid = (unsigned)((L.tiles_ub + kTileWaves - 1) / kTileWaves);
+  const unsigned fgrid = (unsigned)((L.tiles_ub + kWavesPerBlock - 1) / kWavesPerBlock);
   // one launch per storage type present; fixed row width when all tables share it
   int32_t glog2 = log2_lanes_per_row(4 * h->h_meta[0].dim);
   for (int32_t t = 1; t < h->num_tables; ++t)
     if (log2_lanes_per_row(4 * h->h_meta[t].dim) != glog2) glog2 = -1;
   for (int dt = 0; dt < 2 && e == hipSuccess; ++dt) {
     if (!(h->dtype_mask & (1 << dt))) continue;
-    hipLaunchKernelGGL(dt == kF32 ? pick_tiles<kF32>(glog2) : pick_tiles<kF16>(glog2), dim3(tgrid), dim3(kBlock), 0,
+    hipLaunchKernelGGL(dt == kF32 ? pick_tiles<kF32>(glog2) : pick_tiles<kF16>(glog2), dim3(tgrid),
+                       dim3(kWave * kTileWaves), 0,
                        h->stream, a);
     e = hipGetLastError();
   }
   // 4. runs that cross tiles
   for (int dt = 0; dt < 2 && e == hipSuccess; ++dt) {
     if (!(h->dtype_mask & (1 << dt))) continue;
-    hipLaunchKernelGGL(dt == kF32 ? eb_bwd_fixup_kernel<kF32> : eb_bwd_fixup_kernel<kF16>, dim3(tgrid), dim3(kBlock),
+    hipLaunchKernelGGL(dt == kF32 ? eb_bwd_fixup_kernel<kF32> : eb_bwd_fixup_kernel<kF16>, dim3(fgrid), dim3(kBlock),
                        0, h->stream, a);
     e = hipGetLastError();
   }
