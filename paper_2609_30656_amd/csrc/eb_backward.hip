@@ -99,6 +99,43 @@ __device__ __forceinline__ int64_t clamp_pos(int64_t p, int64_t lo, int64_t hi) 
   return p < lo ? lo : (p > hi ? hi : p);
 }
 
+// Keys and bag ids of positions [P0, P1) (bags g0 .. g0 + nb - 1, whose
+// offsets lane j holds in my_off).  kKeyChunks chunks of 64 positions per
+// round: every index load of a round is issued before its first key is
+// stored, and none sits behind a branch (a position past P1 re-reads P1 - 1),
+// so a round costs one memory round trip.  Returns whether this lane saw an
+// index outside the table.
+template <typename IT>
+__device__ __forceinline__ bool key_positions(const BwdArgs &a, const TableMeta &m, int64_t P0, int64_t P1,
+                                              int64_t my_off, int nb, int32_t g0) {
+  constexpr int kKeyChunks = 4;
+  const int lane = threadIdx.x & (kWave - 1);
+  const IT *idx = static_cast<const IT *>(a.indices);
+  bool oob = false;
+  for (int64_t c = P0; c < P1; c += kKeyChunks * kWave) {
+    int64_t r[kKeyChunks];
+#pragma unroll
+    for (int u = 0; u < kKeyChunks; ++u) {
+      const int64_t p = c + u * kWave + lane;
+      r[u] = (int64_t)__builtin_nontemporal_load(idx + (p < P1 ? p : P1 - 1));
+    }
+#pragma unroll
+    for (int u = 0; u < kKeyChunks; ++u) {
+      const int64_t p = c + u * kWave + lane;
+      if (p < P1) {
+        int j = 0;
+        for (int jj = 1; jj < nb; ++jj)
+          if (readlane64(my_off, jj) <= p) j = jj;
+        const bool ok = r[u] >= 0 && r[u] < m.num_rows;
+        oob |= !ok;
+        a.keys[p] = m.key_base + (ok ? (uint32_t)r[u] : (uint32_t)m.num_rows);
+        a.bag_of[p] = g0 + j;
+      }
+    }
+  }
+  return oob;
+}
+
 // Step 1: sort key and bag id of every position.  A wavefront takes a run of
 // consecutive bags of one table and walks their positions 64 at a time (the
 // same work map as the forward).  An index outside its table gets the table's
@@ -128,21 +165,8 @@ __global__ __launch_bounds__(kBlock) void eb_bwd_keys_kernel(BwdArgs a) {
   const int64_t my_off = clamp_pos(raw, 0, N);
   const int64_t P0 = readlane64(my_off, 0);
   const int64_t P1 = readlane64(my_off, nb);
-  bool oob = false;
-  for (int64_t c = P0; c < P1; c += kWave) {
-    const int64_t p = c + lane;
-    if (p < P1) {
-      int j = 0;
-      for (int jj = 1; jj < nb; ++jj)
-        if (readlane64(my_off, jj) <= p) j = jj;
-      const int64_t r = a.idx64 ? __builtin_nontemporal_load(static_cast<const int64_t *>(a.indices) + p)
-                                : (int64_t)__builtin_nontemporal_load(static_cast<const int32_t *>(a.indices) + p);
-      const bool ok = r >= 0 && r < m.num_rows;
-      oob |= !ok;
-      a.keys[p] = m.key_base + (ok ? (uint32_t)r : (uint32_t)m.num_rows);
-      a.bag_of[p] = g0 + j;
-    }
-  }
+  const bool oob = a.idx64 ? key_positions<int64_t>(a, m, P0, P1, my_off, nb, g0)
+                           : key_positions<int32_t>(a, m, P0, P1, my_off, nb, g0);
   if (__ballot(oob)) {
     if (lane == 0) atomicOr(a.ctx.err, kErrIndex);
   }
