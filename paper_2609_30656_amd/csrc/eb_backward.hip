@@ -14,11 +14,11 @@
 //
 // Computed without atomics on data, and deterministically:
 //   1. every position gets a 32-bit sort key (the table's key base + row) and
-//      its bag id;
+//      its bag id, and each table's first tile is found from the offsets;
 //   2. (key, position) pairs are radix-sorted (rocPRIM): each row's
 //      occurrences become one run, in position order, and each table's
 //      positions stay inside that table's range of the sorted array;
-//   3. each table's sorted range is cut into tiles of 64..256 positions; a
+//   3. each table's sorted range is cut into tiles of 64 or 128 positions; a
 //      wavefront walks its tile's runs, pools each run's gradient rows with the
 //      forward's 16-byte-slice gather and reduce-scatter (the gradient is an
 //      fp32 "table" of B rows), and updates the run's table row; a run that
@@ -99,6 +99,61 @@ __device__ __forceinline__ int64_t clamp_pos(int64_t p, int64_t lo, int64_t hi) 
   return p < lo ? lo : (p > hi ? hi : p);
 }
 
+// tiles of table t (its clamped position range cut into tile_size pieces)
+__device__ __forceinline__ void table_range(const BwdArgs &a, int32_t t, int64_t &p0, int64_t &p1) {
+  p0 = clamp_pos(load_offset(a, (int64_t)t * a.batch), 0, a.num_indices);
+  p1 = clamp_pos(load_offset(a, (int64_t)(t + 1) * a.batch), p0, a.num_indices);
+}
+
+// Step 3a: first tile of every table, an exclusive scan of the tables' tile
+// counts by one workgroup of NT threads (part: 2 * NT / 64 slots of LDS).
+// Tile counts depend on the offsets alone, so the keys kernel's last
+// workgroup runs this before its own positions.
+template <int NT>
+__device__ __forceinline__ void scan_tile_starts(const BwdArgs &a, int64_t *part) {
+  constexpr int kWaves = NT / kWave;
+  const int T = a.num_tables;
+  const int tid = threadIdx.x;
+  const int per = (T + NT - 1) / NT;
+  const int t0 = tid * per < T ? tid * per : T;
+  const int t1 = t0 + per < T ? t0 + per : T;
+  int64_t sum = 0;
+  for (int t = t0; t < t1; ++t) {
+    int64_t p0, p1;
+    table_range(a, t, p0, p1);
+    sum += (p1 - p0 + a.tile_size - 1) / a.tile_size;
+  }
+  // exclusive scan of the per-thread sums: within each wavefront, then over
+  // the wavefronts' totals
+  const int lane = tid & (kWave - 1), wave = tid / kWave;
+  int64_t incl = sum;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int64_t v = __shfl_up(incl, o);
+    if (lane >= o) incl += v;
+  }
+  if (lane == kWave - 1) part[wave] = incl;
+  __syncthreads();
+  if (wave == 0) {
+    int64_t w = lane < kWaves ? part[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < kWaves; o <<= 1) {
+      const int64_t v = __shfl_up(w, o);
+      if (lane >= o) w += v;
+    }
+    if (lane < kWaves) part[kWaves + lane] = w;  // inclusive totals of waves 0..lane
+  }
+  __syncthreads();
+  int64_t run = incl - sum + (wave > 0 ? part[kWaves + wave - 1] : 0);
+  if (tid == NT - 1) a.tile_start[T] = (int32_t)(run + sum);
+  for (int t = t0; t < t1; ++t) {
+    a.tile_start[t] = (int32_t)run;
+    int64_t p0, p1;
+    table_range(a, t, p0, p1);
+    run += (p1 - p0 + a.tile_size - 1) / a.tile_size;
+  }
+}
+
 // Keys and bag ids of positions [P0, P1) (bags g0 .. g0 + nb - 1, whose
 // offsets lane j holds in my_off).  kKeyChunks chunks of 64 positions per
 // round: every index load of a round is issued before its first key is
@@ -142,6 +197,11 @@ __device__ __forceinline__ bool key_positions(const BwdArgs &a, const TableMeta 
 // sentinel key (one past its last row), which sorts after the table's rows
 // and is skipped later.
 __global__ __launch_bounds__(kBlock) void eb_bwd_keys_kernel(BwdArgs a) {
+  if (blockIdx.x == gridDim.x - 1) {
+    // every thread of the workgroup, before any wavefront can leave
+    __shared__ int64_t part[2 * kWavesPerBlock];
+    scan_tile_starts<kBlock>(a, part);
+  }
   const int32_t wid = (int32_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if (wid >= a.num_waves) return;
   const int lane = threadIdx.x & (kWave - 1);
@@ -169,57 +229,6 @@ __global__ __launch_bounds__(kBlock) void eb_bwd_keys_kernel(BwdArgs a) {
                            : key_positions<int32_t>(a, m, P0, P1, my_off, nb, g0);
   if (__ballot(oob)) {
     if (lane == 0) atomicOr(a.ctx.err, kErrIndex);
-  }
-}
-
-// tiles of table t (its clamped position range cut into tile_size pieces)
-__device__ __forceinline__ void table_range(const BwdArgs &a, int32_t t, int64_t &p0, int64_t &p1) {
-  p0 = clamp_pos(load_offset(a, (int64_t)t * a.batch), 0, a.num_indices);
-  p1 = clamp_pos(load_offset(a, (int64_t)(t + 1) * a.batch), p0, a.num_indices);
-}
-
-// Step 3a: first tile of every table (one workgroup; exclusive scan over tables).
-__global__ __launch_bounds__(1024) void eb_bwd_tile_start_kernel(BwdArgs a) {
-  __shared__ int64_t part[1024];
-  const int T = a.num_tables;
-  const int tid = threadIdx.x;
-  const int per = (T + 1023) / 1024;
-  const int t0 = tid * per < T ? tid * per : T;
-  const int t1 = t0 + per < T ? t0 + per : T;
-  int64_t sum = 0;
-  for (int t = t0; t < t1; ++t) {
-    int64_t p0, p1;
-    table_range(a, t, p0, p1);
-    sum += (p1 - p0 + a.tile_size - 1) / a.tile_size;
-  }
-  // exclusive scan of the per-thread sums: within each wavefront, then over
-  // the 16 wavefronts' totals
-  const int lane = tid & (kWave - 1), wave = tid / kWave;
-  int64_t incl = sum;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int64_t v = __shfl_up(incl, o);
-    if (lane >= o) incl += v;
-  }
-  if (lane == kWave - 1) part[wave] = incl;
-  __syncthreads();
-  if (wave == 0) {
-    int64_t w = lane < 1024 / kWave ? part[lane] : 0;
-#pragma unroll
-    for (int o = 1; o < 1024 / kWave; o <<= 1) {
-      const int64_t v = __shfl_up(w, o);
-      if (lane >= o) w += v;
-    }
-    if (lane < 1024 / kWave) part[kWave + lane] = w;  // inclusive totals of waves 0..lane
-  }
-  __syncthreads();
-  int64_t run = incl - sum + (wave > 0 ? part[kWave + wave - 1] : 0);
-  if (tid == 1023) a.tile_start[T] = (int32_t)(run + sum);
-  for (int t = t0; t < t1; ++t) {
-    a.tile_start[t] = (int32_t)run;
-    int64_t p0, p1;
-    table_range(a, t, p0, p1);
-    run += (p1 - p0 + a.tile_size - 1) / a.tile_size;
   }
 }
 
@@ -974,11 +983,7 @@ eb_status eb_backward_update(const eb_tables *h, eb_tensor indices, eb_tensor of
                                     rocprim::counting_iterator<uint32_t>(0), const_cast<uint32_t *>(a.spos),
                                     (unsigned int)n, 0, end_bit, h->stream);
   }
-  // 3. tiles: first tile per table, then pool and update
-  if (e == hipSuccess) {
-    hipLaunchKernelGGL(eb_bwd_tile_start_kernel, dim3(1), dim3(1024), 0, h->stream, a);
-    e = hipGetLastError();
-  }
+  // 3. tiles: pool and update (the first tile of each table came with the keys)
   const unsigned tgrid = (unsigned)((L.tiles_ub + kTileWaves - 1) / kTileWaves);
   const unsigned fgrid = (unsigned)((L.tiles_ub + kWavesPerBlock - 1) / kWavesPerBlock);
   // one launch per storage type present; fixed row width when all tables share it
