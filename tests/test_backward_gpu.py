@@ -211,6 +211,34 @@ def test_mixed_storage_and_widths(dev):
         run_and_check(w, dev, "rowwise_adagrad", label=f"mixed {pooling}")
 
 
+def test_many_tables(dev):
+    # 700 tables: the scan that finds each table's first tile runs on one
+    # workgroup with several tables per thread; whole tables without a
+    # lookup, and empty bags, sit between tables with lookups
+    g = torch.Generator(device="cpu")
+    g.manual_seed(5)
+    T, B = 700, 6
+    tables = []
+    for t in range(T):
+        R = int(torch.randint(20, 200, (1,), generator=g))
+        D = [4, 8, 16, 64][t % 4]
+        if t % 3 == 1:  # fp16 rows take dims that are multiples of 8
+            D = max(D, 8)
+            tables.append(Table((torch.randn((R, D), generator=g) * 0.01).half().to(dev), D, "f16"))
+        else:
+            tables.append(Table(torch.randn((R, D), generator=g).to(dev), D, "f32"))
+    lens = torch.randint(0, 30, (T * B,), generator=g)
+    for t in range(0, T, 7):
+        lens[t * B:(t + 1) * B] = 0
+    off = torch.zeros(T * B + 1, dtype=torch.int64)
+    torch.cumsum(lens, 0, out=off[1:])
+    parts = [torch.randint(0, t.num_rows, (int(lens[i * B:(i + 1) * B].sum()),), generator=g)
+             for i, t in enumerate(tables)]
+    idx = torch.cat(parts)
+    w = Workload("many tables", tables, B, idx.to(dev), off.to(dev), None, "sum", lens.to(dev))
+    run_and_check(w, dev, "rowwise_adagrad", label="700 tables")
+
+
 def test_deterministic(dev):
     w = make_workload("c3b", dev, **REDUCED["c3b"])
     init = [t.rows.clone() for t in w.tables]
