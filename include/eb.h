@@ -64,7 +64,7 @@
  * at the same time, forces how workgroups map onto the GPU's XCDs (default:
  * XCD-contiguous for handles of up to 32 tables, round-robin otherwise).
  * EB_BWD_TILE_CHUNKS=c (1..16) fixes the backward's tiles at 64*c sorted
- * positions (default: 64 to 256, from the number of lookups), and
+ * positions (default: 64, or 128 from about two million lookups on), and
  * EB_BWD_XCD_REMAP=0|1 its workgroup order (default as for the forward).
  * EB_LONG_BAG=n (n > 0) makes the handle's lookups pool every bag of more
  * than n lookups with all four wavefronts of a workgroup (each a contiguous
@@ -261,8 +261,8 @@ typedef enum { EB_OPT_SGD = 0, EB_OPT_ROWWISE_ADAGRAD = 1 } eb_optimizer;
 
 /*
  * Device workspace (bytes) eb_backward_update needs for num_indices lookups
- * on this handle: 16 bytes per lookup, then per tile of 64 to 256 sorted
- * lookups an 8-byte descriptor and two partial rows of the widest table
+ * on this handle: 16 bytes per lookup, then per tile of 64 or 128 sorted
+ * lookups (64*c under EB_BWD_TILE_CHUNKS=c) an 8-byte descriptor and two partial rows of the widest table
  * (8 * max dim bytes), and the sort's scratch.  Synchronous, host only.
  */
 eb_status eb_backward_workspace_size(const eb_tables *tables, int64_t num_indices, size_t *bytes);
