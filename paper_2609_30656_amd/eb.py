@@ -254,10 +254,11 @@ def eb_backward_update(tables: EbTables, indices: torch.Tensor, offsets: torch.T
                        workspace: Optional[torch.Tensor] = None) -> None:
     """Enqueue the backward + optimizer step on the handle's stream.
 
-    workspace: a device uint8 tensor of at least eb_backward_workspace_size()
-    bytes that stays untouched until the step has run on the handle's stream;
-    when None, one is allocated on that stream (torch's allocator then reuses
-    it only for work ordered after the step on the same stream)."""
+    workspace: a contiguous device tensor (any element type) of at least
+    eb_backward_workspace_size() bytes that stays untouched until the step
+    has run on the handle's stream; when None, one is allocated on that
+    stream (torch's allocator then reuses it only for work ordered after the
+    step on the same stream)."""
     lib = load_library()
     d = tables.device
     args = (_as_tensor(indices, d), _as_tensor(offsets, d), _as_tensor(per_sample_weights, d))
@@ -268,9 +269,11 @@ def eb_backward_update(tables: EbTables, indices: torch.Tensor, offsets: torch.T
             workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=d)
     elif workspace.device != d:
         raise ValueError(f"the workspace must be on the handle's GPU ({d}), got one on {workspace.device}")
+    elif not workspace.is_contiguous():
+        raise ValueError("the workspace must be contiguous")
     mode = POOLING[pooling] if isinstance(pooling, str) else int(pooling)
     opt = OPTIMIZERS[optimizer] if isinstance(optimizer, str) else int(optimizer)
     st = lib.eb_backward_update(tables.ptr, *args, mode, g, opt, float(learning_rate), float(eps),
-                                st_t, workspace.data_ptr(), workspace.numel())
+                                st_t, workspace.data_ptr(), workspace.numel() * workspace.element_size())
     if st != EB_OK:
         raise EBError(st, "eb_backward_update")

@@ -331,5 +331,18 @@ def test_backward_argument_errors(dev):
         with pytest.raises(eb.EBError) as e:  # workspace too small
             eb.eb_backward_update(h, idx, off, None, "sum", gr, workspace=torch.empty(16, dtype=torch.uint8, device=dev))
         assert e.value.status == eb.EB_ERR_INVALID_ARG
+        need = eb.eb_backward_workspace_size(h, idx.numel())
+        with pytest.raises(eb.EBError) as e:  # a float workspace counts its bytes: one float short
+            eb.eb_backward_update(h, idx, off, None, "sum", gr,
+                                  workspace=torch.empty((need + 3) // 4 - 1, dtype=torch.float32, device=dev))
+        assert e.value.status == eb.EB_ERR_INVALID_ARG
+        with pytest.raises(ValueError):
+            eb.eb_backward_update(h, idx, off, None, "sum", gr,
+                                  workspace=torch.empty((need + 8) * 2, dtype=torch.uint8, device=dev)[::2])
         torch.cuda.synchronize()
         assert torch.all(tab == 0)
+        # a float workspace of enough bytes is accepted, and the step runs
+        eb.eb_backward_update(h, idx, off, None, "sum", torch.ones((2, 16), device=dev), learning_rate=0.5,
+                              workspace=torch.empty((need + 3) // 4, dtype=torch.float32, device=dev))
+        torch.cuda.synchronize()
+        assert torch.all(tab[1:3] == -0.5) and torch.all(tab[0] == 0) and torch.all(tab[3:] == 0)
