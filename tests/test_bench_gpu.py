@@ -1,0 +1,58 @@
+"""bench.py's output line on the GPU: one JSON object with the fields its
+readers rely on (the metric and its unit, the step counts and timing, the
+workload, the roofline of the timed kernel and the CPU baseline), for a short
+run of the default workload and of the backward mode."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+pytestmark = pytest.mark.gpu
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _bench(*args):
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    print(f"[bench] {' '.join(args)}", flush=True)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [l for l in r.stdout.splitlines() if l.strip()]
+    assert len(lines) == 1, r.stdout
+    return json.loads(lines[0])
+
+
+def _check_common(d, steps, warmup):
+    for k in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+              "scaling", "vs_baseline", "dtype", "data", "config", "roofline"):
+        assert k in d, k
+    assert d["n_gpus"] == 1 and d["steps"] == steps and d["warmup"] == warmup
+    assert d["unit"] == "GB/s" and d["higher_is_better"] is True and d["scaling"] == "weak"
+    assert d["value"] > 0 and d["ms_per_step"] > 0
+    assert isinstance(d["config"].get("workload"), str) and d["config"]["workload"]
+    r = d["roofline"]
+    for k in ("bound", "achieved", "peak", "unit", "frac", "traffic"):
+        assert k in r, k
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert abs(r["frac"] - r["achieved"] / r["peak"]) < 1e-3
+    assert r["traffic"] is None or r["traffic"] > 0
+
+
+def test_default_workload_line():
+    d = _bench("--steps", "20", "--warmup", "3", "--cpu-budget", "1", "--cold-reps", "3")
+    _check_common(d, 20, 3)
+    assert d["config"]["workload"].startswith("c2")
+    cb = d["cpu_baseline"]
+    for k in ("value", "unit", "cores", "kind", "sample"):
+        assert k in cb, k
+    assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1 and cb["unit"] == d["unit"]
+
+
+def test_backward_mode_line():
+    d = _bench("--mode", "backward", "--steps", "5", "--warmup", "2", "--cpu-budget", "0", "--cold-reps", "0")
+    _check_common(d, 5, 2)
+    assert "bwd" in d["metric"]
