@@ -35,6 +35,7 @@ constexpr size_t kZeroBytes = 4 * kMaxDim + 16;
 constexpr int kMaxBagsPerWave = 32;
 // Wavefronts resident on a full MI355X (256 CUs x 4 SIMDs x 8 waves).
 constexpr int64_t kResidentWaves = 256 * 4 * 8;
+constexpr int64_t kTailGens = 4;  // default taper of the lookup's runs (sets of resident wavefronts)
 // The backward keeps one gradient row slice per lane: rows of up to 64 lanes
 // x 4 fp32 values.
 constexpr int kMaxBackwardDim = 256;
@@ -521,6 +522,8 @@ struct eb_tables {
   int32_t num_tables;
   int32_t checked;
   int32_t bags_per_wave;  // 0: chosen per call from the bag count
+  int32_t tail_gens;      // lookup taper: tail runs for this many sets of resident wavefronts (-1: default rule)
+  int32_t tail_run;       // bags per tail run
   int64_t long_bag_len;   // > 0: the lookup splits bags with more lookups over a workgroup's wavefronts
   int32_t dtype_mask;     // bit d set: some table has storage type d
   int32_t single_log2;    // lanes-per-row log2 shared by every table of one type, else -1
