@@ -9,9 +9,10 @@
 // is no matrix-core work because there is no dense contraction.
 //
 // Execution model:
-//   * a wavefront (64 lanes, a workgroup of its own) pools k consecutive
-//     bags of one table, walking their index positions as one stream of
-//     chunks of up to 64 indices, one coalesced load per chunk, the next
+//   * a wavefront (64 lanes, a workgroup of its own) pools a run of
+//     consecutive bags of one table (k bags; each table's last bags in runs
+//     of one, dispatched last), walking their index positions as one stream
+//     of chunks of up to 64 indices, one coalesced load per chunk, the next
 //     chunk's load issued before the current chunk's rows are gathered;
 //   * a row is split into 16-byte lane slices; LPR = lanes per row (the next
 //     power of two >= row bytes / 16, at most 64), so one wave-wide load
