@@ -522,8 +522,8 @@ struct eb_tables {
   int32_t num_tables;
   int32_t checked;
   int32_t bags_per_wave;  // 0: chosen per call from the bag count
-  int32_t tail_gens;      // lookup taper: tail runs for this many sets of resident wavefronts (-1: default rule)
-  int32_t tail_run;       // bags per tail run
+  int64_t tail_bags;      // lookup taper: bags per table in short runs at the end (-1: chosen per call)
+  int32_t tail_run;       // bags per such run
   int64_t long_bag_len;   // > 0: the lookup splits bags with more lookups over a workgroup's wavefronts
   int32_t dtype_mask;     // bit d set: some table has storage type d
   int32_t single_log2;    // lanes-per-row log2 shared by every table of one type, else -1

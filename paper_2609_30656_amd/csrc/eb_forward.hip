@@ -34,6 +34,8 @@
 namespace eb {
 namespace {
 
+constexpr int kMaxAutoBagsPerWave = 8;  // cap of the lookup's own choice of bags per wavefront
+
 struct FwdArgs {
   const TableMeta *meta;
   GatherCtx ctx;
@@ -511,23 +513,26 @@ hipError_t launch_forward(const eb_tables *h, const eb_tensor &indices, const eb
     // More bags per wavefront hide more latency (each bag's indices arrive
     // while the previous bag's rows are in flight); fewer leave more
     // wavefronts to balance the load.  Measured optimum on MI355X: about
-    // sqrt(bags / resident wavefronts).
+    // sqrt(bags / resident wavefronts), at most 8 (with the taper below, 8
+    // beat the 10 and 22 of that rule on c4 and c5 by 1.5 and 3%).
     const int64_t per_slot = sh.num_bags / kResidentWaves;
     k = 1;
     while ((k + 1) * (k + 1) <= per_slot) ++k;
-    k = k > kMaxBagsPerWave ? kMaxBagsPerWave : k;
+    k = k > kMaxAutoBagsPerWave ? kMaxAutoBagsPerWave : k;
   }
   a.bags_per_wave = (int32_t)k;
   // Taper: the last bags of each table go in runs of tail_run bags, enough of
-  // them for `gens` full sets of resident wavefronts over all tables; the
+  // them for kTailGens full sets of resident wavefronts over all tables; the
   // rest in runs of k.  Long runs first and short ones last end the launch
   // sooner when bag lengths are heavy-tailed (on MI355X, power-law c3-like
   // lengths: 6-10% faster at 4 sets).  With k <= 2 the runs are short
-  // already and a taper only adds wavefronts.
-  int64_t gens = h->tail_gens >= 0 ? h->tail_gens : (k >= 3 ? kTailGens : 0);
-  const int64_t tail_run = gens > 0 ? (h->tail_run < k ? h->tail_run : k) : k;
-  int64_t tail_bags = (gens * kResidentWaves * tail_run + h->num_tables - 1) / h->num_tables;
+  // already and a taper only adds wavefronts.  A handle made with
+  // EB_TAIL_BAGS set uses that many tail bags per table instead.
+  const int64_t run = h->tail_run < k ? h->tail_run : k;
+  int64_t tail_bags = h->tail_bags >= 0 ? h->tail_bags
+                      : (k >= 3 ? (kTailGens * kResidentWaves * run + h->num_tables - 1) / h->num_tables : 0);
   tail_bags = tail_bags < sh.batch ? tail_bags : sh.batch;
+  const int64_t tail_run = tail_bags > 0 ? run : k;
   const int64_t head_groups = (sh.batch - tail_bags) / k;
   const int64_t rest = sh.batch - head_groups * k;
   a.head_groups = (int32_t)head_groups;
@@ -538,7 +543,7 @@ hipError_t launch_forward(const eb_tables *h, const eb_tensor &indices, const eb
   // so the tail runs of every table go last; with it, each XCD runs its own
   // contiguous range of tables and a table's tail runs end that table.  The
   // long-bag split needs a workgroup's runs contiguous, so keeps table order.
-  a.tail_last = (gens > 0 && !h->xcd_remap && h->long_bag_len == 0 && head_groups > 0 && a.tail_groups > 0) ? 1 : 0;
+  a.tail_last = (tail_bags > 0 && !h->xcd_remap && h->long_bag_len == 0 && head_groups > 0 && a.tail_groups > 0) ? 1 : 0;
   a.head_waves = (int32_t)(head_groups * h->num_tables);
   const int64_t num_waves = (int64_t)a.groups_per_table * h->num_tables;
   a.num_waves = (int32_t)num_waves;
@@ -709,9 +714,9 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   h->long_bag_len = lb ? atoll(lb) : 0;
   if (h->long_bag_len < 0) h->long_bag_len = 0;
   if (h->long_bag_len > 0 && h->long_bag_len < kWavesPerBlock) h->long_bag_len = kWavesPerBlock;
-  const char *tg = getenv("EB_TAIL_GENS");
-  h->tail_gens = tg ? atoi(tg) : -1;
-  if (h->tail_gens < -1 || h->tail_gens > 64) h->tail_gens = -1;
+  const char *tb = getenv("EB_TAIL_BAGS");
+  h->tail_bags = tb ? atoll(tb) : -1;
+  if (h->tail_bags < -1) h->tail_bags = -1;
   const char *tr = getenv("EB_TAIL_RUN");
   h->tail_run = tr ? atoi(tr) : 1;
   if (h->tail_run < 1 || h->tail_run > kMaxBagsPerWave) h->tail_run = 1;

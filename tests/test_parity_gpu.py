@@ -150,8 +150,41 @@ def test_bags_per_wave(dev, monkeypatch, name, k):
     # last group of each table is partial whenever k does not divide B
     say(f"[parity] bags per wave {k} {name}")
     monkeypatch.setenv("EB_BAGS_PER_WAVE", str(k))
+    monkeypatch.setenv("EB_TAIL_BAGS", "0")  # runs of k bags only (no taper)
     w = make_workload(name, dev, **REDUCED[name])
     full_check(w, f"k={k} {name}")
+
+
+@pytest.mark.parametrize("remap", ["0", "1"])
+@pytest.mark.parametrize("name", ["c3b", "c4"])
+def test_tapered_runs(dev, monkeypatch, name, remap):
+    # each table's last bags in short runs after its runs of k bags: with the
+    # XCD renumbering the runs go table by table, without it every table's
+    # head runs come first; with the long-bag split a workgroup's runs stay
+    # contiguous.  Which wavefront pools a bag changes, the order of a bag's
+    # additions does not, so every mapping gives the untapered output's bits.
+    say(f"[parity] tapered runs {name} remap={remap}")
+    monkeypatch.setenv("EB_XCD_REMAP", remap)
+    w = make_workload(name, dev, **REDUCED[name])
+    monkeypatch.setenv("EB_BAGS_PER_WAVE", "3")
+    monkeypatch.setenv("EB_TAIL_BAGS", "0")
+    base = full_check(w, f"untapered {name}")
+    ref, asum = oracle_forward(w)
+    B = w.batch
+    cases = [(k, tail, run, long_len)
+             for k in ("3", "7") for tail in (1, 37, B - 1, B, 10 ** 9) for run in ("1", "2", "5")
+             for long_len in ("0", "16")]
+    for k, tail, run, long_len in cases:
+        monkeypatch.setenv("EB_BAGS_PER_WAVE", k)
+        monkeypatch.setenv("EB_TAIL_BAGS", str(tail))
+        monkeypatch.setenv("EB_TAIL_RUN", run)
+        monkeypatch.setenv("EB_LONG_BAG", long_len)
+        got = run_gpu(w).cpu().numpy()
+        label = f"{name} remap={remap} k={k} tail={tail} run={run} long={long_len}"
+        if long_len == "0":
+            assert np.array_equal(got.view(np.uint32), base.view(np.uint32)), label
+        else:  # the split adds a long bag's four quarters: a different order
+            check(got, ref, asum, per_element_lengths(w), RTOL[w.tables[0].dtype], label)
 
 
 @pytest.mark.parametrize("long_len", ["4", "16", "64"])
