@@ -60,7 +60,11 @@
  * Tuning.  EB_BAGS_PER_WAVE=k (1..32), read when a handle is created, fixes
  * how many consecutive bags of one table a wavefront pools (and how many
  * 64-position chunks a wavefront of eb_forward_seq copies); without it the
- * count is chosen per call from the number of bags (positions).  EB_XCD_REMAP=0|1, read
+ * count is chosen per call from the number of bags (positions).  With 3 or
+ * more bags per wavefront, each table's last bags go in short runs that the
+ * GPU starts last; EB_TAIL_BAGS=n (n >= 0, 0: none) fixes how many bags of
+ * each table that tail holds and EB_TAIL_RUN=r (1..32, default 1) the bags
+ * per tail run.  EB_XCD_REMAP=0|1, read
  * at the same time, forces how workgroups map onto the GPU's XCDs (default:
  * XCD-contiguous for handles of up to 32 tables, round-robin otherwise).
  * EB_BWD_TILE_CHUNKS=c (1..16) fixes the backward's tiles at 64*c sorted
