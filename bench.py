@@ -44,6 +44,17 @@ METRIC_SEQ = "Un-pooled (sequence) embedding lookup achieved HBM GB/s (% of peak
 SAMPLE = 7
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_cores() -> int:
     try:
         return len(os.sched_getaffinity(0))
@@ -51,14 +62,15 @@ def cpu_cores() -> int:
         return os.cpu_count() or 1
 
 
-def run_cpu_baseline_seq(w, budget_s: float, host_bytes_cap: float = 3e9):
+def run_cpu_baseline_seq(w, budget_s: float, host_bytes_cap: float = 3e9, threads: int = 0):
     """Time the oracle's un-pooled lookup (as it stands) on the positions of
     the first tables of `w` whose rows fit in `host_bytes_cap` bytes, repeated
     until `budget_s` seconds have passed.  Returns (reps, seconds, threads,
     lookups per rep, algorithmic bytes per rep, tables used)."""
     import oracle
 
-    threads = min(cpu_cores(), int(os.environ.get("OMP_NUM_THREADS", cpu_cores())))
+    if threads <= 0:
+        threads = min(cpu_cores(), int(os.environ.get("OMP_NUM_THREADS", cpu_cores())))
     use, acc = 0, 0
     for t in w.tables:
         nbytes = t.rows.numel() * t.rows.element_size()
@@ -84,7 +96,7 @@ def run_cpu_baseline_seq(w, budget_s: float, host_bytes_cap: float = 3e9):
     return reps, el, threads, look, nbytes, use
 
 
-def run_cpu_baseline(w, budget_s: float, host_bytes_cap: float = 3e9, fm: bool = False):
+def run_cpu_baseline(w, budget_s: float, host_bytes_cap: float = 3e9, fm: bool = False, threads: int = 0):
     """Time the oracle (as it stands) on the bags of the first tables of `w`
     whose rows fit in `host_bytes_cap` bytes of host memory (all tables for the
     smaller workloads), repeated until `budget_s` seconds have passed.  With
@@ -96,7 +108,8 @@ def run_cpu_baseline(w, budget_s: float, host_bytes_cap: float = 3e9, fm: bool =
 
     import oracle
 
-    threads = min(cpu_cores(), int(os.environ.get("OMP_NUM_THREADS", cpu_cores())))
+    if threads <= 0:
+        threads = min(cpu_cores(), int(os.environ.get("OMP_NUM_THREADS", cpu_cores())))
     use, acc = 0, 0
     for t in w.tables:
         nbytes = t.rows.numel() * t.rows.element_size()
@@ -365,7 +378,17 @@ def main():
             "kind": "oracle",
             "sample": f"{reps} pass(es) of the oracle over {what} of batch 0 of {args.config} "
                       f"({look} lookups per pass) on the host, {el:.1f} s",
+            "cpu_model": cpu_model(),
         }
+        if threads > 1:
+            # the same sample on one thread, for a fifth of the budget (at least one pass)
+            b1 = args.cpu_budget / 5
+            if args.mode == "seq":
+                r1, e1, _, look1, nb1, _ = run_cpu_baseline_seq(w0, b1, threads=1)
+            else:
+                r1, e1, _, look1, nb1, _ = run_cpu_baseline(w0, b1, fm=fm, threads=1)
+            cpu["one_thread"] = {"value": round(nb1 * r1 / e1 / 1e9, 4), "unit": "GB/s",
+                                 "lookups_per_s": round(look1 * r1 / e1, 1), "seconds": round(e1, 1)}
 
     dtypes = sorted({t.dtype for t in w0.tables})
     line = {

@@ -50,6 +50,10 @@ def test_default_workload_line():
     for k in ("value", "unit", "cores", "kind", "sample"):
         assert k in cb, k
     assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1 and cb["unit"] == d["unit"]
+    assert isinstance(cb.get("cpu_model"), str) and cb["cpu_model"]
+    if cb["cores"] > 1:  # the same sample on one host thread
+        one = cb["one_thread"]
+        assert one["value"] > 0 and one["lookups_per_s"] > 0 and one["unit"] == d["unit"]
 
 
 def test_backward_mode_line():
