@@ -10,7 +10,13 @@ consecutive steps do not replay identical lookups.  Tables, indices and
 offsets are resident in HBM before the timed region starts.
 
 Prints one JSON line:
-  value            algorithmic GB/s over the K timed steps (wall clock)
+  value            algorithmic GB/s over the K timed steps (wall clock): the
+                   bytes the operation must move, duplicates counted, over
+                   the time.  Zipf rows repeat within a batch and are served
+                   from L2 and the Infinity Cache, so this rate is not an HBM
+                   rate and can exceed the HBM peak; the fabric's own rate
+                   (rocprofv3 byte counters) and a uniform-index control are
+                   reported beside it
   lookups_per_s    pooled lookups per second over the same steps
   roofline         eb_pool_kernel's algorithmic bytes per launch / its mean
                    launch time: the K timed steps between one pair of HIP
@@ -21,7 +27,13 @@ Prints one JSON line:
                    events and the launch's dispatch); and `cold`: calls each
                    preceded (outside their events) by a 1 GiB read that
                    evicts L2 and the Infinity Cache
+  uniform_control  the same tables with uniformly drawn indices (no reuse
+                   between lookups): the kernel's rate when every row comes
+                   from HBM
   cpu_baseline     the CPU oracle on a bounded sample of the same workload
+
+The default workload is c5, the largest that fits one GPU (64 int8 row-wise
+tables of 6 M rows: one GPU's share of a table-wise sharded model).
 
 Algorithmic bytes per step = gathered row bytes (every lookup, duplicates
 counted) + index bytes + offset bytes + weight bytes + output bytes.
@@ -151,13 +163,16 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="c2", help="workload: c1 c2 c3a c3b c4 c5")
+    ap.add_argument("--config", default="c5", help="workload: c1 c2 c3a c3b c4 c5")
     ap.add_argument("--index-law", default="zipf", choices=["zipf", "uniform"],
                     help="uniform = no-reuse control at the same shapes")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing (0 = skip)")
     ap.add_argument("--cold-reps", type=int, default=15,
                     help="after the timed loop, time this many calls each preceded (outside the events) by a "
                          "1 GiB read that evicts L2 and the Infinity Cache (0 = skip)")
+    ap.add_argument("--uniform-steps", type=int, default=-1,
+                    help="forward mode with Zipf indices: time this many steps over the same tables with uniform "
+                         "indices (the no-reuse control; -1: min(steps, 20); 0 = skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (to scale rocprofv3 byte counters)")
     ap.add_argument("--mode", default="forward", choices=["forward", "fm", "seq", "backward"],
@@ -324,6 +339,43 @@ def main():
                 "achieved": round(cold_bytes / args.cold_reps / (c50 * 1e-3) / 1e9, 2)}
     w10, w50, w90 = quantiles(kern_ms)
 
+    uniform = None
+    n_uni = min(args.steps, 20) if args.uniform_steps < 0 else args.uniform_steps
+    if args.mode == "forward" and args.index_law == "zipf" and n_uni > 0:
+        # the no-reuse control: one batch of the same shape over the same
+        # tables with uniformly drawn rows, timed like the main loop
+        print(f"[bench] uniform-index control, {n_uni} steps", file=sys.stderr, flush=True)
+        wu = make_workload(args.config, dev, batch_seed=0, index_law="uniform", tables=w0.tables)
+        cu = (eb._as_tensor(wu.indices), eb._as_tensor(wu.offsets), eb._as_tensor(wu.weights),
+              eb.POOLING[wu.pooling])
+
+        def uniform_step(k):
+            st = lib.eb_forward(h.ptr, *cu[:3], cu[3], o)
+            if st != eb.EB_OK:
+                raise eb.EBError(st, "eb_forward")
+
+        for k in range(min(3, n_uni)):
+            uniform_step(k)
+        r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        r0.record(stream)
+        for k in range(n_uni):
+            uniform_step(k)
+        r1.record(stream)
+        torch.cuda.synchronize()
+        u_ms = r0.elapsed_time(r1) / n_uni
+        u_bytes = wu.algorithmic_bytes()
+        u_traffic = counter_traffic(args.config, "uniform", "forward")
+        uniform = {"index_law": "uniform", "steps": n_uni, "kernel_ms_avg": round(u_ms, 5),
+                   "lookups": wu.num_indices, "algorithmic_bytes": u_bytes,
+                   "achieved": round(u_bytes / (u_ms * 1e-3) / 1e9, 2),
+                   "frac": round(u_bytes / (u_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                   "lookups_per_s": round(wu.num_indices / (u_ms * 1e-3), 1),
+                   "traffic": None if u_traffic is None else round(u_traffic),
+                   "traffic_frac": None if u_traffic is None else
+                   round(u_traffic / (u_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+        del wu, cu
+
     bytes_total = sum(algo[k % 3] for k in range(args.steps))
     look_total = sum(nlook[k % 3] for k in range(args.steps))
     value = bytes_total / wall / 1e9
@@ -391,11 +443,18 @@ def main():
                                  "lookups_per_s": round(look1 * r1 / e1, 1), "seconds": round(e1, 1)}
 
     dtypes = sorted({t.dtype for t in w0.tables})
+    # what the path computes in: the stored values (u8 codes with fp16 scale
+    # and bias, fp16 or fp32) widened or dequantised to fp32, summed in fp32
+    path_dtype = "+".join({"f32": "f32", "f16": "f16->f32", "int8_rowwise": "u8->f32"}[d] for d in dtypes)
+    fabric_gbs = None if traffic is None else traffic / kern_avg_s / 1e9
     line = {
         "metric": {"forward": METRIC, "fm": METRIC_FM, "seq": METRIC_SEQ, "backward": METRIC_BACKWARD}[args.mode],
         "value": round(value, 2),
         "unit": "GB/s",
-        "pct_of_peak_hbm": round(100.0 * value / PEAK_HBM_GBS, 2),
+        "value_basis": "algorithmic bytes (rows gathered with duplicates counted, indices, offsets, weights, "
+                       "outputs) / wall time of the timed steps; not an HBM rate when rows repeat",
+        "algorithmic_pct_of_peak": round(100.0 * value / PEAK_HBM_GBS, 2),
+        "fabric_pct_of_peak": None if fabric_gbs is None else round(100.0 * fabric_gbs / PEAK_HBM_GBS, 2),
         "lookups_per_s": round(look_total / wall, 1),
         "n_gpus": 1,
         "steps": args.steps,
@@ -404,7 +463,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": path_dtype,
+        "accumulate": "f32",
         "data": "synthetic",
         "config": {
             "workload": f"{args.config}: {CONFIGS[args.config].summary}",
@@ -440,6 +500,7 @@ def main():
             "sampled_launches": len(sample),
             "cold": cold,
         },
+        "uniform_control": uniform,
         "cpu_baseline": cpu,
     }
     if fm_pass is not None:

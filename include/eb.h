@@ -156,7 +156,10 @@ typedef struct eb_tables eb_tables;
  * device at this call is the handle's device.  On success *out receives the
  * handle, which the caller releases with eb_destroy.  Synchronous: allocates
  * one small device array (EB_ERR_OOM if that fails) and copies the
- * descriptors into it.  Each table's rows must be memory the handle's device
+ * descriptors into it.  EB_DEVICE_ALLOC_LIMIT=n, read at this call, caps that
+ * array at n bytes (about 33 KiB plus 56 bytes per table): a larger one fails
+ * with EB_ERR_OOM as if the device were out of memory (for processes that
+ * budget device memory).  Each table's rows must be memory the handle's device
  * can read in place: its own device memory, managed memory or pinned host
  * memory; pageable host memory and another device's memory give
  * EB_ERR_INVALID_ARG.  On error *out is set to NULL.
@@ -296,10 +299,22 @@ eb_status eb_backward_update(const eb_tables *tables, eb_tensor indices, eb_tens
                              int32_t optimizer, float learning_rate, float eps,
                              eb_tensor optimizer_state, void *workspace, size_t workspace_bytes);
 
-/* Release a handle (synchronises its stream first).  NULL is a no-op. */
+/*
+ * Release a handle: synchronises its stream, then frees the device array
+ * that eb_create_tables allocated and the handle itself (never the tables'
+ * rows, which the caller owns).  NULL is a no-op returning EB_OK.  Returns
+ * EB_ERR_HIP if the synchronisation or the free fails; the handle is released
+ * either way and must not be used again.
+ * Handle plumbing of the lookup's life cycle (create, use, destroy); it
+ * computes nothing the paper describes.
+ */
 eb_status eb_destroy(eb_tables *tables);
 
-/* Static, never-NULL English description of a status code. */
+/*
+ * Static, never-NULL English description of a status code (unknown codes
+ * give "unknown status").  Host only, thread-safe.
+ * Error-reporting plumbing of this interface; no paper passage defines it.
+ */
 const char *eb_status_string(eb_status s);
 
 #ifdef __cplusplus

@@ -31,15 +31,28 @@ class OracleError(RuntimeError):
         self.code = code
 
 
+# EBO_ORACLE_LIB names another build of eb_oracle.c to load (the sanitizer
+# build of the tests); by default the library built next to the source.
+_LIB_ENV = "EBO_ORACLE_LIB"
+
+# AddressSanitizer and UndefinedBehaviorSanitizer, every report fatal.
+SANITIZE_FLAGS = ["-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                  "-fno-omit-frame-pointer"]
+
+
 def lib_path() -> str:
-    return os.path.join(_HERE, _LIB_NAME)
+    return os.environ.get(_LIB_ENV) or os.path.join(_HERE, _LIB_NAME)
 
 
-def build() -> str:
-    """Compile eb_oracle.c with gcc (-O2, no fast-math, no FP contraction, OpenMP)."""
-    out = lib_path()
+def build(out: Optional[str] = None, sanitize: bool = False) -> str:
+    """Compile eb_oracle.c with gcc (-O2, no fast-math, no FP contraction,
+    OpenMP) into `out` (default: lib_path()).  sanitize=True builds it with
+    AddressSanitizer and UndefinedBehaviorSanitizer instead of -O2; such a
+    library must be loaded into a process that preloads the ASan runtime."""
+    out = out or lib_path()
     tmp = out + ".tmp"
-    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+    opt = SANITIZE_FLAGS if sanitize else ["-O2"]
+    cmd = ["gcc", *opt, "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
            "-Wall", "-Wextra", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, out)
@@ -63,7 +76,8 @@ def _load():
     global _lib
     if _lib is None:
         path = lib_path()
-        if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
+        if not os.environ.get(_LIB_ENV) and (not os.path.exists(path) or
+                                             os.path.getmtime(path) < os.path.getmtime(_SRC)):
             build()
         lib = ctypes.CDLL(path)
         lib.ebo_forward.restype = ctypes.c_int

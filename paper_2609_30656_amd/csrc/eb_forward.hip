@@ -729,6 +729,14 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   // [descriptors][error word, padded to 256 B][zero row]
   const size_t err_off = (meta_bytes + 255) / 256 * 256;
   const size_t zero_off = err_off + 256;
+  // a caller's cap on the handle's device memory: past it, fail as the
+  // allocator would
+  const char *cap = getenv("EB_DEVICE_ALLOC_LIMIT");
+  if (cap && cap[0] && strtoull(cap, nullptr, 10) < zero_off + kZeroBytes) {
+    free(meta);
+    free(h);
+    return EB_ERR_OOM;
+  }
   void *dev = nullptr;
   hipError_t e = hipMalloc(&dev, zero_off + kZeroBytes);
   if (e != hipSuccess) {

@@ -1,6 +1,6 @@
 """rocprofv3 summaries of the benchmark's dominant kernel.
 
-    python -m paper_2609_30656_amd.profiling --mode forward --config c2 [--index-law zipf]
+    python -m paper_2609_30656_amd.profiling --mode forward --config c5 [--index-law zipf]
 
 runs, one after another (each under its own time limit):
   1. a kernel trace of `bench.py` (--kernel-trace --stats): per-launch duration;
@@ -116,7 +116,7 @@ def _match(name, kernel):
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--mode", default="forward", choices=sorted(KERNELS))
-    ap.add_argument("--config", default="c2")
+    ap.add_argument("--config", default="c5")
     ap.add_argument("--index-law", default="zipf", choices=["zipf", "uniform"])
     ap.add_argument("--work", default="/tmp/eb_profiling", help="scratch directory for rocprofv3 output")
     ap.add_argument("--limit", type=int, default=300, help="seconds allowed per rocprofv3 run")

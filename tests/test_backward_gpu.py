@@ -9,7 +9,15 @@ gradient G (fp64), error scale S = sum_i |c_i g| and occurrence count n:
             propagated (bounds computed below from G, S, n), and the state
             itself within its bound,
 with u = 2^-24: fp32 summation of the n terms in any order, the tile partial
-sums included.
+sums included.  Those bounds are first order in u: each term is k u X with
+k <= n + 16.  Higham's gamma_k = k u / (1 - k u) makes such a term rigorous
+(the roundings' second-order products included), and gamma_k <= k u / (1 -
+(n + 16) u) for every such k, so the first-order bound divided by
+1 - (n + 16) u is a rigorous one.  The Adagrad step size sigma = lr /
+(sqrt(s) + eps) is taken with its exact perturbation: a state off by at most
+ds moves sqrt(s) by at most ds / (sqrt(s) + sqrt(max(s - ds, 0))), so sigma
+moves by at most that over (sqrt(max(s - ds, 0)) + eps) relative to itself,
+for any ds; its own roundings add gamma_6.
 """
 import numpy as np
 import pytest
@@ -97,12 +105,21 @@ def run_and_check(w, dev, optimizer, lr=0.05, eps=1e-4, check_tables=None, label
             D = tb.dim
             ds = 2 * (np.abs(G) * dG).sum(axis=1) / D + (D + 8) * U * s_new
             scale = lr / (np.sqrt(s_new) + eps)
-            rel = 0.5 * ds / np.maximum(s_new, 1e-30) + 6 * U
-            bound = scale[:, None] * dG + np.abs(scale[:, None] * G) * rel[:, None] + store
+            # relative error of the step size lr / (sqrt(s) + eps) when the
+            # state is off by at most ds (valid for any ds; module docstring),
+            # plus its own roundings
+            sq, sq_lo = np.sqrt(s_new), np.sqrt(np.maximum(s_new - ds, 0.0))
+            with np.errstate(divide="ignore", invalid="ignore"):
+                rel = np.where(s_new > 0, ds / (sq + sq_lo) / (sq_lo + eps), 0.0)
+            rel = rel + 6 * U / (1 - 6 * U) * (1 + rel)
+            moved = np.any(G != 0, axis=1)  # a zero gradient moves nothing, whatever the step size
+            bound = scale[:, None] * dG + np.where(moved[:, None], np.abs(scale[:, None] * G) * rel[:, None], 0.0) \
+                + store
             np.testing.assert_array_less(np.abs(state1[base[t] + rows] - s_new), ds + 2 * U * s_new + 1e-30)
             assert np.array_equal(state1[base[t]:base[t + 1]][untouched], state0[base[t]:base[t + 1]][untouched])
         err = np.abs(g64 - r64)
-        bad = err > bound * 1.0001 + 1e-30
+        bound = bound / (1 - (n[:, None] + 16) * U)  # first order -> rigorous (module docstring)
+        bad = err > bound + 1e-30
         assert not bad.any(), (f"{label} t{t}: {bad.sum()} elements beyond the bound; worst ratio "
                                f"{np.max(err / np.maximum(bound, 1e-30)):.3g}")
 

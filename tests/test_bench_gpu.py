@@ -19,7 +19,7 @@ def _bench(*args):
         pytest.skip("no GPU")
     print(f"[bench] {' '.join(args)}", flush=True)
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], capture_output=True, text=True,
-                       timeout=300)
+                       timeout=600)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [l for l in r.stdout.splitlines() if l.strip()]
     assert len(lines) == 1, r.stdout
@@ -43,9 +43,17 @@ def _check_common(d, steps, warmup):
 
 
 def test_default_workload_line():
-    d = _bench("--steps", "20", "--warmup", "3", "--cpu-budget", "1", "--cold-reps", "3")
+    # the default workload is c5 (64 int8 row-wise tables, the largest that
+    # fits one GPU), with its uniform-index control
+    d = _bench("--steps", "20", "--warmup", "3", "--cpu-budget", "1", "--cold-reps", "3", "--uniform-steps", "5")
     _check_common(d, 20, 3)
-    assert d["config"]["workload"].startswith("c2")
+    assert d["config"]["workload"].startswith("c5")
+    assert d["dtype"] == "u8->f32" and d["accumulate"] == "f32"
+    assert abs(d["algorithmic_pct_of_peak"] - 100 * d["value"] / 8000.0) < 0.01
+    u = d["uniform_control"]
+    assert u["index_law"] == "uniform" and u["steps"] == 5 and u["kernel_ms_avg"] > 0
+    assert abs(u["frac"] - u["achieved"] / 8000.0) < 1e-3
+    assert 0 < u["frac"] <= 1.0  # no reuse: every row comes from HBM
     cb = d["cpu_baseline"]
     for k in ("value", "unit", "cores", "kind", "sample"):
         assert k in cb, k
@@ -57,6 +65,8 @@ def test_default_workload_line():
 
 
 def test_backward_mode_line():
-    d = _bench("--mode", "backward", "--steps", "5", "--warmup", "2", "--cpu-budget", "0", "--cold-reps", "0")
+    d = _bench("--mode", "backward", "--config", "c2", "--steps", "5", "--warmup", "2", "--cpu-budget", "0",
+               "--cold-reps", "0")
     _check_common(d, 5, 2)
-    assert "bwd" in d["metric"]
+    assert "bwd" in d["metric"] and d["dtype"] == "f32"
+    assert d["uniform_control"] is None

@@ -22,7 +22,7 @@ from oracle import OracleTable, ebo_forward, ebo_forward_seq
 from paper_2609_30656_amd import eb
 from paper_2609_30656_amd.workload import Workload
 from test_backward_gpu import run_and_check
-from test_parity_gpu import RTOL, _table, check, per_element_lengths
+from test_parity_gpu import RTOL, _table, check, int8_parts, per_element_lengths
 
 pytestmark = pytest.mark.gpu
 
@@ -126,12 +126,15 @@ def test_pooled_lookup_past_4gib(dev, tables, mode):
     check(got[:, :128], ref[:, :128], asum[:, :128], L[:, :128], RTOL["f32"], f"large f32 {mode}")
     bscale = None
     if mode != "weighted":
-        u8 = tabs[1].rows
+        # s' = sum(|s q|) + sum(|c|): the oracle's fp64 absolute sums over a
+        # table of |s| q and one of |c| in every column (both exact in fp32)
         D = 128
-        sc = np.abs(u8[:, D:D + 2].copy().view(np.float16).astype(np.float32))
-        bi = np.abs(u8[:, D + 2:D + 4].copy().view(np.float16).astype(np.float32))
-        a = OracleTable(np.ascontiguousarray((u8[:, :D] * sc + bi) * np.float32(1.0001)), D, "f32")
-        bscale = ebo_forward([tabs[0], a], idx, off, None, w.pooling, with_absum=True)[1][:, 128:]
+        q, sc, bi = int8_parts(tabs[1].rows, D)
+        R = q.shape[0]
+        prod = OracleTable(np.ascontiguousarray(q.astype(np.float32) * sc), D, "f32")
+        bias = OracleTable(np.ascontiguousarray(np.broadcast_to(bi, (R, D))), D, "f32")
+        bscale = (ebo_forward([tabs[0], prod], idx, off, None, w.pooling, with_absum=True)[1][:, 128:] +
+                  ebo_forward([tabs[0], bias], idx, off, None, w.pooling, with_absum=True)[1][:, 128:])
     check(got[:, 128:], ref[:, 128:], asum[:, 128:], L[:, 128:], RTOL["int8_rowwise"], f"large int8 {mode}",
           bscale)
 

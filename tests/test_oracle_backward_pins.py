@@ -58,6 +58,41 @@ def test_worked_rowwise_adagrad():
     np.testing.assert_array_equal(state, [36, 5, 0, 0])  # untouched rows keep their state
 
 
+@pytest.mark.parametrize("lr,eps,expect", [
+    # eps is added to the square root, outside it: lr / (sqrt(36) + 2) = 8 / 8 = 1
+    (8.0, 2.0, [[0, -5], [3, 4], [5, 6], [7, 8]]),
+    # 4 / (6 + 2) = 1/2: W0 - G / 2
+    (4.0, 2.0, [[0.5, -1.5], [3, 4], [5, 6], [7, 8]]),
+    # 10 / (6 + 4) = 1 again, with a larger eps
+    (10.0, 4.0, [[0, -5], [3, 4], [5, 6], [7, 8]]),
+])
+def test_worked_rowwise_adagrad_eps(lr, eps, expect):
+    # The same row as above (state 11, G = [1, 7]: s = 11 + 25 = 36, sqrt 6),
+    # with eps != 0.  Every step is exact in binary, so eps inside the square
+    # root (sqrt(38) is irrational), eps added to the stored state, or eps
+    # dropped all fail here.
+    t = _t(W4)
+    grad = np.array([[1, 7], [0, 0]], np.float32)
+    state = np.array([11, 5, 0, 0], np.float32)
+    ebo_backward_update([t], np.array([0], np.int64), np.array([0, 1, 1], np.int64), None, "sum", grad,
+                        "rowwise_adagrad", lr=lr, eps=eps, state=state)
+    np.testing.assert_array_equal(t.rows, expect)
+    np.testing.assert_array_equal(state, [36, 5, 0, 0])  # the state holds s, without eps
+
+
+def test_worked_rowwise_adagrad_two_occurrences():
+    # row 1 in bags 0 and 1 (weights 1): G = [1, 3] + [3, 1] = [4, 4],
+    # mean(G^2) = 16; state 20 -> 36, sqrt 6; lr 3, eps 2: step 3/8, so
+    # W1 - 3/8 * [4, 4] = [3 - 1.5, 4 - 1.5]
+    t = _t(W4)
+    grad = np.array([[1, 3], [3, 1]], np.float32)
+    state = np.array([0, 20, 0, 0], np.float32)
+    ebo_backward_update([t], np.array([1, 1], np.int64), np.array([0, 1, 2], np.int64), None, "sum", grad,
+                        "rowwise_adagrad", lr=3.0, eps=2.0, state=state)
+    np.testing.assert_array_equal(t.rows, [[1, 2], [1.5, 2.5], [5, 6], [7, 8]])
+    np.testing.assert_array_equal(state, [0, 36, 0, 0])
+
+
 def test_worked_two_tables_and_fp16():
     w16 = np.array([[1, 2, 3, 4, 5, 6, 7, 8], [0.5] * 8], np.float16)
     t0, t1 = _t(W4), _t(w16, "f16")

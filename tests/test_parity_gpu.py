@@ -8,8 +8,9 @@ and the oracle's error scale s = sum_i |w_i x_i| (divided by L for mean)):
   * and, tighter, the a-priori bound of fp32 summation in any order,
     |g - o| <= (L + 3) * 2^-24 * s' + 2 * 2^-24 * s, where s' = s except for
     unweighted int8 row-wise tables: the kernel sums s*q and the biases c
-    separately (a reassociation), so s' = sum_i (|s_i q_i| + |c_i|), obtained
-    by running the oracle over an fp32 table holding |s| q + |c|.
+    separately (a reassociation), so s' = sum_i (|s_i q_i| + |c_i|), the sum
+    of the oracle's fp64 absolute sums over a table of |s| q and over a table
+    of |c| (both exact in fp32).
 """
 import os
 
@@ -79,31 +80,46 @@ def per_element_lengths(w, bags=None):
     return lens.reshape(-1)[bags][:, None]
 
 
-def split_scale_tables(w, tables):
-    """Oracle tables for the summation-bound scale: unweighted int8 row-wise
-    tables become fp32 tables of |s| q + |c| (others are unchanged)."""
+def int8_parts(rows, D):
+    """Codes [R, D] (uint8), |scale| and |bias| [R, 1] (fp32, exact) of the
+    bytes of an int8 row-wise table in its packed layout (codes, then the
+    fp16 scale and bias of each row)."""
+    sc = np.abs(rows[:, D:D + 2].copy().view(np.float16).astype(np.float32))
+    bi = np.abs(rows[:, D + 2:D + 4].copy().view(np.float16).astype(np.float32))
+    return rows[:, :D], sc, bi
+
+
+def split_scale(w, tables, bags=None):
+    """Scale s' of the summation bound for unweighted int8 row-wise tables,
+    whose kernel sums s*q and the biases c separately:
+    s' = sum_i (|s_i q_i| + |c_i|), the oracle's fp64 absolute sums over a
+    table of |s| q (exact in fp32: an 11-bit by 8-bit product) plus those over
+    a table holding |c| in every column (exact).  Other tables contribute
+    their own |w x| sums.  None when no table of `w` takes the split sum."""
     if w.weights is not None or not any(t.dtype == "int8_rowwise" for t in w.tables):
         return None
-    out = []
+    prods, biases = [], []
     for tb, ot in zip(w.tables, tables):
-        if tb.dtype != "int8_rowwise" or ot.rows is None:
-            out.append(ot)
+        if ot.rows is None:
+            prods.append(ot)
+            biases.append(ot)
             continue
-        D = tb.dim
-        rows = ot.rows
-        sc = np.abs(rows[:, D:D + 2].copy().view(np.float16).astype(np.float32))
-        bi = np.abs(rows[:, D + 2:D + 4].copy().view(np.float16).astype(np.float32))
-        a = rows[:, :D].astype(np.float32) * sc + bi
-        out.append(OracleTable(np.ascontiguousarray(a * np.float32(1.0001)), D, "f32", tb.num_rows))
-    return out
+        R, D = ot.rows.shape[0], tb.dim
+        if tb.dtype != "int8_rowwise":
+            prods.append(ot)
+            biases.append(OracleTable(np.zeros((R, D), np.float32), D, "f32", R))
+            continue
+        q, sc, bi = int8_parts(ot.rows, D)
+        prods.append(OracleTable(np.ascontiguousarray(q.astype(np.float32) * sc), D, "f32", R))
+        biases.append(OracleTable(np.ascontiguousarray(np.broadcast_to(bi, (R, D))), D, "f32", R))
+    return (oracle_forward(w, tables=prods, bags=bags)[1] + oracle_forward(w, tables=biases, bags=bags)[1])
 
 
 def full_check(w, label, stream=None):
     got = run_gpu(w, stream).cpu().numpy()
     tabs = oracle_tables(w)
     ref, asum = oracle_forward(w, tables=tabs)
-    bs_tabs = split_scale_tables(w, tabs)
-    bscale = None if bs_tabs is None else oracle_forward(w, tables=bs_tabs)[1]
+    bscale = split_scale(w, tabs)
     rtol = max(RTOL[t.dtype] for t in w.tables)
     check(got, ref, asum, per_element_lengths(w), rtol, label, bscale)
     return got
@@ -254,8 +270,8 @@ def test_full_size_sampled(dev, name):
     tabs = [OracleTable(tb.rows.cpu().numpy() if t in check_tables else None, tb.dim, tb.dtype, tb.num_rows)
             for t, tb in enumerate(w.tables)]
     ref, asum = oracle_forward(w, tables=tabs, bags=bags)
-    bs_tabs = split_scale_tables(w, tabs)
-    bscale = asum if bs_tabs is None else oracle_forward(w, tables=bs_tabs, bags=bags)[1]
+    bscale = split_scale(w, tabs, bags)
+    bscale = asum if bscale is None else bscale
     g_host = got.cpu().numpy()
     doff = np.concatenate([[0], np.cumsum([tb.dim for tb in w.tables])])
     B = w.batch
@@ -496,6 +512,38 @@ def test_create_refuses_memory_the_gpu_cannot_read(dev):
         assert lib.eb_destroy(h) == eb.EB_OK
     with pytest.raises(ValueError):
         eb.eb_create_tables([(torch.zeros(10, 16), 16, "f32")])
+
+
+def test_create_reports_out_of_memory(dev, monkeypatch):
+    # a cap on the handle's device memory below what it needs: EB_ERR_OOM,
+    # *out set to NULL, nothing leaked; a cap above it: a working handle
+    say("[parity] device allocation refused at create time")
+    import ctypes
+
+    lib = eb.load_library()
+    rows = torch.zeros((10, 16), device=dev)
+
+    def create():
+        arr = (eb.eb_table_desc * 1)(eb.eb_table_desc(rows.data_ptr(), 10, 16, eb.EB_F32, 64))
+        h = ctypes.c_void_p(0xDEAD)  # must be overwritten
+        st = lib.eb_create_tables(arr, 1, None, ctypes.byref(h))
+        return st, h.value
+
+    for cap in ("0", "1", "4096"):
+        monkeypatch.setenv("EB_DEVICE_ALLOC_LIMIT", cap)
+        st, h = create()
+        assert st == eb.EB_ERR_OOM and h is None, (cap, st, h)
+    monkeypatch.setenv("EB_DEVICE_ALLOC_LIMIT", str(1 << 20))
+    st, h = create()
+    assert st == eb.EB_OK and h
+    out = torch.full((1, 16), float("nan"), device=dev)
+    rows.copy_(torch.arange(160, dtype=torch.float32, device=dev).view(10, 16))
+    idx, off = torch.tensor([3], device=dev), torch.tensor([0, 1], device=dev)  # kept alive past the call
+    o, i, f = eb._as_tensor(out), eb._as_tensor(idx), eb._as_tensor(off)
+    assert lib.eb_forward(h, i, f, eb._as_tensor(None), eb.EB_POOL_SUM, o) == eb.EB_OK
+    assert lib.eb_destroy(h) == eb.EB_OK
+    torch.cuda.synchronize()
+    assert torch.equal(out[0], rows[3])
 
 
 def test_checked_mode_reports_bad_data(dev, monkeypatch):
