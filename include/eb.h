@@ -300,6 +300,29 @@ eb_status eb_backward_update(const eb_tables *tables, eb_tensor indices, eb_tens
                              eb_tensor optimizer_state, void *workspace, size_t workspace_bytes);
 
 /*
+ * eb_backward_update for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same computation and arguments without the workspace,
+ * which comes from a static device array of EB_NOALLOC_SCRATCH_BYTES bytes
+ * (128 MiB) that the library holds on every GPU it runs on until the process
+ * ends.  The call allocates nothing and calls no allocating routine.  The
+ * workspace this call needs (eb_backward_workspace_size for its lookup
+ * count) must fit in the array, else EB_ERR_UNSUPPORTED is returned before
+ * anything is enqueued (a batch of about three million lookups into tables
+ * of 128-element rows fits).  Every call on one GPU shares that GPU's
+ * array: calls that overlap on one GPU (several streams, several host
+ * threads) race and must not be issued; calls ordered on one stream are
+ * safe.  No part of the array
+ * must start at zero, so the contents a previous call left behind are
+ * harmless.  EB_ERR_HIP if the array's device address cannot be obtained.
+ */
+#define EB_NOALLOC_SCRATCH_BYTES 134217728
+eb_status eb_backward_update_noalloc(const eb_tables *tables, eb_tensor indices, eb_tensor offsets,
+                                     eb_tensor per_sample_weights, eb_pooling pooling, eb_tensor grad_out,
+                                     int32_t optimizer, float learning_rate, float eps,
+                                     eb_tensor optimizer_state);
+
+/*
  * Release a handle: synchronises its stream, then frees the device array
  * that eb_create_tables allocated and the handle itself (never the tables'
  * rows, which the caller owns).  NULL is a no-op returning EB_OK.  Returns

@@ -32,10 +32,16 @@
 // times per batch) are thereby spread over as many wavefronts as they have
 // tiles, and no wavefront waits for another.
 
+#include <mutex>
+
 #include <rocprim/device/device_radix_sort.hpp>
 #include <rocprim/iterator/counting_iterator.hpp>
 
 #include "eb_device.h"
+
+// The static workspace of eb_backward_update_noalloc (see scratch_address).
+constexpr size_t kScratchBytes = (size_t)EB_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace eb {
 namespace {
@@ -791,6 +797,35 @@ KernelFn pick_tiles(int log2) {
   }
 }
 
+// The workspace of eb_backward_update_noalloc: a static device array, one
+// copy per GPU the library runs on, kept until the process ends.  Host code
+// never uses its name as an address (on the host the name is only a
+// stand-in); it uses the device address that hipGetSymbolAddress returns for
+// the current device, looked up once per device.  No region of the
+// workspace has to start at zero: each is written before it is read, so the
+// contents a previous call left behind do not matter, but two calls that
+// overlap on one GPU share the array and race.
+constexpr size_t kScratchBytes = ::kScratchBytes;
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxScratchDevices];
+
+// Device address of `scratch` on `device`, which must be the current device;
+// nullptr if HIP cannot give it.
+void *scratch_address(int device) {
+  if (device < 0 || device >= kMaxScratchDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[device]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(::scratch)) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_ptr[device] = p;
+  }
+  return g_scratch_ptr[device];
+}
+
 // Workspace regions (each 256-byte aligned).
 struct BwdLayout {
   size_t keys, skeys, spos, bag_of, tile_start, tile_info, carry, sort_tmp, total;
@@ -873,9 +908,17 @@ eb_status eb_backward_workspace_size(const eb_tables *h, int64_t num_indices, si
   return EB_OK;
 }
 
-eb_status eb_backward_update(const eb_tables *h, eb_tensor indices, eb_tensor offsets, eb_tensor per_sample_weights,
-                             eb_pooling pooling, eb_tensor grad_out, int32_t optimizer, float learning_rate,
-                             float eps, eb_tensor optimizer_state, void *workspace, size_t workspace_bytes) {
+}  // extern "C"
+
+namespace eb {
+namespace {
+
+// The backward of eb_backward_update and eb_backward_update_noalloc, with
+// its workspace given: the caller's, or (no_alloc) the library's static
+// array, whose size is checked against what this call needs.
+eb_status backward_update(const eb_tables *h, eb_tensor indices, eb_tensor offsets, eb_tensor per_sample_weights,
+                          eb_pooling pooling, eb_tensor grad_out, int32_t optimizer, float learning_rate, float eps,
+                          eb_tensor optimizer_state, void *workspace, size_t workspace_bytes, bool no_alloc) {
   if (!h) return EB_ERR_INVALID_ARG;
   if (!h->backward_ok) return EB_ERR_UNSUPPORTED;
   if (indices.elem_type != EB_I32 && indices.elem_type != EB_I64) return EB_ERR_DTYPE;
@@ -912,12 +955,25 @@ eb_status eb_backward_update(const eb_tables *h, eb_tensor indices, eb_tensor of
   BwdLayout L;
   eb_status st = layout(h, n, &L);
   if (st != EB_OK) return st;
-  if (n > 0 && (!workspace || workspace_bytes < L.total)) return EB_ERR_INVALID_ARG;
+  if (no_alloc && L.total > kScratchBytes) return EB_ERR_UNSUPPORTED;  // past the static array
   if (n == 0) return EB_OK;  // no row was read: nothing to update
 
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return EB_ERR_HIP;
   if (cur != h->device && hipSetDevice(h->device) != hipSuccess) return EB_ERR_HIP;
+  if (no_alloc) {
+    // the static array's address on the handle's device (now current)
+    workspace = scratch_address(h->device);
+    workspace_bytes = kScratchBytes;
+    if (!workspace) {
+      if (cur != h->device) (void)hipSetDevice(cur);
+      return EB_ERR_HIP;
+    }
+  }
+  if (!workspace || workspace_bytes < L.total) {
+    if (cur != h->device) (void)hipSetDevice(cur);
+    return EB_ERR_INVALID_ARG;
+  }
 
   unsigned char *ws = static_cast<unsigned char *>(workspace);
   BwdArgs a;
@@ -1014,6 +1070,25 @@ eb_status eb_backward_update(const eb_tables *h, eb_tensor indices, eb_tensor of
   if (e != hipSuccess) st = EB_ERR_HIP;
   if (cur != h->device) (void)hipSetDevice(cur);
   return st;
+}
+
+}  // namespace
+}  // namespace eb
+
+extern "C" {
+
+eb_status eb_backward_update(const eb_tables *h, eb_tensor indices, eb_tensor offsets, eb_tensor per_sample_weights,
+                             eb_pooling pooling, eb_tensor grad_out, int32_t optimizer, float learning_rate,
+                             float eps, eb_tensor optimizer_state, void *workspace, size_t workspace_bytes) {
+  return backward_update(h, indices, offsets, per_sample_weights, pooling, grad_out, optimizer, learning_rate, eps,
+                         optimizer_state, workspace, workspace_bytes, false);
+}
+
+eb_status eb_backward_update_noalloc(const eb_tables *h, eb_tensor indices, eb_tensor offsets,
+                                     eb_tensor per_sample_weights, eb_pooling pooling, eb_tensor grad_out,
+                                     int32_t optimizer, float learning_rate, float eps, eb_tensor optimizer_state) {
+  return backward_update(h, indices, offsets, per_sample_weights, pooling, grad_out, optimizer, learning_rate, eps,
+                         optimizer_state, nullptr, 0, true);
 }
 
 }  // extern "C"

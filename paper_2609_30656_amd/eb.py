@@ -40,7 +40,9 @@ TABLE_DTYPES = {"f32": EB_F32, "f16": EB_F16, "int8_rowwise": EB_INT8_ROWWISE}
 POOLING = {"sum": EB_POOL_SUM, "mean": EB_POOL_MEAN}
 OPTIMIZERS = {"sgd": EB_OPT_SGD, "rowwise_adagrad": EB_OPT_ROWWISE_ADAGRAD}
 EXPORTED = ("eb_create_tables", "eb_forward", "eb_forward_seq", "eb_fm_cross", "eb_forward_fm", "eb_destroy",
-            "eb_status_string", "eb_backward_workspace_size", "eb_backward_update")
+            "eb_status_string", "eb_backward_workspace_size", "eb_backward_update", "eb_backward_update_noalloc")
+# bytes of the static workspace of eb_backward_update_noalloc
+EB_NOALLOC_SCRATCH_BYTES = 128 << 20
 
 
 class EBError(RuntimeError):
@@ -96,6 +98,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.eb_backward_update.argtypes = [ctypes.c_void_p, eb_tensor, eb_tensor, eb_tensor, ctypes.c_int, eb_tensor,
                                            ctypes.c_int32, ctypes.c_float, ctypes.c_float, eb_tensor,
                                            ctypes.c_void_p, ctypes.c_size_t]
+        lib.eb_backward_update_noalloc.restype = ctypes.c_int
+        lib.eb_backward_update_noalloc.argtypes = [ctypes.c_void_p, eb_tensor, eb_tensor, eb_tensor, ctypes.c_int,
+                                                   eb_tensor, ctypes.c_int32, ctypes.c_float, ctypes.c_float,
+                                                   eb_tensor]
         _lib = lib
     return _lib
 
@@ -277,3 +283,22 @@ def eb_backward_update(tables: EbTables, indices: torch.Tensor, offsets: torch.T
                                 st_t, workspace.data_ptr(), workspace.numel() * workspace.element_size())
     if st != EB_OK:
         raise EBError(st, "eb_backward_update")
+
+
+def eb_backward_update_noalloc(tables: EbTables, indices: torch.Tensor, offsets: torch.Tensor,
+                               per_sample_weights: Optional[torch.Tensor], pooling, grad_out: torch.Tensor,
+                               optimizer="sgd", learning_rate: float = 0.01, eps: float = 1e-8,
+                               optimizer_state: Optional[torch.Tensor] = None) -> None:
+    """eb_backward_update with the library's static workspace: allocates
+    nothing (EB_ERR_UNSUPPORTED if the batch needs more than
+    EB_NOALLOC_SCRATCH_BYTES of workspace).  Calls that overlap on one GPU
+    race on that workspace."""
+    lib = load_library()
+    d = tables.device
+    args = (_as_tensor(indices, d), _as_tensor(offsets, d), _as_tensor(per_sample_weights, d))
+    g, st_t = _as_tensor(grad_out, d), _as_tensor(optimizer_state, d)
+    mode = POOLING[pooling] if isinstance(pooling, str) else int(pooling)
+    opt = OPTIMIZERS[optimizer] if isinstance(optimizer, str) else int(optimizer)
+    st = lib.eb_backward_update_noalloc(tables.ptr, *args, mode, g, opt, float(learning_rate), float(eps), st_t)
+    if st != EB_OK:
+        raise EBError(st, "eb_backward_update_noalloc")

@@ -35,6 +35,17 @@ def test_exports_match_header(lib):
     assert exported == declared  # nothing else leaks out of the library
 
 
+def test_noalloc_workspace_size_matches_header():
+    m = re.search(r"^#define EB_NOALLOC_SCRATCH_BYTES (\d+)", open(HEADER).read(), re.M)
+    assert m and int(m.group(1)) == eb.EB_NOALLOC_SCRATCH_BYTES == 128 << 20
+
+
+def test_noalloc_rejects_null_handle(lib):
+    none = eb._as_tensor(None)
+    assert lib.eb_backward_update_noalloc(None, none, none, none, 0, none, 0, ctypes.c_float(0.1),
+                                          ctypes.c_float(0.0), none) == eb.EB_ERR_INVALID_ARG
+
+
 def test_status_strings(lib):
     codes = [eb.EB_OK, eb.EB_ERR_INVALID_ARG, eb.EB_ERR_DTYPE, eb.EB_ERR_SHAPE, eb.EB_ERR_UNSUPPORTED,
              eb.EB_ERR_INDEX_OOB, eb.EB_ERR_OFFSETS, eb.EB_ERR_OOM, eb.EB_ERR_HIP]
