@@ -25,7 +25,11 @@
  *   fp16 rows:     the binary16 value, decoded here from its bit fields
  *                  (exact in fp32);
  *   int8 row-wise: D unsigned codes q, then fp16 scale s and fp16 bias c;
- *                  x = fp32(s*q + c) rounded once, i.e. fmaf(s, q, c).
+ *                  x = fp32(s*q + c) rounded once, i.e. fmaf(s, q, c);
+ *   int8 row-wise, split layout: the same values stored apart: row r's D
+ *                  codes at data + r*stride, and the scale/bias words of all
+ *                  rows in one block after the codes, row r's (s, then c) at
+ *                  data + num_rows*stride + 4*r.
  * The paper fixes none of pooling mode, weights, row format or rounding; the
  * readings taken here are the ones listed with the oracle's design notes.
  *
@@ -55,6 +59,7 @@
 #define EBO_ROW_F32 0
 #define EBO_ROW_F16 1
 #define EBO_ROW_U8 2
+#define EBO_ROW_U8_SPLIT 3
 
 #define EBO_IDX_I32 0
 #define EBO_IDX_I64 1
@@ -100,10 +105,15 @@ static float ebo_element(const ebo_table *tb, int64_t r, int32_t d) {
     memcpy(&h, row + 2 * (size_t)d, 2);
     return (float)ebo_half_to_double(h);
   }
-  /* int8 row-wise */
+  /* int8 row-wise: the scale/bias word follows the row's codes, or (split
+     layout) sits in the block after all rows' codes */
+  const unsigned char *word =
+      tb->dtype == EBO_ROW_U8_SPLIT
+          ? (const unsigned char *)tb->data + (size_t)tb->num_rows * (size_t)tb->row_stride_bytes + 4 * (size_t)r
+          : row + tb->dim;
   uint16_t hs, hc;
-  memcpy(&hs, row + tb->dim, 2);
-  memcpy(&hc, row + tb->dim + 2, 2);
+  memcpy(&hs, word, 2);
+  memcpy(&hc, word + 2, 2);
   float s = (float)ebo_half_to_double(hs);
   float c = (float)ebo_half_to_double(hc);
   return fmaf(s, (float)row[d], c);
@@ -165,7 +175,8 @@ int ebo_forward(const ebo_table *tables, int32_t num_tables, const void *indices
   int64_t sum_d = 0;
   for (int32_t t = 0; t < num_tables; ++t) {
     const ebo_table *tb = &tables[t];
-    if (tb->dtype != EBO_ROW_F32 && tb->dtype != EBO_ROW_F16 && tb->dtype != EBO_ROW_U8)
+    if (tb->dtype != EBO_ROW_F32 && tb->dtype != EBO_ROW_F16 && tb->dtype != EBO_ROW_U8 &&
+        tb->dtype != EBO_ROW_U8_SPLIT)
       return EBO_ERR_DTYPE;
     if (tb->dim < 1 || tb->num_rows < 1) return EBO_ERR_INVALID_ARG;
     sum_d += tb->dim;
@@ -540,7 +551,8 @@ int ebo_forward_seq(const ebo_table *tables, int32_t num_tables, const void *ind
   const int64_t nbags = num_offsets - 1;
   for (int32_t t = 0; t < num_tables; ++t) {
     const ebo_table *tb = &tables[t];
-    if (tb->dtype != EBO_ROW_F32 && tb->dtype != EBO_ROW_F16 && tb->dtype != EBO_ROW_U8)
+    if (tb->dtype != EBO_ROW_F32 && tb->dtype != EBO_ROW_F16 && tb->dtype != EBO_ROW_U8 &&
+        tb->dtype != EBO_ROW_U8_SPLIT)
       return EBO_ERR_DTYPE;
     if (tb->dim < 1 || tb->num_rows < 1 || !tb->data) return EBO_ERR_INVALID_ARG;
   }

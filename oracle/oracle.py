@@ -20,7 +20,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "eb_oracle.c")
 _LIB_NAME = "libeb_oracle.so"
 
-_ROW_CODES = {"f32": 0, "f16": 1, "int8_rowwise": 2}
+_ROW_CODES = {"f32": 0, "f16": 1, "int8_rowwise": 2, "int8_rowwise_split": 3}
 _MODE_CODES = {"sum": 0, "mean": 1}
 _ERRORS = {-1: "invalid argument", -2: "dtype", -3: "shape", -5: "index out of range", -6: "bad offsets"}
 
@@ -114,12 +114,53 @@ def _load():
 class OracleTable:
     """Host rows of one table: `rows` is a C-contiguous numpy array whose first
     axis is the row (its byte stride is the row stride), or None when no bag
-    that is asked for reads this table (then num_rows must be given)."""
+    that is asked for reads this table (then num_rows must be given).
+
+    For "int8_rowwise_split" the table is one byte buffer: num_rows rows of
+    codes at row_stride bytes apart, then the rows' 4-byte scale/bias words;
+    `rows` is that whole buffer (any shape, C-contiguous) and num_rows and
+    row_stride must be given."""
 
     rows: Optional[np.ndarray]
     dim: int
     dtype: str
     num_rows: Optional[int] = None
+    row_stride: Optional[int] = None
+
+    @classmethod
+    def of(cls, table, with_rows: bool = True) -> "OracleTable":
+        """The oracle's view of a table object with host_bytes(), dim, dtype,
+        num_rows and row_stride_bytes (the seeded input generator's Table):
+        a host copy of its bytes, or only its shape when with_rows is False."""
+        rows = table.host_bytes() if with_rows else None
+        stride = table.row_stride_bytes if table.dtype == "int8_rowwise_split" else None
+        return cls(rows, table.dim, table.dtype, table.num_rows, stride)
+
+
+def _fill_table(ct, tb: OracleTable, need_rows: bool = False, writable: bool = False):
+    """Marshal one OracleTable into the oracle's C struct."""
+    if tb.rows is None:
+        if need_rows:
+            raise ValueError("this oracle call reads every table's rows")
+        ct.data = None
+        ct.num_rows = int(tb.num_rows)
+        ct.row_stride_bytes = 0
+    else:
+        if not tb.rows.flags["C_CONTIGUOUS"] or (writable and not tb.rows.flags["WRITEABLE"]):
+            raise ValueError("table rows must be C-contiguous" + (" and writable" if writable else ""))
+        ct.data = tb.rows.ctypes.data
+        if tb.dtype == "int8_rowwise_split":
+            if tb.num_rows is None or tb.row_stride is None:
+                raise ValueError("a split int8 table needs num_rows and row_stride")
+            if tb.rows.nbytes < int(tb.num_rows) * (int(tb.row_stride) + 4):
+                raise ValueError("a split int8 table's buffer must hold the codes and the scale/bias block")
+            ct.num_rows = int(tb.num_rows)
+            ct.row_stride_bytes = int(tb.row_stride)
+        else:
+            ct.num_rows = tb.rows.shape[0]
+            ct.row_stride_bytes = tb.rows.strides[0]
+    ct.dim = int(tb.dim)
+    ct.dtype = _ROW_CODES[tb.dtype]
 
 
 def half_to_double(bits: int) -> float:
@@ -159,18 +200,7 @@ def ebo_forward(
         raise TypeError("indices and offsets must share a dtype")
     ct = (_CTable * len(tables))()
     for i, tb in enumerate(tables):
-        if tb.rows is not None:
-            if not tb.rows.flags["C_CONTIGUOUS"]:
-                raise ValueError("table rows must be C-contiguous")
-            ct[i].data = tb.rows.ctypes.data
-            ct[i].num_rows = tb.rows.shape[0]
-            ct[i].row_stride_bytes = tb.rows.strides[0]
-        else:
-            ct[i].data = None
-            ct[i].num_rows = int(tb.num_rows)
-            ct[i].row_stride_bytes = 0
-        ct[i].dim = int(tb.dim)
-        ct[i].dtype = _ROW_CODES[tb.dtype]
+        _fill_table(ct[i], tb)
     T = len(tables)
     nbags = offsets.size - 1
     B = nbags // T if T else 0
@@ -246,17 +276,7 @@ def ebo_backward_update(
     T = len(tables)
     ct = (_CTable * T)()
     for i, tb in enumerate(tables):
-        if tb.rows is not None:
-            if not tb.rows.flags["C_CONTIGUOUS"] or not tb.rows.flags["WRITEABLE"]:
-                raise ValueError("table rows must be C-contiguous and writable")
-            ct[i].data = tb.rows.ctypes.data
-            ct[i].num_rows = tb.rows.shape[0]
-            ct[i].row_stride_bytes = tb.rows.strides[0]
-        else:
-            ct[i].data = None
-            ct[i].num_rows = int(tb.num_rows)
-        ct[i].dim = int(tb.dim)
-        ct[i].dtype = _ROW_CODES[tb.dtype]
+        _fill_table(ct[i], tb, writable=True)
     B = (offsets.size - 1) // T
     lens = [int(offsets[(t + 1) * B] - offsets[t * B]) for t in range(T)]
     reps = (_CReport * T)()
@@ -328,13 +348,7 @@ def ebo_forward_seq(tables: Sequence[OracleTable], indices: np.ndarray, offsets:
     T = len(tables)
     ct = (_CTable * T)()
     for i, tb in enumerate(tables):
-        if not tb.rows.flags["C_CONTIGUOUS"]:
-            raise ValueError("table rows must be C-contiguous")
-        ct[i].data = tb.rows.ctypes.data
-        ct[i].num_rows = tb.rows.shape[0]
-        ct[i].row_stride_bytes = tb.rows.strides[0]
-        ct[i].dim = int(tb.dim)
-        ct[i].dtype = _ROW_CODES[tb.dtype]
+        _fill_table(ct[i], tb, need_rows=True)
     if out_numel is None:
         B = (offsets.size - 1) // T
         out_numel = sum(int(offsets[(t + 1) * B] - offsets[t * B]) * int(tables[t].dim) for t in range(T))

@@ -30,6 +30,12 @@ SEED_ROOT = 2609
 F32 = "f32"
 F16 = "f16"
 INT8_ROWWISE = "int8_rowwise"
+INT8_ROWWISE_SPLIT = "int8_rowwise_split"
+INT8_DTYPES = (INT8_ROWWISE, INT8_ROWWISE_SPLIT)
+# int8 row layouts: "packed" = codes then the fp16 scale and bias in each row
+# (D + 4 bytes); "split" = codes only in the rows, the rows' scale/bias words
+# in one block after them
+INT8_LAYOUTS = {"packed": INT8_ROWWISE, "split": INT8_ROWWISE_SPLIT}
 
 
 @dataclass
@@ -37,12 +43,16 @@ class Table:
     """One embedding table: `rows` is a [R, ...] tensor whose first axis is the row.
 
     For f32/f16 it is [R, D] of that dtype; for int8_rowwise it is [R, stride]
-    uint8 holding D codes, an fp16 scale and an fp16 bias per row.
+    uint8 holding D codes, an fp16 scale and an fp16 bias per row.  For
+    int8_rowwise_split, `storage` is the table's whole byte buffer (R rows of
+    `stride` bytes holding the D codes, then R 4-byte scale/bias words) and
+    `rows` the [R, stride] view of its codes.
     """
 
     rows: torch.Tensor
     dim: int
     dtype: str
+    storage: Optional[torch.Tensor] = None
 
     @property
     def num_rows(self) -> int:
@@ -55,7 +65,21 @@ class Table:
     @property
     def row_bytes(self) -> int:
         """Bytes of one row that a lookup reads (codes + scale/bias for int8)."""
-        return {F32: 4 * self.dim, F16: 2 * self.dim, INT8_ROWWISE: self.dim + 4}[self.dtype]
+        return 4 * self.dim if self.dtype == F32 else (2 * self.dim if self.dtype == F16 else self.dim + 4)
+
+    def host_bytes(self):
+        """A host (numpy) copy of the table's memory: the rows, or for the
+        split int8 layout the whole buffer (codes, then scale/bias block)."""
+        src = self.storage if self.dtype == INT8_ROWWISE_SPLIT else self.rows
+        return src.detach().cpu().numpy()
+
+    def clone(self) -> "Table":
+        """A copy of the table in new memory on the same device."""
+        if self.dtype == INT8_ROWWISE_SPLIT:
+            st = self.storage.clone()
+            R, stride = self.num_rows, self.row_stride_bytes
+            return Table(st[:R * stride].view(R, stride), self.dim, self.dtype, st)
+        return Table(self.rows.clone(), self.dim, self.dtype)
 
 
 @dataclass
@@ -182,6 +206,21 @@ def _values_int8_rowwise(R, D, gen, device, stride):
     return rows
 
 
+def _values_int8_rowwise_split(R, D, gen, device, stride):
+    """The values of _values_int8_rowwise (same draws in the same order), in
+    the split layout: rows of `stride` bytes holding the codes (zero padded),
+    then the rows' (scale, bias) words.  Returns (rows view, storage)."""
+    storage = torch.zeros((R * stride + 4 * R,), dtype=torch.uint8, device=device)
+    rows = storage[:R * stride].view(R, stride)
+    rows[:, :D] = torch.randint(0, 256, (R, D), generator=gen, device=device, dtype=torch.uint8)
+    scale = torch.rand((R,), generator=gen, device=device).mul_(3e-4).add_(1e-4).to(torch.float16)
+    bias = torch.rand((R,), generator=gen, device=device).mul_(0.04).sub_(0.06).to(torch.float16)
+    words = storage[R * stride:].view(R, 4)
+    words[:, 0:2] = scale.view(torch.uint8).view(R, 2)
+    words[:, 2:4] = bias.view(torch.uint8).view(R, 2)
+    return rows, storage
+
+
 # ----------------------------------------------------------------------------
 # bag-length laws (each returns int64 [B] on `device`)
 
@@ -292,6 +331,7 @@ class ConfigSpec:
     weighted: bool
     tables: Callable[[], List[TableSpec]]
     summary: str
+    int8_layout: str = "packed"  # layout of int8 row-wise tables unless make_workload names one
 
 
 def _c1_tables():
@@ -339,8 +379,8 @@ CONFIGS = {
                      "100 fp16 tables D in {32,64,128,256}, rows log-U(1e3,5e6), B=8192, 40 one-hot + 60 "
                      "geometric(mean 30) cap 500, Zipf 1.05, sum"),
     "c5": ConfigSpec("c5", 5, 65536, "sum", False, _c5_tables,
-                     "64 int8-rowwise tables 6Mx128 (132-B rows), B=65536, lognormal(3,1) cap 1000, "
-                     "Zipf 1.05, sum"),
+                     "64 int8-rowwise tables 6Mx128 (u8 codes + fp16 scale/bias per row, 50.7 GB), B=65536, "
+                     "lognormal(3,1) cap 1000, Zipf 1.05, sum"),
 }
 
 
@@ -355,13 +395,16 @@ def make_workload(
     index_dtype=torch.int64,
     index_law: Optional[str] = None,
     tables: Optional[List[Table]] = None,
+    int8_layout: Optional[str] = None,
 ) -> Workload:
     """Draw one batch of config `name`.
 
     rows_cap / batch / num_tables shrink the shape (same laws) for tests that
     the oracle must finish in seconds; index_law="uniform" gives the
     no-reuse control; `tables` reuses tables drawn earlier (a new batch over
-    the same tables: only lengths, indices and weights are drawn).
+    the same tables: only lengths, indices and weights are drawn);
+    int8_layout ("packed" or "split") stores int8 row-wise tables in that
+    layout (default: the config's), with the same values either way.
     """
     cfg = CONFIGS[name]
     device = torch.device(device)
@@ -381,6 +424,14 @@ def make_workload(
             elif s.values == "normal":
                 rows = _values_normal(R, s.dim, gen, device, torch.float32 if s.dtype == F32 else torch.float16)
             else:
+                layout = int8_layout or cfg.int8_layout
+                if layout not in INT8_LAYOUTS:
+                    raise ValueError(f"int8_layout must be one of {sorted(INT8_LAYOUTS)}, got {layout!r}")
+                if layout == "split":
+                    stride = (s.dim + 15) // 16 * 16
+                    rows, storage = _values_int8_rowwise_split(R, s.dim, gen, device, stride)
+                    tables.append(Table(rows, s.dim, INT8_ROWWISE_SPLIT, storage))
+                    continue
                 rows = _values_int8_rowwise(R, s.dim, gen, device, s.stride or s.dim + 4)
             tables.append(Table(rows, s.dim, s.dtype))
     assert len(tables) == len(specs)

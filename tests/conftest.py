@@ -32,7 +32,7 @@ def oracle_tables(workload):
     """Host copies of a workload's tables in the oracle's format."""
     from oracle import OracleTable
 
-    return [OracleTable(t.rows.detach().cpu().numpy(), t.dim, t.dtype) for t in workload.tables]
+    return [OracleTable.of(t) for t in workload.tables]
 
 
 def oracle_forward(workload, tables=None, bags=None, with_absum=True, num_threads=0):

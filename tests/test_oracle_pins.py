@@ -84,6 +84,44 @@ def test_worked_int8_rowwise_dequant():
     np.testing.assert_array_equal(out, [[-1, 126.5], [-1 + 3.5, 126.5 + 4]])
 
 
+def _split_buffer(codes, words, stride, pad=0xAB):
+    """One split-layout int8 table as bytes: row r's codes at r*stride (the
+    bytes after them, up to the stride, set to `pad`), then the rows' 4-byte
+    scale/bias words."""
+    R, D = codes.shape
+    body = np.full((R, stride), pad, np.uint8)
+    body[:, :D] = codes
+    return np.concatenate([body.reshape(-1), np.ascontiguousarray(words, np.uint8).reshape(-1)])
+
+
+def _half_bytes(x):
+    return np.frombuffer(np.float16(x).tobytes(), np.uint8)
+
+
+@pytest.mark.parametrize("stride", [2, 16])
+def test_worked_int8_rowwise_split_dequant(stride):
+    # the rows of the packed case above plus a third, stored apart: codes at
+    # `stride` bytes per row (padding bytes 0xAB, never read), then the
+    # scale/bias words of rows 0, 1, 2 in order
+    codes = np.array([[0, 255], [2, 4], [8, 16]], np.uint8)
+    words = np.stack([np.concatenate([_half_bytes(0.5), _half_bytes(-1.0)]),
+                      np.concatenate([_half_bytes(0.25), _half_bytes(3.0)]),
+                      np.concatenate([_half_bytes(2.0), _half_bytes(0.5)])])
+    t = OracleTable(_split_buffer(codes, words, stride), 2, "int8_rowwise_split", 3, stride)
+    out = ebo_forward([t], np.array([0, 0, 1, 2], np.int64), np.array([0, 1, 3, 4], np.int64))
+    # row 0: 0.5*[0,255] - 1 = [-1, 126.5]; row 1: 0.25*[2,4] + 3 = [3.5, 4];
+    # row 2: 2*[8,16] + 0.5 = [16.5, 32.5]
+    np.testing.assert_array_equal(out, [[-1, 126.5], [-1 + 3.5, 126.5 + 4], [16.5, 32.5]])
+
+
+def test_split_buffer_must_hold_the_scale_bias_block():
+    codes = np.zeros((3, 2), np.uint8)
+    buf = _split_buffer(codes, np.zeros((3, 4), np.uint8), 2)
+    with pytest.raises(ValueError):
+        ebo_forward([OracleTable(buf[:-1], 2, "int8_rowwise_split", 3, 2)], np.array([0], np.int64),
+                    np.array([0, 1], np.int64))
+
+
 def test_worked_f16_rows():
     bits = np.array([[0x3C00, 0xC000], [0x0001, 0x7BFF]], dtype=np.uint16)  # 1, -2, 2^-24, 65504
     t = OracleTable(bits.view(np.float16), 2, "f16")
@@ -118,6 +156,9 @@ def _rand_table(rng, R, D, dtype):
     rows[:, :D] = rng.integers(0, 256, (R, D))
     rows[:, D:D + 2] = rng.uniform(1e-4, 4e-4, R).astype(np.float16).view(np.uint8).reshape(R, 2)
     rows[:, D + 2:] = rng.uniform(-0.06, -0.02, R).astype(np.float16).view(np.uint8).reshape(R, 2)
+    if dtype == "int8_rowwise_split":
+        stride = D + 16
+        return OracleTable(_split_buffer(rows[:, :D], rows[:, D:], stride), D, dtype, R, stride)
     return OracleTable(rows, D, "int8_rowwise")
 
 
@@ -128,6 +169,14 @@ def _decode(t: OracleTable) -> np.ndarray:
     if t.dtype == "f16":
         return t.rows.astype(np.float64)
     D = t.dim
+    if t.dtype == "int8_rowwise_split":
+        R, st = t.num_rows, t.row_stride
+        buf = t.rows.reshape(-1)
+        q = buf[:R * st].reshape(R, st)[:, :D].astype(np.float64)
+        words = buf[R * st:R * st + 4 * R].reshape(R, 4)
+        s = words[:, 0:2].copy().view(np.float16).astype(np.float64)
+        c = words[:, 2:4].copy().view(np.float16).astype(np.float64)
+        return (s * q + c).astype(np.float32).astype(np.float64)
     q = t.rows[:, :D].astype(np.float64)
     s = t.rows[:, D:D + 2].copy().view(np.float16).astype(np.float64)
     c = t.rows[:, D + 2:D + 4].copy().view(np.float16).astype(np.float64)
@@ -135,7 +184,26 @@ def _decode(t: OracleTable) -> np.ndarray:
     return (s * q + c).astype(np.float32).astype(np.float64)
 
 
-DTYPES = ["f32", "f16", "int8_rowwise"]
+DTYPES = ["f32", "f16", "int8_rowwise", "int8_rowwise_split"]
+
+
+@pytest.mark.parametrize("mode", ["sum", "mean", "weighted"])
+def test_split_layout_equals_packed_layout(mode):
+    # the same codes, scales and biases stored packed (132-byte rows) and
+    # split (codes apart from the scale/bias block) pool to the same bits
+    rng = np.random.default_rng(19)
+    R, D = 300, 128
+    packed = _rand_table(rng, R, D, "int8_rowwise")
+    split = OracleTable(_split_buffer(packed.rows[:, :D], packed.rows[:, D:], 128), D, "int8_rowwise_split", R,
+                        128)
+    lens = rng.integers(0, 50, 64)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    idx = rng.integers(0, R, off[-1]).astype(np.int64)
+    w = rng.uniform(0, 1, off[-1]).astype(np.float32) if mode == "weighted" else None
+    pool = "mean" if mode == "mean" else "sum"
+    a = ebo_forward([packed], idx, off, w, pool)
+    b = ebo_forward([split], idx, off, w, pool)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
