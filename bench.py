@@ -93,7 +93,7 @@ def run_cpu_baseline_seq(w, budget_s: float, host_bytes_cap: float = 3e9, thread
     B = w.batch
     off = w.offsets[:use * B + 1].cpu().numpy()
     idx = w.indices[:int(off[-1])].cpu().numpy()
-    tabs = [oracle.OracleTable(t.rows.cpu().numpy(), t.dim, t.dtype) for t in w.tables[:use]]
+    tabs = [oracle.OracleTable.of(t) for t in w.tables[:use]]
     esz = w.indices.element_size()
     look = int(off[-1])
     nbytes = (use + 1) * esz + sum(int(off[(t + 1) * B] - off[t * B]) * (w.tables[t].row_bytes + esz + 4 * w.tables[t].dim)
@@ -129,8 +129,7 @@ def run_cpu_baseline(w, budget_s: float, host_bytes_cap: float = 3e9, fm: bool =
             break
         acc += nbytes
         use += 1
-    tabs = [oracle.OracleTable(t.rows.cpu().numpy() if i < use else None, t.dim, t.dtype, t.num_rows)
-            for i, t in enumerate(w.tables)]
+    tabs = [oracle.OracleTable.of(t, with_rows=i < use) for i, t in enumerate(w.tables)]
     idx = w.indices.cpu().numpy()
     off = w.offsets.cpu().numpy()
     wt = None if w.weights is None else w.weights.cpu().numpy()
@@ -170,6 +169,8 @@ def main():
     ap.add_argument("--cold-reps", type=int, default=15,
                     help="after the timed loop, time this many calls each preceded (outside the events) by a "
                          "1 GiB read that evicts L2 and the Infinity Cache (0 = skip)")
+    ap.add_argument("--int8-layout", default=None, choices=["packed", "split"],
+                    help="layout of int8 row-wise tables (default: the workload's)")
     ap.add_argument("--uniform-steps", type=int, default=-1,
                     help="forward mode with Zipf indices: time this many steps over the same tables with uniform "
                          "indices (the no-reuse control; -1: min(steps, 20); 0 = skip)")
@@ -195,9 +196,13 @@ def main():
     torch.cuda.set_device(dev)
     lib = eb.load_library()
     law = None if args.index_law == "zipf" else "uniform"
+    # the workload's name in profile summaries: the config, plus the int8
+    # layout when it is not the config's own
+    cfg_key = args.config if args.int8_layout in (None, CONFIGS[args.config].int8_layout) else \
+        f"{args.config}-{args.int8_layout}"
 
     print(f"[bench] generating {args.config} ({CONFIGS[args.config].summary})", file=sys.stderr, flush=True)
-    batches = [make_workload(args.config, dev, batch_seed=0, index_law=law)]
+    batches = [make_workload(args.config, dev, batch_seed=0, index_law=law, int8_layout=args.int8_layout)]
     for s in (1, 2):
         batches.append(make_workload(args.config, dev, batch_seed=s, index_law=law, tables=batches[0].tables))
     w0 = batches[0]
@@ -365,7 +370,7 @@ def main():
         torch.cuda.synchronize()
         u_ms = r0.elapsed_time(r1) / n_uni
         u_bytes = wu.algorithmic_bytes()
-        u_traffic = counter_traffic(args.config, "uniform", "forward")
+        u_traffic = counter_traffic(cfg_key, "uniform", "forward")
         uniform = {"index_law": "uniform", "steps": n_uni, "kernel_ms_avg": round(u_ms, 5),
                    "lookups": wu.num_indices, "algorithmic_bytes": u_bytes,
                    "achieved": round(u_bytes / (u_ms * 1e-3) / 1e9, 2),
@@ -380,7 +385,7 @@ def main():
     look_total = sum(nlook[k % 3] for k in range(args.steps))
     value = bytes_total / wall / 1e9
     achieved = kern_bytes / kern_avg_s / 1e9
-    traffic = counter_traffic(args.config, args.index_law, args.mode) if args.mode in ("forward", "seq") else None
+    traffic = counter_traffic(cfg_key, args.index_law, args.mode) if args.mode in ("forward", "seq") else None
 
     fm_pass = None
     if args.mode == "fm":
@@ -445,7 +450,7 @@ def main():
     dtypes = sorted({t.dtype for t in w0.tables})
     # what the path computes in: the stored values (u8 codes with fp16 scale
     # and bias, fp16 or fp32) widened or dequantised to fp32, summed in fp32
-    path_dtype = "+".join({"f32": "f32", "f16": "f16->f32", "int8_rowwise": "u8->f32"}[d] for d in dtypes)
+    path_dtype = "+".join(sorted({{"f32": "f32", "f16": "f16->f32"}.get(d, "u8->f32") for d in dtypes}))
     fabric_gbs = None if traffic is None else traffic / kern_avg_s / 1e9
     line = {
         "metric": {"forward": METRIC, "fm": METRIC_FM, "seq": METRIC_SEQ, "backward": METRIC_BACKWARD}[args.mode],
@@ -476,6 +481,10 @@ def main():
             "algorithmic_bytes_per_step": round(sum(algo) / 3),
             "index_dtype": str(w0.indices.dtype).replace("torch.", ""),
             "table_storage": dtypes,
+            "int8_layout": ({"int8_rowwise": "packed (codes, scale, bias in each row)",
+                             "int8_rowwise_split": "split (codes in the rows, scale/bias block after them)"}
+                            .get(dtypes[0]) if len(dtypes) == 1 else None),
+            "row_stride_bytes": sorted({t.row_stride_bytes for t in w0.tables}),
         },
         "mode": args.mode,
         "roofline": {

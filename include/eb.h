@@ -108,8 +108,21 @@ typedef enum {
  *                    byte D and an fp16 bias c at byte D+2 (little endian);
  *                    x[d] = fp32(s*q[d] + c) rounded once (s*q is exact in
  *                    fp32, so this equals fmaf(s, q, c)).
+ *   EB_INT8_ROWWISE_SPLIT: the same values with the scale and bias stored
+ *                    apart from the codes: row r holds its D codes only, and
+ *                    the rows' 4-byte (fp16 s, fp16 c) words follow all the
+ *                    rows as one block, row r's at
+ *                    data + num_rows*row_stride_bytes + 4*r.  The table spans
+ *                    num_rows*(row_stride_bytes + 4) bytes.  With D = 128 at a
+ *                    128-byte stride each row's codes fill one 128-byte line,
+ *                    where the packed 132-byte row always touches two; the
+ *                    scale/bias block (4 bytes per row) is small enough to
+ *                    stay in the GPU's caches while its table is in use.
+ * The int8 layouts store the per-row affine (scale, bias) quantisation whose
+ * tables make up the single-GPU share of a sharded model (Sec. III-B.1
+ * shrinks tables to fit one GPU); the paper fixes no format.
  */
-typedef enum { EB_F32 = 0, EB_F16 = 1, EB_INT8_ROWWISE = 2 } eb_table_dtype;
+typedef enum { EB_F32 = 0, EB_F16 = 1, EB_INT8_ROWWISE = 2, EB_INT8_ROWWISE_SPLIT = 3 } eb_table_dtype;
 
 /* Element type of an eb_tensor. */
 typedef enum { EB_I32 = 0, EB_I64 = 1, EB_T_F32 = 2 } eb_elem_type;
@@ -126,7 +139,10 @@ typedef enum { EB_POOL_SUM = 0, EB_POOL_MEAN = 1 } eb_pooling;
  *                    row_stride_bytes multiples of 16;
  *   EB_INT8_ROWWISE: dim % 16 == 0, row_stride_bytes >= dim+4, data and
  *                    row_stride_bytes multiples of 4 (dim=128 packs rows at
- *                    132 bytes).
+ *                    132 bytes);
+ *   EB_INT8_ROWWISE_SPLIT: dim % 16 == 0, row_stride_bytes >= dim, data and
+ *                    row_stride_bytes multiples of 16 (dim=128 at 128 bytes),
+ *                    and the scale/bias block after the rows readable too.
  *   dim <= 8192.  Any other value gives EB_ERR_INVALID_ARG, an unknown dtype
  *   EB_ERR_DTYPE, a dim or alignment the kernels cannot take
  *   EB_ERR_UNSUPPORTED.

@@ -53,6 +53,11 @@ enum : int32_t { kF32 = 0, kF16 = 1, kU8 = 2 };
 struct TableMeta {
   const unsigned char *data;
   int64_t state_base;   // first optimizer-state slot: rows of the earlier tables
+  // int8 row-wise tables: row r's 4-byte scale/bias word is at
+  // sb_base + r * sb_stride (packed rows: data + dim and the row stride;
+  // split layout: the block after all rows' codes, 4 bytes per row)
+  const unsigned char *sb_base;
+  uint32_t sb_stride;
   uint32_t row_stride;  // bytes
   int32_t num_rows;
   int32_t dim;
@@ -133,6 +138,11 @@ __device__ __forceinline__ void accumulate(float (&acc)[Vals<DT>::n], float &cb,
       }
     }
   }
+}
+
+// Row `row`'s scale/bias word of an int8 row-wise table (see TableMeta).
+__device__ __forceinline__ gbyte *sb_word(const TableMeta &m, uint32_t row) {
+  return (gbyte *)m.sb_base + (uint64_t)row * m.sb_stride;
 }
 
 template <int DT>
@@ -290,7 +300,7 @@ __device__ __forceinline__ void gather_steps(const TableMeta &m, const GatherCtx
     const bool ok = (r < k.n) && (row != kBadRow) && colok;
     gbyte *p = ok ? (gbyte *)m.data + (uint64_t)row * m.row_stride : (gbyte *)a.zero;
     v[u] = load_slice<DT>(p + colb);
-    if constexpr (DT == kU8) sb[u] = *reinterpret_cast<const EB_GLOBAL uint32_t *>(p + m.dim);
+    if constexpr (DT == kU8) sb[u] = *reinterpret_cast<const EB_GLOBAL uint32_t *>(ok ? sb_word(m, row) : p);
     else sb[u] = 0u;
     if constexpr (!W) w[u] = 1.0f;
   }

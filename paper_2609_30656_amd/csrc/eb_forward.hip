@@ -632,6 +632,8 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
       esize = 2; align = 16; dim_mult = 8;
     } else if (d.dtype == EB_INT8_ROWWISE) {
       esize = 1; align = 4; dim_mult = 16;
+    } else if (d.dtype == EB_INT8_ROWWISE_SPLIT) {
+      esize = 1; align = 16; dim_mult = 16;
     } else {
       st = EB_ERR_DTYPE;
       break;
@@ -652,7 +654,17 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
       m.dim = d.dim;
       m.code_bytes = (int32_t)code_bytes;
       m.out_col = (int32_t)col;
-      m.kind = d.dtype * 8 + log2_lanes_per_row((int)code_bytes);
+      // both int8 row-wise layouts run the int8 kernels; they differ only in
+      // where a row's scale/bias word is
+      const int kernel_dt = d.dtype == EB_INT8_ROWWISE_SPLIT ? kU8 : d.dtype;
+      m.kind = kernel_dt * 8 + log2_lanes_per_row((int)code_bytes);
+      if (d.dtype == EB_INT8_ROWWISE_SPLIT) {
+        m.sb_base = m.data + (size_t)d.num_rows * (size_t)d.row_stride_bytes;
+        m.sb_stride = 4;
+      } else {
+        m.sb_base = m.data + code_bytes;
+        m.sb_stride = m.row_stride;
+      }
       m.passes = (int32_t)((code_bytes + kPassBytes - 1) / kPassBytes);
       m.state_base = rows_before;
       m.key_base = (uint32_t)(key_before <= UINT32_MAX ? key_before : 0);

@@ -132,7 +132,7 @@ __device__ __forceinline__ void copy_steps(const SeqArgs &a, const TableMeta &m,
         v[u][j] = *reinterpret_cast<const EB_GLOBAL uint32_t *>(q);
       }
     }
-    if constexpr (DT == kU8) sb[u] = *reinterpret_cast<const EB_GLOBAL uint32_t *>(p + m.dim);
+    if constexpr (DT == kU8) sb[u] = *reinterpret_cast<const EB_GLOBAL uint32_t *>(ok ? sb_word(m, row) : p);
     else sb[u] = 0u;
   }
 #pragma unroll

@@ -28,7 +28,7 @@ EB_ERR_OFFSETS = -6
 EB_ERR_OOM = -7
 EB_ERR_HIP = -8
 # eb_table_dtype
-EB_F32, EB_F16, EB_INT8_ROWWISE = 0, 1, 2
+EB_F32, EB_F16, EB_INT8_ROWWISE, EB_INT8_ROWWISE_SPLIT = 0, 1, 2, 3
 # eb_elem_type
 EB_I32, EB_I64, EB_T_F32 = 0, 1, 2
 # eb_pooling
@@ -36,7 +36,8 @@ EB_POOL_SUM, EB_POOL_MEAN = 0, 1
 # eb_optimizer
 EB_OPT_SGD, EB_OPT_ROWWISE_ADAGRAD = 0, 1
 
-TABLE_DTYPES = {"f32": EB_F32, "f16": EB_F16, "int8_rowwise": EB_INT8_ROWWISE}
+TABLE_DTYPES = {"f32": EB_F32, "f16": EB_F16, "int8_rowwise": EB_INT8_ROWWISE,
+                "int8_rowwise_split": EB_INT8_ROWWISE_SPLIT}
 POOLING = {"sum": EB_POOL_SUM, "mean": EB_POOL_MEAN}
 OPTIMIZERS = {"sgd": EB_OPT_SGD, "rowwise_adagrad": EB_OPT_ROWWISE_ADAGRAD}
 EXPORTED = ("eb_create_tables", "eb_forward", "eb_forward_seq", "eb_fm_cross", "eb_forward_fm", "eb_destroy",
@@ -150,7 +151,9 @@ def _stream_handle(stream) -> Optional[int]:
 
 def eb_create_tables(tables: Sequence, stream=None) -> EbTables:
     """tables: objects with .rows (device tensor, first axis = row), .dim and
-    .dtype ("f32" | "f16" | "int8_rowwise"), or (rows, dim, dtype) tuples.
+    .dtype ("f32" | "f16" | "int8_rowwise" | "int8_rowwise_split"), or
+    (rows, dim, dtype) tuples.  A split int8 table's rows view the codes of
+    an allocation whose scale/bias block follows them.
     stream: torch.cuda.Stream, raw hipStream_t as int, or None (null stream)."""
     lib = load_library()
     norm = []
@@ -167,6 +170,14 @@ def eb_create_tables(tables: Sequence, stream=None) -> EbTables:
         descs[i].dim = dim
         descs[i].dtype = TABLE_DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
         descs[i].row_stride_bytes = rows.stride(0) * rows.element_size()
+        if descs[i].dtype == EB_INT8_ROWWISE_SPLIT:
+            # the kernels read the scale/bias block after the rows' codes:
+            # it must lie inside the memory that `rows` views
+            need = rows.shape[0] * (descs[i].row_stride_bytes + 4)
+            have = rows.untyped_storage().nbytes() - rows.storage_offset() * rows.element_size()
+            if have < need:
+                raise ValueError(f"a split int8 table needs {need} bytes from its first row (codes, then the "
+                                 f"scale/bias block), its storage holds {have}")
     out = ctypes.c_void_p()
     st = lib.eb_create_tables(descs, len(norm), _stream_handle(stream), ctypes.byref(out))
     if st != EB_OK:

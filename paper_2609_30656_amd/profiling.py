@@ -86,8 +86,14 @@ def counter_traffic(config: str, law: str, mode: str):
 
 
 def _bench_args(mode, config, law, steps, warmup, calib):
-    a = [sys.executable, os.path.join(ROOT, "bench.py"), "--mode", mode, "--config", config, "--index-law", law,
-         "--steps", str(steps), "--warmup", str(warmup), "--cpu-budget", "0"]
+    """bench.py's arguments for one profiled run of workload `config` (a
+    config name, or config-layout for int8 tables in a layout other than the
+    config's own); only the main loop's kernel runs (no uniform control)."""
+    cfg, _, layout = config.partition("-")
+    a = [sys.executable, os.path.join(ROOT, "bench.py"), "--mode", mode, "--config", cfg, "--index-law", law,
+         "--steps", str(steps), "--warmup", str(warmup), "--cpu-budget", "0", "--uniform-steps", "0"]
+    if layout:
+        a += ["--int8-layout", layout]
     return a + (["--copy-calibration"] if calib else [])
 
 
@@ -116,7 +122,8 @@ def _match(name, kernel):
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--mode", default="forward", choices=sorted(KERNELS))
-    ap.add_argument("--config", default="c5")
+    ap.add_argument("--config", default="c5",
+                    help="workload (c1 c2 c3a c3b c4 c5), or c5-packed / c5-split for an int8 layout")
     ap.add_argument("--index-law", default="zipf", choices=["zipf", "uniform"])
     ap.add_argument("--work", default="/tmp/eb_profiling", help="scratch directory for rocprofv3 output")
     ap.add_argument("--limit", type=int, default=300, help="seconds allowed per rocprofv3 run")

@@ -35,7 +35,7 @@ PEAK_FP32_TFLOPS = 157.3
 
 
 def _flops_per_element(tb, weighted):
-    if tb.dtype == "int8_rowwise":
+    if tb.dtype.startswith("int8_rowwise"):
         return 4 if weighted else 2  # dequantising fma (+ the weight's fma)
     return 2 if weighted else 1
 
@@ -56,7 +56,7 @@ def seq_flops(w):
     off = w.offsets.cpu()
     B = w.batch
     return sum(int(off[(t + 1) * B] - off[t * B]) * tb.dim * 2
-               for t, tb in enumerate(w.tables) if tb.dtype == "int8_rowwise")
+               for t, tb in enumerate(w.tables) if tb.dtype.startswith("int8_rowwise"))
 
 
 def fm_bytes_flops(w):

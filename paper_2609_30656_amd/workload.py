@@ -378,9 +378,11 @@ CONFIGS = {
     "c4": ConfigSpec("c4", 4, 8192, "sum", False, _c4_tables,
                      "100 fp16 tables D in {32,64,128,256}, rows log-U(1e3,5e6), B=8192, 40 one-hot + 60 "
                      "geometric(mean 30) cap 500, Zipf 1.05, sum"),
+    # int8 rows in the split layout by default: on MI355X it was 3% faster than
+    # the packed 132-byte rows under Zipf indices and 8% under uniform ones
     "c5": ConfigSpec("c5", 5, 65536, "sum", False, _c5_tables,
                      "64 int8-rowwise tables 6Mx128 (u8 codes + fp16 scale/bias per row, 50.7 GB), B=65536, "
-                     "lognormal(3,1) cap 1000, Zipf 1.05, sum"),
+                     "lognormal(3,1) cap 1000, Zipf 1.05, sum", int8_layout="split"),
 }
 
 

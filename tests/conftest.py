@@ -35,6 +35,24 @@ def oracle_tables(workload):
     return [OracleTable.of(t) for t in workload.tables]
 
 
+def compact_oracle_table(tb, rows):
+    """An OracleTable holding only rows `rows` (in that order, renumbered
+    0..len-1) of a workload Table, in the table's own layout.  Data movement
+    only."""
+    import torch
+    from oracle import OracleTable
+
+    rows = np.asarray(rows, np.int64)
+    sel = torch.from_numpy(rows if rows.size else np.zeros(1, np.int64)).to(tb.rows.device)
+    if tb.dtype == "int8_rowwise_split":
+        R, st = tb.num_rows, tb.row_stride_bytes
+        codes = tb.rows.index_select(0, sel)
+        words = tb.storage[R * st:R * st + 4 * R].view(R, 4).index_select(0, sel)
+        buf = torch.cat([codes.reshape(-1), words.reshape(-1)]).cpu().numpy()
+        return OracleTable(buf, tb.dim, tb.dtype, int(sel.numel()), st)
+    return OracleTable(np.ascontiguousarray(tb.rows.index_select(0, sel).cpu().numpy()), tb.dim, tb.dtype)
+
+
 def oracle_forward(workload, tables=None, bags=None, with_absum=True, num_threads=0):
     from oracle import ebo_forward
 

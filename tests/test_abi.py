@@ -68,8 +68,8 @@ def _create(lib, descs, n=None, out=True):
 
 def _desc(data=_ALIGNED, rows=10, dim=16, dtype=eb.EB_F32, stride=None):
     if stride is None:
-        stride = dim * {eb.EB_F32: 4, eb.EB_F16: 2, eb.EB_INT8_ROWWISE: 1}.get(dtype, 4) + (
-            4 if dtype == eb.EB_INT8_ROWWISE else 0)
+        stride = dim * {eb.EB_F32: 4, eb.EB_F16: 2, eb.EB_INT8_ROWWISE: 1, eb.EB_INT8_ROWWISE_SPLIT: 1}.get(
+            dtype, 4) + (4 if dtype == eb.EB_INT8_ROWWISE else 0)
     return eb.eb_table_desc(data, rows, dim, dtype, stride)
 
 
@@ -89,6 +89,11 @@ def _desc(data=_ALIGNED, rows=10, dim=16, dtype=eb.EB_F32, stride=None):
     (dict(dim=128, dtype=eb.EB_INT8_ROWWISE, stride=130), eb.EB_ERR_INVALID_ARG),
     (dict(dim=128, dtype=eb.EB_INT8_ROWWISE, stride=134), eb.EB_ERR_UNSUPPORTED),
     (dict(dim=128, dtype=eb.EB_INT8_ROWWISE, data=_ALIGNED + 2), eb.EB_ERR_UNSUPPORTED),
+    (dict(dim=24, dtype=eb.EB_INT8_ROWWISE_SPLIT), eb.EB_ERR_UNSUPPORTED),  # split int8: dim % 16
+    (dict(dim=128, dtype=eb.EB_INT8_ROWWISE_SPLIT, stride=112), eb.EB_ERR_INVALID_ARG),  # shorter than the codes
+    (dict(dim=128, dtype=eb.EB_INT8_ROWWISE_SPLIT, stride=132), eb.EB_ERR_UNSUPPORTED),  # stride % 16
+    (dict(dim=128, dtype=eb.EB_INT8_ROWWISE_SPLIT, data=_ALIGNED + 4), eb.EB_ERR_UNSUPPORTED),  # 16-B aligned
+    (dict(dtype=4), eb.EB_ERR_DTYPE),
 ])
 def test_create_rejects_bad_descriptors(lib, desc, expect):
     st, h = _create(lib, [_desc(), _desc(**desc)])
@@ -115,7 +120,8 @@ def test_valid_descriptors_without_a_device_report_hip_error(lib):
 
     if torch.cuda.is_available():
         pytest.skip("a device is present")
-    st, h = _create(lib, [_desc(), _desc(dim=128, dtype=eb.EB_INT8_ROWWISE)])
+    st, h = _create(lib, [_desc(), _desc(dim=128, dtype=eb.EB_INT8_ROWWISE),
+                          _desc(dim=128, dtype=eb.EB_INT8_ROWWISE_SPLIT)])
     assert st == eb.EB_ERR_HIP and h is None
 
 

@@ -19,6 +19,7 @@ import numpy as np
 import pytest
 import torch
 
+from conftest import compact_oracle_table
 from oracle import OracleTable, ebo_fm, ebo_forward
 from paper_2609_30656_amd import eb
 from paper_2609_30656_amd.workload import make_workload
@@ -70,9 +71,7 @@ def sub_workload(w, examples):
         spans = [(off[t * B + b], off[t * B + b + 1]) for b in examples]
         pos = np.concatenate([np.arange(lo, hi) for lo, hi in spans]) if spans else np.zeros(0, np.int64)
         rows, inv = np.unique(idx[pos], return_inverse=True)
-        sel = torch.from_numpy(rows if rows.size else np.zeros(1, np.int64)).to(tb.rows.device)
-        host = tb.rows.index_select(0, sel).cpu().numpy()
-        tabs.append(OracleTable(np.ascontiguousarray(host), tb.dim, tb.dtype))
+        tabs.append(compact_oracle_table(tb, rows))
         new_idx.append(inv.astype(np.int64))
         if wts is not None:
             new_w.append(wts[pos])
@@ -181,7 +180,8 @@ def test_fm_pass_argument_errors(dev):
 
 FM_WIDTHS = [("f32", 4), ("f32", 12), ("f32", 64), ("f32", 256), ("f32", 260), ("f32", 1028),
              ("f16", 8), ("f16", 24), ("f16", 128), ("f16", 520),
-             ("int8_rowwise", 16), ("int8_rowwise", 48), ("int8_rowwise", 128), ("int8_rowwise", 2064)]
+             ("int8_rowwise", 16), ("int8_rowwise", 48), ("int8_rowwise", 128), ("int8_rowwise", 2064),
+             ("int8_rowwise_split", 128), ("int8_rowwise_split", 2064)]
 
 
 @pytest.mark.parametrize("mode", ["sum", "mean", "weighted"])
@@ -234,10 +234,11 @@ def test_full_c2_every_example(dev):
     full_fm_check(make_workload("c2", dev), "full c2")
 
 
-@pytest.mark.parametrize("name", ["c3a", "c3b", "c5"])
+@pytest.mark.parametrize("name", ["c3a", "c3b", "c5", "c5-packed"])
 def test_full_size_sampled(dev, name):
     say(f"[fm] full {name}: generating")
-    w = make_workload(name, dev)
+    name, _, layout = name.partition("-")
+    w = make_workload(name, dev, int8_layout=layout or None)
     say(f"[fm] full {name}: {w.num_indices} lookups; forward_fm")
     out, fm, ref = run_fm(w)
     assert torch.equal(out.view(torch.int32), ref.view(torch.int32))

@@ -7,7 +7,10 @@ Two tables:
     on start at or past 2^32;
   * int8 row-wise, D = 128 at the packed 132-byte stride, 32.6 M rows
     (4.30 GB): row 32,537,631 straddles 2^32 (its codes before, its scale
-    and bias after).
+    and bias after);
+  * int8 row-wise in the split layout, D = 128 at a 128-byte stride, 33.6 M
+    rows (4.43 GB): rows from 33,554,432 on start at or past 2^32, and the
+    whole scale/bias block lies past it.
 Indices concentrate on the rows past the boundary, with the straddling row,
 the last row and some low rows mixed in.  For the lookups the oracle runs on
 the referenced rows only (a compact host copy with the indices renumbered
@@ -18,18 +21,21 @@ import numpy as np
 import pytest
 import torch
 
+from conftest import compact_oracle_table
 from oracle import OracleTable, ebo_forward, ebo_forward_seq
 from paper_2609_30656_amd import eb
 from paper_2609_30656_amd.workload import Workload
 from test_backward_gpu import run_and_check
-from test_parity_gpu import RTOL, _table, check, int8_parts, per_element_lengths
+from test_parity_gpu import RTOL, _table, check, int8_parts, is_int8, per_element_lengths
 
 pytestmark = pytest.mark.gpu
 
 R_F32 = 8_500_000
 R_U8 = 32_600_000
+R_U8S = 33_600_000
 FIRST_HIGH_F32 = 2 ** 32 // 512  # first fp32 row at or past 2^32
 STRADDLE_U8 = 2 ** 32 // 132     # the int8 row that straddles 2^32
+FIRST_HIGH_U8S = 2 ** 32 // 128  # first split-layout int8 row at or past 2^32
 B = 384
 
 
@@ -49,9 +55,11 @@ def dev():
 
 @pytest.fixture(scope="module")
 def tables(dev):
-    say(f"[large] generating tables: f32 {R_F32} x 128, int8 {R_U8} x 128 (stride 132)")
-    t = [_table(dev, "f32", R_F32, 128, seed=41), _table(dev, "int8_rowwise", R_U8, 128, seed=42)]
-    assert t[0].rows.numel() * 4 > 2 ** 32 and t[1].rows.numel() > 2 ** 32
+    say(f"[large] generating tables: f32 {R_F32} x 128, int8 {R_U8} x 128 (stride 132), "
+        f"split int8 {R_U8S} x 128 (stride 128)")
+    t = [_table(dev, "f32", R_F32, 128, seed=41), _table(dev, "int8_rowwise", R_U8, 128, seed=42),
+         _table(dev, "int8_rowwise_split", R_U8S, 128, seed=43)]
+    assert t[0].rows.numel() * 4 > 2 ** 32 and t[1].rows.numel() > 2 ** 32 and t[2].rows.numel() > 2 ** 32
     assert 132 * STRADDLE_U8 < 2 ** 32 < 132 * (STRADDLE_U8 + 1)
     yield t
     del t
@@ -79,9 +87,11 @@ def _workload(dev, tables, weighted=False, pooling="sum", seed=0):
         R = tb.num_rows
         if tb.dtype == "f32":
             special = [FIRST_HIGH_F32, FIRST_HIGH_F32 - 1, R - 1, 0]
-        else:
+        elif tb.dtype == "int8_rowwise":
             special = [STRADDLE_U8, STRADDLE_U8 - 1, STRADDLE_U8 + 1, R - 1]
-        first_high = FIRST_HIGH_F32 if tb.dtype == "f32" else STRADDLE_U8
+        else:
+            special = [FIRST_HIGH_U8S, FIRST_HIGH_U8S - 1, R - 1, 0]
+        first_high = {"f32": FIRST_HIGH_F32, "int8_rowwise": STRADDLE_U8}.get(tb.dtype, FIRST_HIGH_U8S)
         idx.append(_indices(R, first_high, np.array(special), int(L.sum()), rng))
     lengths = torch.tensor(np.concatenate(lens), dtype=torch.int64)
     offsets = torch.zeros(lengths.numel() + 1, dtype=torch.int64)
@@ -102,8 +112,7 @@ def _compact(w):
     for t, tb in enumerate(w.tables):
         lo, hi = int(off[t * w.batch]), int(off[(t + 1) * w.batch])
         u, inv = np.unique(idx[lo:hi], return_inverse=True)
-        rows = tb.rows[torch.from_numpy(u).to(tb.rows.device)].cpu().numpy()
-        tabs.append(OracleTable(np.ascontiguousarray(rows), tb.dim, tb.dtype))
+        tabs.append(compact_oracle_table(tb, u))
         new[lo:hi] = inv
     return tabs, new, off
 
@@ -119,24 +128,28 @@ def test_pooled_lookup_past_4gib(dev, tables, mode):
     tabs, idx, off = _compact(w)
     wts = None if w.weights is None else w.weights.cpu().numpy()
     ref, asum = ebo_forward(tabs, idx, off, wts, w.pooling, with_absum=True)
-    # int8 rows sum s*q and the biases separately when unweighted: the bound
-    # scale then is sum(|s q| + |c|), which the rtol bar below already covers
     got = out.cpu().numpy()
     L = per_element_lengths(w)
-    check(got[:, :128], ref[:, :128], asum[:, :128], L[:, :128], RTOL["f32"], f"large f32 {mode}")
-    bscale = None
-    if mode != "weighted":
-        # s' = sum(|s q|) + sum(|c|): the oracle's fp64 absolute sums over a
-        # table of |s| q and one of |c| in every column (both exact in fp32)
-        D = 128
-        q, sc, bi = int8_parts(tabs[1].rows, D)
-        R = q.shape[0]
-        prod = OracleTable(np.ascontiguousarray(q.astype(np.float32) * sc), D, "f32")
-        bias = OracleTable(np.ascontiguousarray(np.broadcast_to(bi, (R, D))), D, "f32")
-        bscale = (ebo_forward([tabs[0], prod], idx, off, None, w.pooling, with_absum=True)[1][:, 128:] +
-                  ebo_forward([tabs[0], bias], idx, off, None, w.pooling, with_absum=True)[1][:, 128:])
-    check(got[:, 128:], ref[:, 128:], asum[:, 128:], L[:, 128:], RTOL["int8_rowwise"], f"large int8 {mode}",
-          bscale)
+    D = 128
+    for t, tb in enumerate(w.tables):
+        cols = slice(t * D, (t + 1) * D)
+        bscale = None
+        if is_int8(tb.dtype) and mode != "weighted":
+            # int8 rows sum s*q and the biases separately when unweighted: the
+            # bound scale s' = sum(|s q|) + sum(|c|), the oracle's fp64
+            # absolute sums over a table of |s| q and one of |c| in every
+            # column (both exact in fp32)
+            q, sc, bi = int8_parts(tabs[t])
+            R = q.shape[0]
+            prod = OracleTable(np.ascontiguousarray(q.astype(np.float32) * sc), D, "f32")
+            bias = OracleTable(np.ascontiguousarray(np.broadcast_to(bi, (R, D))), D, "f32")
+            others = [tabs[s] if s != t else None for s in range(len(tabs))]
+            bscale = (ebo_forward([prod if x is None else x for x in others], idx, off, None, w.pooling,
+                                  with_absum=True)[1][:, cols] +
+                      ebo_forward([bias if x is None else x for x in others], idx, off, None, w.pooling,
+                                  with_absum=True)[1][:, cols])
+        check(got[:, cols], ref[:, cols], asum[:, cols], L[:, cols], RTOL[tb.dtype], f"large {tb.dtype} {mode}",
+              bscale)
 
 
 def test_sequence_lookup_past_4gib(dev, tables):

@@ -67,14 +67,22 @@ def _row_values(table, rows):
     if table.dtype == "f16":
         return a[rows].astype(np.float64)
     D = table.dim
-    codes = a[rows, :D].astype(np.float64)
-    sb = np.ascontiguousarray(a[rows, D:D + 4]).view(np.float16).astype(np.float64)
+    if table.dtype == "int8_rowwise_split":
+        R, st = table.num_rows, table.row_stride
+        buf = a.reshape(-1)
+        codes = buf[:R * st].reshape(R, st)[rows, :D].astype(np.float64)
+        sb = np.ascontiguousarray(buf[R * st:R * st + 4 * R].reshape(R, 4)[rows]).view(np.float16)
+    else:
+        codes = a[rows, :D].astype(np.float64)
+        sb = np.ascontiguousarray(a[rows, D:D + 4]).view(np.float16)
+    sb = sb.astype(np.float64)
     return (sb[:, :1] * codes + sb[:, 1:2]).astype(np.float32).astype(np.float64)
 
 
-@pytest.mark.parametrize("name", ["c2", "c3a", "c3b", "c5"])
+@pytest.mark.parametrize("name", ["c2", "c3a", "c3b", "c5", "c5-packed"])
 def test_brute_force_from_table_rows(name):
-    w = make_workload(name, "cpu", rows_cap=400, batch=12, num_tables=4)
+    name, _, layout = name.partition("-")
+    w = make_workload(name, "cpu", rows_cap=400, batch=12, num_tables=4, int8_layout=layout or None)
     tabs = oracle_tables(w)
     T, B, D = len(tabs), w.batch, tabs[0].dim
     pooled, asum = oracle_forward(w, tables=tabs)

@@ -25,7 +25,7 @@ from paper_2609_30656_amd.workload import Table, make_workload
 
 pytestmark = pytest.mark.gpu
 
-RTOL = {"f32": 1e-5, "f16": 2e-3, "int8_rowwise": 2e-3}
+RTOL = {"f32": 1e-5, "f16": 2e-3, "int8_rowwise": 2e-3, "int8_rowwise_split": 2e-3}
 U = 2.0 ** -24
 
 
@@ -80,13 +80,24 @@ def per_element_lengths(w, bags=None):
     return lens.reshape(-1)[bags][:, None]
 
 
-def int8_parts(rows, D):
-    """Codes [R, D] (uint8), |scale| and |bias| [R, 1] (fp32, exact) of the
-    bytes of an int8 row-wise table in its packed layout (codes, then the
-    fp16 scale and bias of each row)."""
-    sc = np.abs(rows[:, D:D + 2].copy().view(np.float16).astype(np.float32))
-    bi = np.abs(rows[:, D + 2:D + 4].copy().view(np.float16).astype(np.float32))
-    return rows[:, :D], sc, bi
+def int8_parts(ot):
+    """Codes [R, D] (uint8), |scale| and |bias| [R, 1] (fp32, exact) of an
+    int8 row-wise OracleTable, packed (codes, then the fp16 scale and bias of
+    each row) or split (codes in the rows, the scale/bias words after them)."""
+    D = ot.dim
+    if ot.dtype == "int8_rowwise_split":
+        R, st = ot.num_rows, ot.row_stride
+        buf = ot.rows.reshape(-1)
+        codes, words = buf[:R * st].reshape(R, st)[:, :D], buf[R * st:R * st + 4 * R].reshape(R, 4)
+    else:
+        codes, words = ot.rows[:, :D], ot.rows[:, D:D + 4]
+    sc = np.abs(words[:, 0:2].copy().view(np.float16).astype(np.float32))
+    bi = np.abs(words[:, 2:4].copy().view(np.float16).astype(np.float32))
+    return codes, sc, bi
+
+
+def is_int8(dtype):
+    return dtype in ("int8_rowwise", "int8_rowwise_split")
 
 
 def split_scale(w, tables, bags=None):
@@ -96,7 +107,7 @@ def split_scale(w, tables, bags=None):
     table of |s| q (exact in fp32: an 11-bit by 8-bit product) plus those over
     a table holding |c| in every column (exact).  Other tables contribute
     their own |w x| sums.  None when no table of `w` takes the split sum."""
-    if w.weights is not None or not any(t.dtype == "int8_rowwise" for t in w.tables):
+    if w.weights is not None or not any(is_int8(t.dtype) for t in w.tables):
         return None
     prods, biases = [], []
     for tb, ot in zip(w.tables, tables):
@@ -104,12 +115,12 @@ def split_scale(w, tables, bags=None):
             prods.append(ot)
             biases.append(ot)
             continue
-        R, D = ot.rows.shape[0], tb.dim
-        if tb.dtype != "int8_rowwise":
+        R, D = tb.num_rows, tb.dim
+        if not is_int8(tb.dtype):
             prods.append(ot)
             biases.append(OracleTable(np.zeros((R, D), np.float32), D, "f32", R))
             continue
-        q, sc, bi = int8_parts(ot.rows, D)
+        q, sc, bi = int8_parts(ot)
         prods.append(OracleTable(np.ascontiguousarray(q.astype(np.float32) * sc), D, "f32", R))
         biases.append(OracleTable(np.ascontiguousarray(np.broadcast_to(bi, (R, D))), D, "f32", R))
     return (oracle_forward(w, tables=prods, bags=bags)[1] + oracle_forward(w, tables=biases, bags=bags)[1])
@@ -157,6 +168,29 @@ def test_uniform_index_control(dev, name):
     say(f"[parity] uniform indices {name}")
     w = make_workload(name, dev, index_law="uniform", **REDUCED[name])
     full_check(w, f"uniform {name}")
+
+
+@pytest.mark.parametrize("variant", ["zipf", "int32", "uniform", "k3", "k32"])
+def test_c5_split_int8_layout(dev, monkeypatch, variant):
+    # c5's tables in the split layout (codes in 128-byte rows, scale/bias
+    # block after them): the same values as the packed layout, so the same
+    # bar and the same oracle outputs
+    say(f"[parity] c5 split layout, {variant}")
+    kw = dict(REDUCED["c5"], int8_layout="split")
+    if variant == "int32":
+        kw["index_dtype"] = torch.int32
+    if variant == "uniform":
+        kw["index_law"] = "uniform"
+    if variant.startswith("k"):
+        monkeypatch.setenv("EB_BAGS_PER_WAVE", variant[1:])
+    w = make_workload("c5", dev, **kw)
+    assert all(t.dtype == "int8_rowwise_split" and t.row_stride_bytes == 128 for t in w.tables)
+    got = full_check(w, f"c5 split {variant}")
+    packed = make_workload("c5", dev, **dict(kw, int8_layout="packed"))
+    assert torch.equal(packed.indices, w.indices)
+    # the layout changes where the bytes are, not the values or the order of
+    # the sum: the packed tables give the same bits
+    assert np.array_equal(got.view(np.uint32), run_gpu(packed).cpu().numpy().view(np.uint32))
 
 
 @pytest.mark.parametrize("k", [2, 3, 7, 32])
@@ -247,10 +281,11 @@ def _sampled(w, tables_to_check, n_random=400, seed=0):
     return np.unique(np.array(picks, dtype=np.int64))
 
 
-@pytest.mark.parametrize("name", ["c3a", "c3b", "c4", "c5"])
+@pytest.mark.parametrize("name", ["c3a", "c3b", "c4", "c5", "c5-packed"])
 def test_full_size_sampled(dev, name):
     say(f"[parity] full {name}: generating")
-    w = make_workload(name, dev)
+    name, _, layout = name.partition("-")
+    w = make_workload(name, dev, int8_layout=layout or None)
     T = w.num_tables
     check_tables = sorted({0, T // 2, T - 1})
     say(f"[parity] full {name}: {w.num_indices} lookups, {w.num_bags} bags; forward")
@@ -267,8 +302,7 @@ def test_full_size_sampled(dev, name):
         col += tb.dim
     bags = _sampled(w, check_tables)
     say(f"[parity] full {name}: oracle on {bags.size} sampled bags of tables {check_tables}")
-    tabs = [OracleTable(tb.rows.cpu().numpy() if t in check_tables else None, tb.dim, tb.dtype, tb.num_rows)
-            for t, tb in enumerate(w.tables)]
+    tabs = [OracleTable.of(tb, with_rows=t in check_tables) for t, tb in enumerate(w.tables)]
     ref, asum = oracle_forward(w, tables=tabs, bags=bags)
     bscale = split_scale(w, tabs, bags)
     bscale = asum if bscale is None else bscale
@@ -296,14 +330,30 @@ def _table(dev, dtype, R, D, stride=None, seed=0):
     elif dtype == "f16":
         width = D if stride is None else stride // 2
         rows = (torch.randn((R, width), generator=g, device=dev) * 0.01).half()
-    else:
+    elif dtype == "int8_rowwise":
         width = D + 4 if stride is None else stride
         rows = torch.randint(0, 256, (R, width), generator=g, device=dev, dtype=torch.uint8)
         sc = (torch.rand(R, generator=g, device=dev) * 3e-4 + 1e-4).half().view(torch.uint8).view(R, 2)
         bi = (torch.rand(R, generator=g, device=dev) * 0.04 - 0.06).half().view(torch.uint8).view(R, 2)
         rows[:, D:D + 2] = sc
         rows[:, D + 2:D + 4] = bi
+    else:
+        # the values _table draws for a packed table, stored split: codes in
+        # rows of `stride` bytes (padding bytes 0xAB, never read), then the
+        # rows' scale/bias words
+        return to_split(_table(dev, "int8_rowwise", R, D, seed=seed), stride)
     return Table(rows, D, dtype)
+
+
+def to_split(packed, stride=None):
+    """A packed int8 row-wise Table's values in the split layout."""
+    R, D = packed.num_rows, packed.dim
+    stride = (D + 15) // 16 * 16 if stride is None else stride
+    storage = torch.full((R * stride + 4 * R,), 0xAB, dtype=torch.uint8, device=packed.rows.device)
+    rows = storage[:R * stride].view(R, stride)
+    rows[:, :D] = packed.rows[:, :D]
+    storage[R * stride:].view(R, 4).copy_(packed.rows[:, D:D + 4])
+    return Table(rows, D, "int8_rowwise_split", storage)
 
 
 def _custom(dev, tables, lens_per_table, weighted=False, pooling="sum", index_dtype=torch.int64, seed=0):
@@ -328,7 +378,8 @@ def _custom(dev, tables, lens_per_table, weighted=False, pooling="sum", index_dt
 WIDTHS = [("f32", 4), ("f32", 12), ("f32", 20), ("f32", 100), ("f32", 260), ("f32", 1024), ("f32", 1028),
           ("f16", 8), ("f16", 24), ("f16", 40), ("f16", 136), ("f16", 520), ("f16", 2048),
           ("int8_rowwise", 16), ("int8_rowwise", 48), ("int8_rowwise", 272), ("int8_rowwise", 1024),
-          ("int8_rowwise", 2064)]
+          ("int8_rowwise", 2064), ("int8_rowwise_split", 16), ("int8_rowwise_split", 128),
+          ("int8_rowwise_split", 272), ("int8_rowwise_split", 2064)]
 
 
 @pytest.mark.parametrize("k", ["0", "5"])
@@ -374,18 +425,20 @@ def test_one_very_long_bag(dev, monkeypatch, long_len):
 def test_padded_row_strides(dev):
     say("[parity] padded strides")
     tables = [_table(dev, "f32", 500, 64, stride=512), _table(dev, "f16", 500, 64, stride=256),
-              _table(dev, "int8_rowwise", 500, 128, stride=144), _table(dev, "int8_rowwise", 500, 32, stride=40)]
+              _table(dev, "int8_rowwise", 500, 128, stride=144), _table(dev, "int8_rowwise", 500, 32, stride=40),
+              _table(dev, "int8_rowwise_split", 500, 128, stride=160, seed=1),
+              _table(dev, "int8_rowwise_split", 500, 32, stride=48, seed=2)]
     rng = np.random.default_rng(6)
     w = _custom(dev, tables, [rng.integers(0, 50, 64) for _ in tables], weighted=True)
     full_check(w, "padded strides")
 
 
 @pytest.mark.parametrize("k", ["0", "3"])
-@pytest.mark.parametrize("dtype", ["f32", "f16", "int8_rowwise"])
+@pytest.mark.parametrize("dtype", ["f32", "f16", "int8_rowwise", "int8_rowwise_split"])
 def test_long_bags(dev, monkeypatch, dtype, k):
     say(f"[parity] long bags {dtype} k={k}")
     monkeypatch.setenv("EB_BAGS_PER_WAVE", k)
-    D = {"f32": 64, "f16": 128, "int8_rowwise": 128}[dtype]
+    D = {"f32": 64, "f16": 128}.get(dtype, 128)
     tables = [_table(dev, dtype, 5000, D)]
     w = _custom(dev, tables, [np.array([5000, 0, 1, 63, 64, 65, 1000, 4097])])
     full_check(w, f"long {dtype}")

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from conftest import oracle_tables
+from conftest import compact_oracle_table, oracle_tables
 from oracle import OracleTable, ebo_forward_seq
 from paper_2609_30656_amd import eb
 from paper_2609_30656_amd.workload import make_workload
@@ -61,6 +61,15 @@ def test_reduced_configs(dev, name):
     full_seq_check(make_workload(name, dev, **REDUCED[name]), f"reduced {name}")
 
 
+@pytest.mark.parametrize("variant", ["int64", "int32"])
+def test_c5_split_int8_layout(dev, variant):
+    say(f"[seq] c5 split layout {variant}")
+    kw = dict(REDUCED["c5"], int8_layout="split")
+    if variant == "int32":
+        kw["index_dtype"] = torch.int32
+    full_seq_check(make_workload("c5", dev, **kw), f"c5 split {variant}")
+
+
 @pytest.mark.parametrize("name", ["c2", "c4", "c5"])
 def test_int32_indices(dev, name):
     say(f"[seq] int32 {name}")
@@ -95,7 +104,9 @@ def test_every_width_and_empty_tables(dev, monkeypatch, k):
 def test_padded_row_strides(dev):
     say("[seq] padded strides")
     tables = [_table(dev, "f32", 500, 64, stride=512), _table(dev, "f16", 500, 64, stride=256),
-              _table(dev, "int8_rowwise", 500, 128, stride=144), _table(dev, "int8_rowwise", 500, 32, stride=40)]
+              _table(dev, "int8_rowwise", 500, 128, stride=144), _table(dev, "int8_rowwise", 500, 32, stride=40),
+              _table(dev, "int8_rowwise_split", 500, 128, stride=160, seed=1),
+              _table(dev, "int8_rowwise_split", 500, 32, stride=48, seed=2)]
     rng = np.random.default_rng(6)
     full_seq_check(_custom(dev, tables, [rng.integers(0, 50, 64) for _ in tables]), "padded strides")
 
@@ -115,9 +126,10 @@ def test_full_size_every_element(dev, name):
     full_seq_check(make_workload(name, dev), f"full {name}")
 
 
-def test_full_c5_sampled(dev):
-    say("[seq] full c5: generating")
-    w = make_workload("c5", dev)
+@pytest.mark.parametrize("layout", ["packed", "split"])
+def test_full_c5_sampled(dev, layout):
+    say(f"[seq] full c5 ({layout} int8 rows): generating")
+    w = make_workload("c5", dev, int8_layout=layout)
     n = w.num_indices
     say(f"[seq] full c5: {n} positions, {n * 128 * 4 / 1e9:.1f} GB of output")
     out = run_seq(w).view(n, 128)
@@ -132,8 +144,7 @@ def test_full_c5_sampled(dev):
     for t in np.unique(tabs):
         sel = np.nonzero(tabs == t)[0]
         rows, inv = np.unique(idx[sel], return_inverse=True)
-        host = w.tables[t].rows.index_select(0, torch.from_numpy(rows).to(dev)).cpu().numpy()
-        ref = ebo_forward_seq([OracleTable(np.ascontiguousarray(host), 128, "int8_rowwise")],
+        ref = ebo_forward_seq([compact_oracle_table(w.tables[t], rows)],
                               inv.astype(np.int64), np.array([0, inv.size], np.int64)).reshape(-1, 128)
         assert np.array_equal(got[sel].view(np.uint32), ref.view(np.uint32)), f"table {t}"
 

@@ -66,12 +66,31 @@ def test_zipf_is_skewed_and_uniform_is_not():
 
 
 def test_int8_row_layout():
-    w = make_workload("c5", "cpu", rows_cap=500, batch=8, num_tables=2)
+    w = make_workload("c5", "cpu", rows_cap=500, batch=8, num_tables=2, int8_layout="packed")
     t = w.tables[0]
+    assert t.dtype == "int8_rowwise"
     assert t.rows.dtype == torch.uint8 and t.row_stride_bytes == 132 and t.row_bytes == 132
     s = t.rows[:, 128:130].contiguous().view(torch.float16).float()
     c = t.rows[:, 130:132].contiguous().view(torch.float16).float()
     assert s.min() >= 0.99e-4 and s.max() <= 4.01e-4 and c.min() >= -0.0601 and c.max() <= -0.0199
+
+
+def test_int8_split_layout_holds_the_packed_values():
+    # c5's default layout: codes in 128-byte rows, then the scale/bias block;
+    # the same draws as the packed layout, byte for byte
+    split = make_workload("c5", "cpu", rows_cap=500, batch=8, num_tables=2)
+    packed = make_workload("c5", "cpu", rows_cap=500, batch=8, num_tables=2, int8_layout="packed")
+    for s, p in zip(split.tables, packed.tables):
+        R = s.num_rows
+        assert s.dtype == "int8_rowwise_split" and s.row_stride_bytes == 128 and s.row_bytes == 132
+        assert s.storage.numel() == R * 132 and s.rows.data_ptr() == s.storage.data_ptr()
+        assert torch.equal(s.rows[:, :128], p.rows[:, :128])
+        assert torch.equal(s.storage[R * 128:].view(R, 4), p.rows[:, 128:132])
+        assert s.host_bytes().shape == (R * 132,)
+        c = s.clone()
+        assert torch.equal(c.storage, s.storage) and c.storage.data_ptr() != s.storage.data_ptr()
+    assert torch.equal(split.indices, packed.indices) and torch.equal(split.offsets, packed.offsets)
+    assert split.algorithmic_bytes() == packed.algorithmic_bytes()
 
 
 def test_algorithmic_bytes_counts_every_term():
