@@ -69,7 +69,10 @@
  * XCD-contiguous for handles of up to 32 tables, round-robin otherwise).
  * EB_BWD_TILE_CHUNKS=c (1..16) fixes the backward's tiles at 64*c sorted
  * positions (default: 64, or 128 from about two million lookups on), and
- * EB_BWD_XCD_REMAP=0|1 its workgroup order (default as for the forward).
+ * EB_BWD_XCD_REMAP=0|1 its workgroup order (default as for the forward);
+ * EB_BWD_SORT_ITEMS=4|8|12|16 fixes the backward sort's blocks at 512
+ * threads of that many elements (default: chosen per call from the number of
+ * lookups and how many of the sort's workgroups the GPU holds at once).
  * EB_LONG_BAG=n (n > 0) makes the handle's lookups pool every bag of more
  * than n lookups with all four wavefronts of a workgroup (each a contiguous
  * quarter, partial sums added in a fixed order): for inputs with very long
@@ -284,9 +287,14 @@ typedef enum { EB_OPT_SGD = 0, EB_OPT_ROWWISE_ADAGRAD = 1 } eb_optimizer;
 
 /*
  * Device workspace (bytes) eb_backward_update needs for num_indices lookups
- * on this handle: 16 bytes per lookup, then per tile of 64 or 128 sorted
- * lookups (64*c under EB_BWD_TILE_CHUNKS=c) an 8-byte descriptor and two partial rows of the widest table
- * (8 * max dim bytes), and the sort's scratch.  Synchronous, host only.
+ * on this handle: 20 bytes per lookup (the sort's two 8-byte element buffers
+ * and a bag id), then per tile of 64 or 128 sorted lookups (64*c under
+ * EB_BWD_TILE_CHUNKS=c) an 8-byte descriptor and two partial rows of the
+ * widest table (8 * max dim bytes), and the sort's counters: 4 bytes per
+ * table, pass and digit value, and 8 bytes per pass, digit value and block of
+ * 2048 lookups (one more block per table), with digits of up to 9 bits and
+ * as many passes as the largest table's row count needs.  Synchronous, host
+ * only.
  */
 eb_status eb_backward_workspace_size(const eb_tables *tables, int64_t num_indices, size_t *bytes);
 
@@ -306,7 +314,9 @@ eb_status eb_backward_workspace_size(const eb_tables *tables, int64_t num_indice
  * The tables' rows (the descriptors' data) are written in place.  Only fp32
  * and fp16 tables with dim <= 256 train (else EB_ERR_UNSUPPORTED), and the
  * handle's total row count plus its table count must stay below 2^32.
- * Asynchronous on the handle's stream (checked mode as for eb_forward);
+ * Asynchronous on the handle's stream (checked mode as for eb_forward;
+ * there EB_ERR_HIP also reports a sort pass whose bounded wait for an earlier
+ * block's counts ran out, which leaves the update wrong but cannot hang);
  * allocates nothing.  Forwards and backwards on one handle are ordered by
  * the stream; two backwards that update the same rows must not overlap.
  */

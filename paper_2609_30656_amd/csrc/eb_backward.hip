@@ -13,11 +13,13 @@
 //   row-wise Adagrad:  s[r] += mean_d G[d]^2;  W[r] -= lr * G / (sqrt(s[r]) + eps)
 //
 // Computed without atomics on data, and deterministically:
-//   1. every position gets a 32-bit sort key (the table's key base + row) and
-//      its bag id, and each table's first tile is found from the offsets;
-//   2. (key, position) pairs are radix-sorted (rocPRIM): each row's
-//      occurrences become one run, in position order, and each table's
-//      positions stay inside that table's range of the sorted array;
+//   1. every position gets a sort element (its row, or the table's sentinel
+//      row, above its table-local bag id or its position), and each table's
+//      first tile and sort blocks are found from the offsets;
+//   2. each table's elements are radix-sorted by row, least significant digit
+//      first, one stable pass per digit: each row's occurrences become one
+//      run, in position order, and each table's positions stay inside that
+//      table's range of the sorted array;
 //   3. each table's sorted range is cut into tiles of 64 or 128 positions; a
 //      wavefront walks its tile's runs, pools each run's gradient rows with the
 //      forward's 16-byte-slice gather and reduce-scatter (the gradient is an
@@ -32,10 +34,8 @@
 // times per batch) are thereby spread over as many wavefronts as they have
 // tiles, and no wavefront waits for another.
 
+#include <atomic>
 #include <mutex>
-
-#include <rocprim/device/device_radix_sort.hpp>
-#include <rocprim/iterator/counting_iterator.hpp>
 
 #include "eb_device.h"
 
@@ -46,22 +46,18 @@ static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 namespace eb {
 namespace {
 
-// The (key, value) sort: onesweep passes of 9 bits with 1024-thread blocks of
-// 8 items each.  rocPRIM's own choice for 32-bit pairs on this GPU takes 16
-// items per thread, so a 1 M-pair sort runs as only 65 blocks per pass; with 8
-// the backward step was 12% faster on 1 M lookups, 4% on 15 M and the same on
-// 3 M (smaller blocks or fewer items were slower on the larger inputs).  Keys
-// of up to 27 bits (tens of millions of rows) take three 9-bit passes instead
-// of four 8-bit ones: 7-10% off the step there; 10-bit digits were slower.
-using SortConfig = rocprim::radix_sort_config<
-    rocprim::default_config, rocprim::default_config,
-    rocprim::radix_sort_onesweep_config<rocprim::kernel_config<1024, 8>, rocprim::kernel_config<1024, 8>, 9,
-                                        rocprim::block_radix_rank_algorithm::match>>;
-
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;  // larger than any key (keys fit below it)
 constexpr uint8_t kTileContinues = 1;      // the tile's last run goes on into the next tile
 constexpr uint8_t kTileOwnsRun = 2;        // ... and started in this tile: this tile finishes it
 constexpr int kOptRowwiseAdagrad = 1;
+
+// The sort (step 2): workgroups of 512 threads, digits of up to 9 bits (one
+// digit per thread where a workgroup handles all digits), up to 4 passes
+// (rows of up to 32 bits).
+constexpr int kSortThreads = 512;
+constexpr int kSortWaves = kSortThreads / kWave;
+constexpr int kSortRadixMax = 512;
+constexpr int kSortMaxPasses = 4;
 
 struct BwdArgs {
   const TableMeta *meta;
@@ -71,8 +67,7 @@ struct BwdArgs {
   const float *weights;
   const float *grad;      // grad_out [B, sum D]
   float *state;           // row-wise Adagrad state [sum R]
-  uint32_t *keys;         // [N] sort keys by position
-  int32_t *bag_of;        // [N] bag id by position
+  int32_t *bag_of;        // [N] bag id by position (positions sorted: weighted pooling)
   const uint32_t *skeys;  // [N] sorted keys
   const uint32_t *spos;   // [N] in sorted order: positions, or bag ids when sorted_bags
   int32_t *tile_start;    // [T + 1] first tile of each table; [T] = number of tiles
@@ -95,6 +90,21 @@ struct BwdArgs {
   int32_t groups_per_table;
   int32_t num_waves;
   int32_t xcd_remap;      // tiles kernel: XCD-contiguous workgroup order
+  // the sort (step 2)
+  void *elems[2];         // [N] sort elements: elems[0] by position, then alternating per pass
+  int4 *sblocks;          // [sort blocks] {table, first position, end position, table's first position}
+  int32_t *sort_nblocks;  // number of sort blocks
+  uint32_t *hist;         // [T][passes][radix] digit counts per table
+  uint64_t *status;       // [passes][sort blocks][radix] per-block digit counts for the look-back
+  uint4 *zero;            // hist and status: cleared by the keys kernel
+  int64_t zero_words;     // 16-byte words from `zero`
+  int32_t sort_block;     // positions per sort block
+  int32_t sort_nblk_ub;   // sort blocks the launch provides for
+  int32_t sort_passes;
+  int32_t sort_bits;      // digit bits per pass
+  int32_t sort_wide;      // 64-bit elements: row << 32 | value; else row << vshift | value
+  int32_t sort_vshift;
+  uint32_t sort_vmask;
 };
 
 __device__ __forceinline__ int64_t load_offset(const BwdArgs &a, int64_t g) {
@@ -111,28 +121,14 @@ __device__ __forceinline__ void table_range(const BwdArgs &a, int32_t t, int64_t
   p1 = clamp_pos(load_offset(a, (int64_t)(t + 1) * a.batch), p0, a.num_indices);
 }
 
-// Step 3a: first tile of every table, an exclusive scan of the tables' tile
-// counts by one workgroup of NT threads (part: 2 * NT / 64 slots of LDS).
-// Tile counts depend on the offsets alone, so the keys kernel's last
-// workgroup runs this before its own positions.
+// Exclusive scan of one int64 per thread over a workgroup of NT threads
+// (part: 2 * NT / 64 slots of LDS); total receives the sum of all.
 template <int NT>
-__device__ __forceinline__ void scan_tile_starts(const BwdArgs &a, int64_t *part) {
+__device__ __forceinline__ int64_t block_exclusive_scan(int64_t x, int64_t *part, int64_t &total) {
   constexpr int kWaves = NT / kWave;
-  const int T = a.num_tables;
   const int tid = threadIdx.x;
-  const int per = (T + NT - 1) / NT;
-  const int t0 = tid * per < T ? tid * per : T;
-  const int t1 = t0 + per < T ? t0 + per : T;
-  int64_t sum = 0;
-  for (int t = t0; t < t1; ++t) {
-    int64_t p0, p1;
-    table_range(a, t, p0, p1);
-    sum += (p1 - p0 + a.tile_size - 1) / a.tile_size;
-  }
-  // exclusive scan of the per-thread sums: within each wavefront, then over
-  // the wavefronts' totals
   const int lane = tid & (kWave - 1), wave = tid / kWave;
-  int64_t incl = sum;
+  int64_t incl = x;
 #pragma unroll
   for (int o = 1; o < kWave; o <<= 1) {
     const int64_t v = __shfl_up(incl, o);
@@ -150,25 +146,58 @@ __device__ __forceinline__ void scan_tile_starts(const BwdArgs &a, int64_t *part
     if (lane < kWaves) part[kWaves + lane] = w;  // inclusive totals of waves 0..lane
   }
   __syncthreads();
-  int64_t run = incl - sum + (wave > 0 ? part[kWaves + wave - 1] : 0);
-  if (tid == NT - 1) a.tile_start[T] = (int32_t)(run + sum);
+  total = part[2 * kWaves - 1];
+  const int64_t r = incl - x + (wave > 0 ? part[kWaves + wave - 1] : 0);
+  __syncthreads();  // part may be reused
+  return r;
+}
+
+// Step 3a: first tile of every table, an exclusive scan of the tables' tile
+// counts, and the sort blocks of step 2 (each table's positions cut into
+// pieces of sort_block), by one workgroup of NT threads.  Both depend on the
+// offsets alone, so the keys kernel's first workgroup does this before its own
+// positions.
+template <int NT>
+__device__ __forceinline__ void scan_tables(const BwdArgs &a, int64_t *part) {
+  const int T = a.num_tables;
+  const int tid = threadIdx.x;
+  const int per = (T + NT - 1) / NT;
+  const int t0 = tid * per < T ? tid * per : T;
+  const int t1 = t0 + per < T ? t0 + per : T;
+  const int64_t SB = a.sort_block;
+  int64_t tiles = 0, blocks = 0;
   for (int t = t0; t < t1; ++t) {
-    a.tile_start[t] = (int32_t)run;
     int64_t p0, p1;
     table_range(a, t, p0, p1);
-    run += (p1 - p0 + a.tile_size - 1) / a.tile_size;
+    tiles += (p1 - p0 + a.tile_size - 1) / a.tile_size;
+    blocks += (p1 - p0 + SB - 1) / SB;
+  }
+  int64_t total_tiles, total_blocks;
+  int64_t tile = block_exclusive_scan<NT>(tiles, part, total_tiles);
+  int64_t blk = block_exclusive_scan<NT>(blocks, part, total_blocks);
+  if (tid == 0) {
+    a.tile_start[T] = (int32_t)total_tiles;
+    *a.sort_nblocks = (int32_t)total_blocks;
+  }
+  for (int t = t0; t < t1; ++t) {
+    a.tile_start[t] = (int32_t)tile;
+    int64_t p0, p1;
+    table_range(a, t, p0, p1);
+    tile += (p1 - p0 + a.tile_size - 1) / a.tile_size;
+    for (int64_t s = p0; s < p1; s += SB, ++blk)
+      a.sblocks[blk] = make_int4(t, (int32_t)s, (int32_t)(s + SB < p1 ? s + SB : p1), (int32_t)p0);
   }
 }
 
-// Keys and bag ids of positions [P0, P1) (bags g0 .. g0 + nb - 1, whose
-// offsets lane j holds in my_off).  kKeyChunks chunks of 64 positions per
-// round: every index load of a round is issued before its first key is
-// stored, and none sits behind a branch (a position past P1 re-reads P1 - 1),
-// so a round costs one memory round trip.  Returns whether this lane saw an
-// index outside the table.
+// Sort elements (and, for weighted pooling, bag ids) of positions [P0, P1)
+// (bags g0 .. g0 + nb - 1 of table t, whose offsets lane j holds in my_off).
+// kKeyChunks chunks of 64 positions per round: every index load of a round is
+// issued before its first element is stored, and none sits behind a branch (a
+// position past P1 re-reads P1 - 1), so a round costs one memory round trip.
+// Returns whether this lane saw an index outside the table.
 template <typename IT>
 __device__ __forceinline__ bool key_positions(const BwdArgs &a, const TableMeta &m, int64_t P0, int64_t P1,
-                                              int64_t my_off, int nb, int32_t g0) {
+                                              int64_t my_off, int nb, int32_t g0, int32_t b0) {
   constexpr int kKeyChunks = 4;
   const int lane = threadIdx.x & (kWave - 1);
   const IT *idx = static_cast<const IT *>(a.indices);
@@ -189,24 +218,31 @@ __device__ __forceinline__ bool key_positions(const BwdArgs &a, const TableMeta 
           if (readlane64(my_off, jj) <= p) j = jj;
         const bool ok = r[u] >= 0 && r[u] < m.num_rows;
         oob |= !ok;
-        a.keys[p] = m.key_base + (ok ? (uint32_t)r[u] : (uint32_t)m.num_rows);
-        a.bag_of[p] = g0 + j;
+        const uint32_t row = ok ? (uint32_t)r[u] : (uint32_t)m.num_rows;
+        // unweighted pooling carries the table-local bag id; weighted pooling
+        // the position, whose weight and bag the tiles kernel looks up
+        const uint32_t v = a.sorted_bags ? (uint32_t)(b0 + j) : (uint32_t)p;
+        if (a.sort_wide) static_cast<uint64_t *>(a.elems[0])[p] = ((uint64_t)row << 32) | v;
+        else static_cast<uint32_t *>(a.elems[0])[p] = (row << a.sort_vshift) | v;
+        if (!a.sorted_bags) a.bag_of[p] = g0 + j;
       }
     }
   }
   return oob;
 }
 
-// Step 1: sort key and bag id of every position.  A wavefront takes a run of
+// Step 1: sort element of every position.  A wavefront takes a run of
 // consecutive bags of one table and walks their positions 64 at a time (the
 // same work map as the forward).  An index outside its table gets the table's
-// sentinel key (one past its last row), which sorts after the table's rows
-// and is skipped later.
+// sentinel row (one past its last row), which sorts after the table's rows
+// and is skipped later.  The kernel also clears the sort's counters.
 __global__ __launch_bounds__(kBlock) void eb_bwd_keys_kernel(BwdArgs a) {
-  if (blockIdx.x == gridDim.x - 1) {
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < a.zero_words; i += (int64_t)gridDim.x * kBlock)
+    a.zero[i] = make_uint4(0u, 0u, 0u, 0u);
+  if (blockIdx.x == 0) {
     // every thread of the workgroup, before any wavefront can leave
     __shared__ int64_t part[2 * kWavesPerBlock];
-    scan_tile_starts<kBlock>(a, part);
+    scan_tables<kBlock>(a, part);
   }
   const int32_t wid = (int32_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if (wid >= a.num_waves) return;
@@ -231,10 +267,288 @@ __global__ __launch_bounds__(kBlock) void eb_bwd_keys_kernel(BwdArgs a) {
   const int64_t my_off = clamp_pos(raw, 0, N);
   const int64_t P0 = readlane64(my_off, 0);
   const int64_t P1 = readlane64(my_off, nb);
-  const bool oob = a.idx64 ? key_positions<int64_t>(a, m, P0, P1, my_off, nb, g0)
-                           : key_positions<int32_t>(a, m, P0, P1, my_off, nb, g0);
+  const bool oob = a.idx64 ? key_positions<int64_t>(a, m, P0, P1, my_off, nb, g0, b0)
+                           : key_positions<int32_t>(a, m, P0, P1, my_off, nb, g0, b0);
   if (__ballot(oob)) {
     if (lane == 0) atomicOr(a.ctx.err, kErrIndex);
+  }
+}
+
+// Step 2: the sort.  Each table's elements are sorted by row, least
+// significant digit first; a pass is a stable partition by one digit of the
+// row inside every table's range of positions, which is cut into sort blocks
+// of sort_block positions.  The digit counts of every table and pass come
+// first (eb_bwd_sort_hist_kernel).  In a pass (eb_bwd_sort_pass_kernel) a
+// workgroup ranks a sort block's elements by digit in LDS, and finds where its
+// digits go from the blocks before it in the same table: it publishes its own
+// digit counts, then walks back over its predecessors' published counts until
+// one of them holds the sum over every block before it, and publishes that sum
+// with its own counts added.  This is the decoupled look-back of single-pass
+// prefix scans (Merrill and Garland, 2016), as radix sorts with one pass per
+// digit use it.  The grid is no larger than the GPU holds at once, and each
+// workgroup takes blocks blockIdx.x, blockIdx.x + gridDim.x, ... in turn, so
+// the lowest unfinished block always belongs to a resident workgroup and
+// waits for nothing: no block waits for one that cannot run.  (A ticket
+// counter that orders workgroups as they start costs every workgroup an
+// atomic on one address, which serialised: about 37 ns each.)  Every wait is
+// bounded besides, so that a wait that never ended would raise kErrSortWait
+// and let the workgroup go on rather than hang.
+constexpr int kHistThreads = 512;
+constexpr int kHistBlocksPerGroup = 1;  // sort blocks a histogram workgroup counts
+constexpr uint32_t kLbAggregate = 1;    // status word: the block's own counts
+constexpr uint32_t kLbPrefix = 2;       // ... counts of every block of the table up to and including it
+constexpr int kSortSpinLimit = 1 << 18;
+constexpr int kLookBack = 8;  // predecessors read per look-back round trip
+
+// row of a sort element
+template <typename E>
+__device__ __forceinline__ uint32_t elem_row(const BwdArgs &a, E e) {
+  if constexpr (sizeof(E) == 8) return (uint32_t)(e >> 32);
+  else return e >> a.sort_vshift;
+}
+
+// Digit counts of each table for every pass, from the elements in position
+// order: a workgroup counts kHistBlocksPerGroup consecutive sort blocks in
+// LDS and adds its counts to the table's (integer additions: the totals do
+// not depend on their order).
+template <typename E>
+__global__ __launch_bounds__(kHistThreads) void eb_bwd_sort_hist_kernel(BwdArgs a) {
+  __shared__ uint32_t h[kSortMaxPasses * kSortRadixMax];
+  const int tid = threadIdx.x;
+  const int np = a.sort_passes, bits = a.sort_bits, radix = 1 << bits;
+  const uint32_t dmask = (uint32_t)radix - 1u;
+  const int nh = np * radix;
+  for (int i = tid; i < nh; i += kHistThreads) h[i] = 0u;
+  const int32_t nblk = *a.sort_nblocks;
+  const int32_t b0 = (int32_t)blockIdx.x * kHistBlocksPerGroup;
+  const int32_t b1 = b0 + kHistBlocksPerGroup < nblk ? b0 + kHistBlocksPerGroup : nblk;
+  const E *src = static_cast<const E *>(a.elems[0]);
+  int32_t cur = -1;  // table whose counts h holds (the same in every thread)
+  auto flush = [&]() {
+    __syncthreads();
+    uint32_t *g = a.hist + (size_t)cur * nh;
+    for (int i = tid; i < nh; i += kHistThreads) {
+      const uint32_t v = h[i];
+      if (v) {
+        atomicAdd(g + i, v);
+        h[i] = 0u;
+      }
+    }
+    __syncthreads();
+  };
+  __syncthreads();
+  constexpr int U = 8;
+  for (int32_t b = b0; b < b1; ++b) {
+    const int4 sb = a.sblocks[b];
+    if (sb.x != cur) {
+      if (cur >= 0) flush();
+      cur = sb.x;
+    }
+    for (int32_t p = sb.y + tid; p < sb.z; p += U * kHistThreads) {
+      E e[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int32_t q = p + u * kHistThreads;
+        e[u] = src[q < sb.z ? q : p];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (p + u * kHistThreads < sb.z) {
+          const uint32_t row = elem_row<E>(a, e[u]);
+          for (int q = 0; q < np; ++q) atomicAdd(&h[q * radix + ((row >> (q * bits)) & dmask)], 1u);
+        }
+      }
+    }
+  }
+  if (cur >= 0) flush();
+}
+
+// Sort block b of a pass (the body of eb_bwd_sort_pass_kernel's loop).
+template <typename E, int IPT>
+__device__ __forceinline__ void sort_block(const BwdArgs &a, int32_t pass, int32_t b, E *stage,
+                                           uint32_t (*cnt)[kSortRadixMax], int32_t *loff, int32_t *goff,
+                                           int64_t *part, int tid, int lane, int w) {
+  for (int i = tid; i < kSortWaves * kSortRadixMax; i += kSortThreads) (&cnt[0][0])[i] = 0;
+  __syncthreads();
+  const int4 sb = a.sblocks[b];  // {table, start, end, table's first position}
+  const int bits = a.sort_bits, radix = 1 << bits;
+  const uint32_t dmask = (uint32_t)radix - 1u;
+  const int shift = (sizeof(E) == 8 ? 32 : a.sort_vshift) + pass * bits;
+  const E *src = static_cast<const E *>(a.elems[pass & 1]);
+  const int32_t n = sb.z - sb.y;
+
+  // elements past the block's end get the largest digit: they rank after
+  // every element of the block and are not stored
+  E e[IPT];
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int k = w * kWave * IPT + i * kWave + lane;
+    e[i] = k < n ? src[sb.y + k] : ~(E)0;
+  }
+  const uint32_t tcount =
+      tid < radix ? a.hist[((size_t)sb.x * a.sort_passes + pass) * radix + tid] : 0u;
+  // stable rank within the wave: the lanes holding the same digit are found
+  // with one ballot per digit bit; the lowest of them adds the group to the
+  // wave's count of that digit (an LDS add that returns the count before it:
+  // one wave's LDS operations take effect in order, so the items' adds need
+  // not wait for each other) and the others read that count from it
+  // (four items at a time, which bounds the registers the adds in flight hold)
+  uint32_t dg[IPT], rk[IPT];
+  const uint64_t below_me = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int i0 = 0; i0 < IPT; i0 += 4) {
+    uint32_t lead[4], old[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u;
+      dg[i] = (uint32_t)(e[i] >> shift) & dmask;
+      uint64_t peers = ~0ull;
+      for (int q = 0; q < bits; ++q) {
+        const bool bit = (dg[i] >> q) & 1u;
+        const uint64_t bal = __ballot(bit);
+        peers &= bit ? bal : ~bal;
+      }
+      const uint64_t below = peers & below_me;
+      rk[i] = (uint32_t)__builtin_popcountll(below);
+      lead[u] = (uint32_t)__builtin_ctzll(peers);
+      old[u] = below == 0 ? atomicAdd(&cnt[w][dg[i]], (uint32_t)__builtin_popcountll(peers)) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) rk[i0 + u] += (uint32_t)__shfl((int)old[u], (int)lead[u]);
+  }
+  __syncthreads();
+  // per digit: counts of the earlier waves, and the block's count, published
+  // at once for the blocks after this one
+  const bool first = sb.y == sb.w;
+  uint64_t *status = a.status + (size_t)pass * a.sort_nblk_ub * radix;
+  uint32_t bcount = 0;
+  if (tid < radix) {
+    uint32_t run = 0;
+#pragma unroll
+    for (int ww = 0; ww < kSortWaves; ++ww) {
+      const uint32_t c = cnt[ww][tid];
+      cnt[ww][tid] = run;
+      run += c;
+    }
+    bcount = run;
+    __hip_atomic_store(status + (size_t)b * radix + tid, ((uint64_t)(first ? kLbPrefix : kLbAggregate) << 32) | bcount,
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  // exclusive scans over the digits: the block's local slots, and where each
+  // digit starts in the table
+  // (one scan of both: the block's counts sum to at most SB, so they stay in
+  // the low 32 bits)
+  int64_t total;
+  const int64_t both =
+      block_exclusive_scan<kSortThreads>(((int64_t)tcount << 32) | (int64_t)bcount, part, total);
+  const int32_t lo = (int32_t)(both & 0xFFFFFFFF);
+  const int32_t tb = (int32_t)(both >> 32);
+  if (tid < radix) loff[tid] = lo;
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) stage[loff[dg[i]] + cnt[w][dg[i]] + rk[i]] = e[i];
+  // look-back: the digit's count over the table's blocks before this one,
+  // kLookBack predecessors' status words per round trip, nearest first; the
+  // table's first block (jmin) holds a prefix, so the walk stops there
+  if (tid < radix) {
+    uint32_t before = 0;
+    if (!first) {
+      const int32_t jmin = b - (sb.y - sb.w) / a.sort_block;
+      int32_t j = b - 1;
+      for (bool done = false; !done;) {
+        uint64_t x[kLookBack];
+#pragma unroll
+        for (int u = 0; u < kLookBack; ++u) {
+          const int32_t jj = j - u > jmin ? j - u : jmin;
+          x[u] = __hip_atomic_load(status + (size_t)jj * radix + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        int ready = kLookBack;  // the nearest predecessor not yet published
+#pragma unroll
+        for (int u = 0; u < kLookBack; ++u) {
+          if (!done && ready == kLookBack) {
+            if ((x[u] >> 32) == 0) {
+              ready = u;
+            } else {
+              before += (uint32_t)x[u];
+              done = (x[u] >> 32) == kLbPrefix;
+            }
+          }
+        }
+        if (done) break;
+        j -= ready;
+        if (ready < kLookBack) {
+          // wait for block j (bounded), then read on from it
+          const uint64_t *sj = status + (size_t)j * radix + tid;
+          uint64_t y = __hip_atomic_load(sj, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          for (int spin = 0; (y >> 32) == 0 && spin < kSortSpinLimit; ++spin) {
+            __builtin_amdgcn_s_sleep(1);
+            y = __hip_atomic_load(sj, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+          if ((y >> 32) == 0) {
+            atomicOr(a.ctx.err, kErrSortWait);
+            break;
+          }
+        }
+      }
+      __hip_atomic_store(status + (size_t)b * radix + tid, ((uint64_t)kLbPrefix << 32) | (before + bcount),
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    goff[tid] = sb.w + tb + (int32_t)before - lo;
+  }
+  __syncthreads();
+  // store in local order: consecutive slots of one digit go to consecutive
+  // positions
+  const bool last = pass == a.sort_passes - 1;
+  E *dst = static_cast<E *>(a.elems[(pass + 1) & 1]);
+  uint32_t key_base = 0, rows = 0, bag_base = 0;
+  if (last) {
+    key_base = a.meta[sb.x].key_base;
+    rows = (uint32_t)a.meta[sb.x].num_rows;
+    bag_base = (uint32_t)sb.x * (uint32_t)a.batch;
+  }
+#pragma unroll 4
+  for (int i = 0; i < IPT; ++i) {
+    const int k = i * kSortThreads + tid;
+    if (k < n) {
+      const E x = stage[k];
+      const int32_t out = goff[(uint32_t)(x >> shift) & dmask] + k;
+      if (!last) {
+        dst[out] = x;
+      } else {
+        // the row (the sentinel for an index outside the table) and the bag
+        // id or position; a value out of range, which only positions the
+        // keys kernel never wrote (broken offsets) can hold, gets the
+        // sentinel row, which later steps skip
+        uint32_t row = elem_row<E>(a, x);
+        uint32_t v = (uint32_t)x & a.sort_vmask;
+        const bool bad = a.sorted_bags ? v >= (uint32_t)a.batch : (int64_t)v >= a.num_indices;
+        if (row > rows || bad) {
+          row = rows;
+          v = 0;
+        }
+        const_cast<uint32_t *>(a.skeys)[out] = key_base + row;
+        const_cast<uint32_t *>(a.spos)[out] = a.sorted_bags ? bag_base + v : v;
+      }
+    }
+  }
+}
+
+// One pass: the sort blocks of workgroup blockIdx.x, each partitioned by
+// digit `pass` of the row.  Element k of a block (position start + k) is item
+// k / 64 % IPT of wave k / (64 * IPT), lane k % 64; the block's stable order
+// is k.
+template <typename E, int IPT>
+__global__ __launch_bounds__(kSortThreads) void eb_bwd_sort_pass_kernel(BwdArgs a, int32_t pass) {
+  constexpr int SB = kSortThreads * IPT;
+  __shared__ E stage[SB];
+  __shared__ uint32_t cnt[kSortWaves][kSortRadixMax];  // per wave: digit counts, then counts of earlier waves
+  __shared__ int32_t loff[kSortRadixMax];               // first local slot of each digit
+  __shared__ int32_t goff[kSortRadixMax];               // output position of a digit's local slot 0
+  __shared__ int64_t part[2 * kSortWaves];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int32_t nblk = *a.sort_nblocks;
+  for (int32_t b = blockIdx.x; b < nblk; b += gridDim.x) {
+    sort_block<E, IPT>(a, pass, b, stage, cnt, loff, goff, part, tid, lane, w);
   }
 }
 
@@ -826,23 +1140,88 @@ void *scratch_address(int device) {
   return g_scratch_ptr[device];
 }
 
+// Elements per thread of the sort's pass kernels, and the kernels (32-bit
+// elements, then 64-bit, each by kSortItems).
+constexpr int kSortItems[4] = {4, 8, 12, 16};
+void (*const kSortPass[8])(BwdArgs, int32_t) = {
+    eb_bwd_sort_pass_kernel<uint32_t, 4>,  eb_bwd_sort_pass_kernel<uint32_t, 8>,
+    eb_bwd_sort_pass_kernel<uint32_t, 12>, eb_bwd_sort_pass_kernel<uint32_t, 16>,
+    eb_bwd_sort_pass_kernel<uint64_t, 4>,  eb_bwd_sort_pass_kernel<uint64_t, 8>,
+    eb_bwd_sort_pass_kernel<uint64_t, 12>, eb_bwd_sort_pass_kernel<uint64_t, 16>};
+
+// Workgroups of sort pass kernel `which` that device `device` holds at once
+// (its compute units times the kernel's occupancy per unit), and its compute
+// units; looked up once per device and kernel.
+std::atomic<int64_t> g_resident[kMaxScratchDevices][8];
+std::atomic<int32_t> g_cus[kMaxScratchDevices];
+
+hipError_t resident_grid(int device, int which, int64_t *grid, int32_t *cus) {
+  if (device < 0 || device >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  int64_t g = g_resident[device][which].load(std::memory_order_relaxed);
+  int32_t c = g_cus[device].load(std::memory_order_relaxed);
+  if (g <= 0 || c <= 0) {
+    int n = 0, per_cu = 0;
+    hipError_t e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, device);
+    if (e == hipSuccess)
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(kSortPass[which]),
+                                                       kSortThreads, 0);
+    if (e != hipSuccess) return e;
+    c = n > 0 ? n : 1;
+    g = (int64_t)c * (per_cu > 0 ? per_cu : 1);
+    g_resident[device][which].store(g, std::memory_order_relaxed);
+    g_cus[device].store(c, std::memory_order_relaxed);
+  }
+  *grid = g;
+  *cus = c;
+  return hipSuccess;
+}
+
+// Elements per thread of this call's sort (kernel `which`, sort blocks of
+// 512 * items positions, `grid` workgroups): the fewest rounds of resident
+// workgroups over the blocks; among those, the largest blocks that still
+// give every compute unit one (fewer blocks shorten the look-back and cost
+// less per block, but a block per unit keeps the GPU busy).
+hipError_t choose_sort_items(const eb_tables *h, int64_t n, bool wide, int *which, int64_t *nblk_ub,
+                             int64_t *grid) {
+  int64_t best_rounds = -1;
+  for (int c = 0; c < 4; ++c) {
+    if (h->bwd_sort_items > 0 && kSortItems[c] != h->bwd_sort_items) continue;
+    const int k = (wide ? 4 : 0) + c;
+    const int64_t sb = (int64_t)kSortThreads * kSortItems[c];
+    const int64_t blocks = (n + sb - 1) / sb + h->num_tables;
+    int64_t g = 0;
+    int32_t cus = 0;
+    const hipError_t e = resident_grid(h->device, k, &g, &cus);
+    if (e != hipSuccess) return e;
+    const int64_t rounds = (blocks + g - 1) / g;
+    if (best_rounds < 0 || rounds < best_rounds || (rounds == best_rounds && blocks >= cus)) {
+      best_rounds = rounds;
+      *which = k;
+      *nblk_ub = blocks;
+      *grid = g < blocks ? g : blocks;
+    }
+  }
+  return best_rounds < 0 ? hipErrorInvalidValue : hipSuccess;
+}
+
 // Workspace regions (each 256-byte aligned).
 struct BwdLayout {
-  size_t keys, skeys, spos, bag_of, tile_start, tile_info, carry, sort_tmp, total;
-  size_t sort_bytes;
+  size_t elems[2], bag_of, tile_start, tile_info, carry, sblocks, nblocks, zero, total;
+  size_t hist_bytes;  // the digit counts at `zero`; the look-back status follows
   int64_t tiles_ub;
   int32_t tile_size;
+  // the sort
+  int32_t row_bits, passes, bits;
+  int64_t nblk_max;
 };
 
 inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
-// Bits the largest sort key of handle h needs.
-unsigned key_bits(const eb_tables *h) {
-  const TableMeta &last = h->h_meta[h->num_tables - 1];
-  const uint64_t max_key = (uint64_t)last.key_base + (uint64_t)last.num_rows;
-  unsigned bits = 1;
-  while (bits < 32 && (max_key >> bits) != 0) ++bits;
-  return bits;
+// Bits of x (0 for 0).
+unsigned bit_width(uint64_t x) {
+  unsigned b = 0;
+  while (b < 64 && (x >> b) != 0) ++b;
+  return b;
 }
 
 eb_status layout(const eb_tables *h, int64_t n, BwdLayout *L) {
@@ -854,29 +1233,23 @@ eb_status layout(const eb_tables *h, int64_t n, BwdLayout *L) {
   if (h->bwd_tile_chunks > 0) chunks = h->bwd_tile_chunks;
   L->tile_size = (int32_t)(64 * chunks);
   L->tiles_ub = (n + L->tile_size - 1) / L->tile_size + h->num_tables;
-  size_t sort_bytes = 0;
-  if (n > 0) {
-    // scratch for either kind of value sorted with the keys (positions, or bag ids)
-    size_t by_pos = 0, by_bag = 0;
-    hipError_t e = rocprim::radix_sort_pairs<SortConfig>(nullptr, by_pos, static_cast<const uint32_t *>(nullptr),
-                                             static_cast<uint32_t *>(nullptr), rocprim::counting_iterator<uint32_t>(0),
-                                             static_cast<uint32_t *>(nullptr), (unsigned int)n, 0, key_bits(h),
-                                             h->stream);
-    if (e == hipSuccess)
-      e = rocprim::radix_sort_pairs<SortConfig>(nullptr, by_bag, static_cast<const uint32_t *>(nullptr),
-                                    static_cast<uint32_t *>(nullptr), static_cast<const uint32_t *>(nullptr),
-                                    static_cast<uint32_t *>(nullptr), (unsigned int)n, 0, key_bits(h), h->stream);
-    if (e != hipSuccess) return EB_ERR_HIP;
-    sort_bytes = by_pos > by_bag ? by_pos : by_bag;
-  }
-  L->sort_bytes = sort_bytes;
+  // The sort: rows up to the largest table's sentinel (its row count), in as
+  // few passes of at most 9 bits as cover them, split evenly.
+  int64_t max_rows = 0;
+  for (int32_t t = 0; t < h->num_tables; ++t)
+    max_rows = h->h_meta[t].num_rows > max_rows ? h->h_meta[t].num_rows : max_rows;
+  L->row_bits = (int32_t)bit_width((uint64_t)max_rows);
+  if (L->row_bits < 1) L->row_bits = 1;
+  L->passes = (L->row_bits + 8) / 9;
+  L->bits = (L->row_bits + L->passes - 1) / L->passes;
+  // sized for the smallest sort block (the most blocks); a call uses a part
+  L->nblk_max = (n + kSortThreads * kSortItems[0] - 1) / (kSortThreads * kSortItems[0]) + h->num_tables;
+  const size_t radix = (size_t)1 << L->bits;
   size_t off = 0;
-  L->keys = off;
-  off += align256(4 * (size_t)n);
-  L->skeys = off;
-  off += align256(4 * (size_t)n);
-  L->spos = off;
-  off += align256(4 * (size_t)n);
+  for (int i = 0; i < 2; ++i) {  // 8 bytes per element: 64-bit elements, or the sorted keys and values
+    L->elems[i] = off;
+    off += align256(8 * (size_t)n);
+  }
   L->bag_of = off;
   off += align256(4 * (size_t)n);
   L->tile_start = off;
@@ -885,8 +1258,14 @@ eb_status layout(const eb_tables *h, int64_t n, BwdLayout *L) {
   off += align256(8 * (size_t)L->tiles_ub);
   L->carry = off;
   off += align256(4 * (size_t)2 * L->tiles_ub * h->max_dim);
-  L->sort_tmp = off;
-  off += align256(sort_bytes);
+  L->sblocks = off;
+  off += align256(16 * (size_t)L->nblk_max);
+  L->nblocks = off;
+  off += 256;
+  // cleared by the keys kernel: digit counts, look-back status
+  L->zero = off;
+  L->hist_bytes = align256(4 * (size_t)h->num_tables * L->passes * radix);
+  off += L->hist_bytes + align256(8 * (size_t)L->passes * L->nblk_max * radix);
   L->total = off;
   return EB_OK;
 }
@@ -986,10 +1365,13 @@ eb_status backward_update(const eb_tables *h, eb_tensor indices, eb_tensor offse
   a.weights = static_cast<const float *>(per_sample_weights.data);
   a.grad = static_cast<const float *>(grad_out.data);
   a.state = static_cast<float *>(const_cast<void *>(optimizer_state.data));
-  a.keys = reinterpret_cast<uint32_t *>(ws + L.keys);
   a.bag_of = reinterpret_cast<int32_t *>(ws + L.bag_of);
-  a.skeys = reinterpret_cast<const uint32_t *>(ws + L.skeys);
-  a.spos = reinterpret_cast<const uint32_t *>(ws + L.spos);
+  // pass q reads elems[q % 2] and writes elems[(q + 1) % 2]; the last pass
+  // writes the sorted keys and values into the buffer it does not read
+  a.elems[0] = ws + L.elems[0];
+  a.elems[1] = ws + L.elems[1];
+  a.skeys = reinterpret_cast<const uint32_t *>(ws + L.elems[L.passes % 2]);
+  a.spos = a.skeys + n;
   a.tile_start = reinterpret_cast<int32_t *>(ws + L.tile_start);
   a.tile_info = reinterpret_cast<uint64_t *>(ws + L.tile_info);
   a.carry = reinterpret_cast<float *>(ws + L.carry);
@@ -1007,6 +1389,32 @@ eb_status backward_update(const eb_tables *h, eb_tensor indices, eb_tensor offse
   a.tile_size = L.tile_size;
   a.max_dim = h->max_dim;
   a.xcd_remap = h->bwd_xcd_remap;
+  a.sblocks = reinterpret_cast<int4 *>(ws + L.sblocks);
+  a.sort_nblocks = reinterpret_cast<int32_t *>(ws + L.nblocks);
+  a.zero = reinterpret_cast<uint4 *>(ws + L.zero);
+  a.hist = reinterpret_cast<uint32_t *>(ws + L.zero);
+  a.status = reinterpret_cast<uint64_t *>(ws + L.zero + L.hist_bytes);
+  a.sort_passes = L.passes;
+  a.sort_bits = L.bits;
+  {
+    // an element holds the row above the value (table-local bag id, or
+    // position): in 32 bits when both fit
+    const int32_t vbits = (int32_t)bit_width(weighted ? (uint64_t)(n - 1) : (uint64_t)(batch - 1));
+    a.sort_wide = L.row_bits + vbits > 32 ? 1 : 0;
+    a.sort_vshift = a.sort_wide ? 32 : vbits;
+    a.sort_vmask = a.sort_wide ? 0xFFFFFFFFu : (uint32_t)(((uint64_t)1 << vbits) - 1);
+  }
+  int sort_kernel = 0;
+  int64_t sort_nblk = 0, sort_grid = 0;
+  if (choose_sort_items(h, n, a.sort_wide != 0, &sort_kernel, &sort_nblk, &sort_grid) != hipSuccess) {
+    if (cur != h->device) (void)hipSetDevice(cur);
+    return EB_ERR_HIP;
+  }
+  a.sort_block = kSortThreads * kSortItems[sort_kernel % 4];
+  a.sort_nblk_ub = (int32_t)sort_nblk;
+  // the keys kernel clears the digit counts and this call's part of the
+  // look-back status
+  a.zero_words = (int64_t)((L.hist_bytes + 8 * (size_t)L.passes * sort_nblk * ((size_t)1 << L.bits) + 15) / 16);
   int64_t k = 1;
   {
     const int64_t per_slot = num_bags / kResidentWaves;
@@ -1025,19 +1433,16 @@ eb_status backward_update(const eb_tables *h, eb_tensor indices, eb_tensor offse
     hipLaunchKernelGGL(eb_bwd_keys_kernel, dim3(grid), dim3(kBlock), 0, h->stream, a);
     e = hipGetLastError();
   }
-  // 2. sort (key, bag id) pairs, or (key, position) pairs when the weights
-  //    (per position) are needed, on the bits the largest key needs
+  // 2. sort: digit counts, then one pass per digit
   if (e == hipSuccess) {
-    const unsigned end_bit = key_bits(h);
-    size_t tmp = L.sort_bytes;
-    if (a.sorted_bags)
-      e = rocprim::radix_sort_pairs<SortConfig>(ws + L.sort_tmp, tmp, a.keys, const_cast<uint32_t *>(a.skeys),
-                                    reinterpret_cast<const uint32_t *>(a.bag_of), const_cast<uint32_t *>(a.spos),
-                                    (unsigned int)n, 0, end_bit, h->stream);
-    else
-      e = rocprim::radix_sort_pairs<SortConfig>(ws + L.sort_tmp, tmp, a.keys, const_cast<uint32_t *>(a.skeys),
-                                    rocprim::counting_iterator<uint32_t>(0), const_cast<uint32_t *>(a.spos),
-                                    (unsigned int)n, 0, end_bit, h->stream);
+    const unsigned hgrid = (unsigned)((sort_nblk + kHistBlocksPerGroup - 1) / kHistBlocksPerGroup);
+    hipLaunchKernelGGL(a.sort_wide ? eb_bwd_sort_hist_kernel<uint64_t> : eb_bwd_sort_hist_kernel<uint32_t>,
+                       dim3(hgrid), dim3(kHistThreads), 0, h->stream, a);
+    e = hipGetLastError();
+  }
+  for (int32_t q = 0; q < L.passes && e == hipSuccess; ++q) {
+    hipLaunchKernelGGL(kSortPass[sort_kernel], dim3((unsigned)sort_grid), dim3(kSortThreads), 0, h->stream, a, q);
+    e = hipGetLastError();
   }
   // 3. tiles: pool and update (the first tile of each table came with the keys)
   const unsigned tgrid = (unsigned)((L.tiles_ub + kTileWaves - 1) / kTileWaves);
@@ -1066,6 +1471,7 @@ eb_status backward_update(const eb_tables *h, eb_tensor indices, eb_tensor offse
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
     if (e == hipSuccess && (herr & kErrOffsets)) st = EB_ERR_OFFSETS;
     else if (e == hipSuccess && (herr & kErrIndex)) st = EB_ERR_INDEX_OOB;
+    else if (e == hipSuccess && (herr & kErrSortWait)) st = EB_ERR_HIP;
   }
   if (e != hipSuccess) st = EB_ERR_HIP;
   if (cur != h->device) (void)hipSetDevice(cur);

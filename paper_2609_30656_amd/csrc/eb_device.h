@@ -46,6 +46,7 @@ constexpr int32_t kRemapMaxTables = 32;
 constexpr int kErrIndex = 1;
 constexpr int kErrOffsets = 2;
 constexpr int kErrOutSize = 4;  // an output row would fall outside the output
+constexpr int kErrSortWait = 8;  // a sort block gave up waiting for its predecessor's counts
 
 enum : int32_t { kF32 = 0, kF16 = 1, kU8 = 2 };
 
@@ -542,6 +543,7 @@ struct eb_tables {
   int64_t sum_dim;
   int32_t backward_ok;    // every table fp32/fp16 with dim <= 256, sort keys fit in 32 bits
   int32_t bwd_tile_chunks;  // 0: chosen per call; else backward tiles of this many 64-position chunks
+  int32_t bwd_sort_items;   // 0: chosen per call; else 4, 8, 12 or 16 elements per thread of the backward's sort
   int32_t bwd_xcd_remap;    // backward tiles in XCD-contiguous order
   int32_t max_dim;
   int32_t uniform_dim;    // the dim every table shares, or 0 if they differ

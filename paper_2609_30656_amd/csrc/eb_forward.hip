@@ -723,6 +723,10 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   const char *btc = getenv("EB_BWD_TILE_CHUNKS");
   h->bwd_tile_chunks = btc ? atoi(btc) : 0;
   if (h->bwd_tile_chunks < 0 || h->bwd_tile_chunks > 16) h->bwd_tile_chunks = 0;
+  const char *bsi = getenv("EB_BWD_SORT_ITEMS");
+  h->bwd_sort_items = bsi ? atoi(bsi) : 0;
+  if (h->bwd_sort_items != 4 && h->bwd_sort_items != 8 && h->bwd_sort_items != 12 && h->bwd_sort_items != 16)
+    h->bwd_sort_items = 0;
   const char *lb = getenv("EB_LONG_BAG");
   h->long_bag_len = lb ? atoll(lb) : 0;
   if (h->long_bag_len < 0) h->long_bag_len = 0;
