@@ -402,12 +402,19 @@ __device__ __forceinline__ void sort_block(const BwdArgs &a, int32_t pass, int32
     for (int u = 0; u < 4; ++u) {
       const int i = i0 + u;
       dg[i] = (uint32_t)(e[i] >> shift) & dmask;
-      uint64_t peers = ~0ull;
+      // a lane keeps the lanes whose bit q equals its own: the ballot of bit
+      // q, complemented where the lane's bit is 0 (m: the bit copied into
+      // every bit of a word)
+      uint32_t plo = ~0u, phi = ~0u;
       for (int q = 0; q < bits; ++q) {
-        const bool bit = (dg[i] >> q) & 1u;
-        const uint64_t bal = __ballot(bit);
-        peers &= bit ? bal : ~bal;
+        const uint32_t m = (uint32_t)((int32_t)(dg[i] << (31 - q)) >> 31);
+        const uint64_t bal = __ballot(m != 0u);
+        // p & ~(ballot ^ m) as one three-input bitwise operation per half
+        // (truth table 0x90: inputs p, ballot, m)
+        plo = __builtin_amdgcn_bitop3_b32(plo, (uint32_t)bal, m, 0x90);
+        phi = __builtin_amdgcn_bitop3_b32(phi, (uint32_t)(bal >> 32), m, 0x90);
       }
+      const uint64_t peers = ((uint64_t)phi << 32) | plo;
       const uint64_t below = peers & below_me;
       rk[i] = (uint32_t)__builtin_popcountll(below);
       lead[u] = (uint32_t)__builtin_ctzll(peers);
@@ -443,10 +450,14 @@ __device__ __forceinline__ void sort_block(const BwdArgs &a, int32_t pass, int32
       block_exclusive_scan<kSortThreads>(((int64_t)tcount << 32) | (int64_t)bcount, part, total);
   const int32_t lo = (int32_t)(both & 0xFFFFFFFF);
   const int32_t tb = (int32_t)(both >> 32);
+  const int32_t table_end = sb.w + (int32_t)(total >> 32);  // the table's element count is its digits' total
   if (tid < radix) loff[tid] = lo;
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < IPT; ++i) stage[loff[dg[i]] + cnt[w][dg[i]] + rk[i]] = e[i];
+  for (int i = 0; i < IPT; ++i) {
+    const uint32_t slot = (uint32_t)loff[dg[i]] + cnt[w][dg[i]] + rk[i];
+    if (slot < (uint32_t)(kSortThreads * IPT)) stage[slot] = e[i];  // always: the ranks are a permutation of the block
+  }
   // look-back: the digit's count over the table's blocks before this one,
   // kLookBack predecessors' status words per round trip, nearest first; the
   // table's first block (jmin) holds a prefix, so the walk stops there
@@ -512,6 +523,7 @@ __device__ __forceinline__ void sort_block(const BwdArgs &a, int32_t pass, int32
     if (k < n) {
       const E x = stage[k];
       const int32_t out = goff[(uint32_t)(x >> shift) & dmask] + k;
+      if (out < sb.w || out >= table_end) continue;  // never: counts and ranks agree
       if (!last) {
         dst[out] = x;
       } else {
