@@ -294,7 +294,6 @@ __global__ __launch_bounds__(kBlock) void eb_bwd_keys_kernel(BwdArgs a) {
 // bounded besides, so that a wait that never ended would raise kErrSortWait
 // and let the workgroup go on rather than hang.
 constexpr int kHistThreads = 512;
-constexpr int kHistBlocksPerGroup = 1;  // sort blocks a histogram workgroup counts
 constexpr uint32_t kLbAggregate = 1;    // status word: the block's own counts
 constexpr uint32_t kLbPrefix = 2;       // ... counts of every block of the table up to and including it
 constexpr int kSortSpinLimit = 1 << 18;
@@ -308,59 +307,55 @@ __device__ __forceinline__ uint32_t elem_row(const BwdArgs &a, E e) {
 }
 
 // Digit counts of each table for every pass, from the elements in position
-// order: a workgroup counts kHistBlocksPerGroup consecutive sort blocks in
-// LDS and adds its counts to the table's (integer additions: the totals do
-// not depend on their order).
+// order: one workgroup per sort block counts in LDS, with all of the block's
+// loads in flight at once, and adds its counts to the table's (integer
+// additions: the totals do not depend on their order).
 template <typename E>
 __global__ __launch_bounds__(kHistThreads) void eb_bwd_sort_hist_kernel(BwdArgs a) {
+  constexpr int U = 16;  // a block's elements per thread
   __shared__ uint32_t h[kSortMaxPasses * kSortRadixMax];
   const int tid = threadIdx.x;
   const int np = a.sort_passes, bits = a.sort_bits, radix = 1 << bits;
   const uint32_t dmask = (uint32_t)radix - 1u;
   const int nh = np * radix;
   for (int i = tid; i < nh; i += kHistThreads) h[i] = 0u;
-  const int32_t nblk = *a.sort_nblocks;
-  const int32_t b0 = (int32_t)blockIdx.x * kHistBlocksPerGroup;
-  const int32_t b1 = b0 + kHistBlocksPerGroup < nblk ? b0 + kHistBlocksPerGroup : nblk;
+  const int32_t b = blockIdx.x;
+  if (b >= *a.sort_nblocks) return;
+  const int4 sb = a.sblocks[b];
   const E *src = static_cast<const E *>(a.elems[0]);
-  int32_t cur = -1;  // table whose counts h holds (the same in every thread)
-  auto flush = [&]() {
-    __syncthreads();
-    uint32_t *g = a.hist + (size_t)cur * nh;
-    for (int i = tid; i < nh; i += kHistThreads) {
-      const uint32_t v = h[i];
-      if (v) {
-        atomicAdd(g + i, v);
-        h[i] = 0u;
-      }
-    }
-    __syncthreads();
-  };
   __syncthreads();
-  constexpr int U = 8;
-  for (int32_t b = b0; b < b1; ++b) {
-    const int4 sb = a.sblocks[b];
-    if (sb.x != cur) {
-      if (cur >= 0) flush();
-      cur = sb.x;
+  for (int32_t p = sb.y + tid; p < sb.z; p += U * kHistThreads) {
+    E e[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int32_t q = p + u * kHistThreads;
+      e[u] = src[q < sb.z ? q : p];
     }
-    for (int32_t p = sb.y + tid; p < sb.z; p += U * kHistThreads) {
-      E e[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int32_t q = p + u * kHistThreads;
-        e[u] = src[q < sb.z ? q : p];
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (p + u * kHistThreads < sb.z) {
-          const uint32_t row = elem_row<E>(a, e[u]);
-          for (int q = 0; q < np; ++q) atomicAdd(&h[q * radix + ((row >> (q * bits)) & dmask)], 1u);
-        }
+    for (int u = 0; u < U; ++u) {
+      if (p + u * kHistThreads < sb.z) {
+        const uint32_t row = elem_row<E>(a, e[u]);
+        const uint64_t below = (1ull << (threadIdx.x & (kWave - 1))) - 1ull;
+        for (int q = 0; q + 1 < np; ++q) atomicAdd(&h[q * radix + ((row >> (q * bits)) & dmask)], 1u);
+        // the top digit: the lanes that share the first active lane's (often
+        // most of them: a small table's rows, a power-law's low rows) add
+        // once together; lanes that add to one LDS word in one instruction
+        // take turns
+        const int q = np - 1;
+        const uint32_t d = (row >> (q * bits)) & dmask;
+        const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
+        const uint64_t same = __ballot(d == d0);
+        if (d != d0) atomicAdd(&h[q * radix + d], 1u);
+        else if ((same & below) == 0) atomicAdd(&h[q * radix + d0], (uint32_t)__builtin_popcountll(same));
       }
     }
   }
-  if (cur >= 0) flush();
+  __syncthreads();
+  uint32_t *g = a.hist + (size_t)sb.x * nh;
+  for (int i = tid; i < nh; i += kHistThreads) {
+    const uint32_t v = h[i];
+    if (v) atomicAdd(g + i, v);
+  }
 }
 
 // Sort block b of a pass (the body of eb_bwd_sort_pass_kernel's loop).
@@ -368,6 +363,7 @@ template <typename E, int IPT>
 __device__ __forceinline__ void sort_block(const BwdArgs &a, int32_t pass, int32_t b, E *stage,
                                            uint32_t (*cnt)[kSortRadixMax], int32_t *loff, int32_t *goff,
                                            int64_t *part, int tid, int lane, int w) {
+  __syncthreads();  // the previous block's reads of LDS are done
   for (int i = tid; i < kSortWaves * kSortRadixMax; i += kSortThreads) (&cnt[0][0])[i] = 0;
   __syncthreads();
   const int4 sb = a.sblocks[b];  // {table, start, end, table's first position}
@@ -550,7 +546,10 @@ __device__ __forceinline__ void sort_block(const BwdArgs &a, int32_t pass, int32
 // k / 64 % IPT of wave k / (64 * IPT), lane k % 64; the block's stable order
 // is k.
 template <typename E, int IPT>
-__global__ __launch_bounds__(kSortThreads) void eb_bwd_sort_pass_kernel(BwdArgs a, int32_t pass) {
+// (12 elements per thread: held to 128 VGPRs, 4 waves per SIMD, so that two
+// workgroups share a compute unit; the compiler's own choice was 135, one.)
+__global__ __launch_bounds__(kSortThreads) __attribute__((amdgpu_waves_per_eu(IPT == 12 ? 4 : 1, 8)))
+void eb_bwd_sort_pass_kernel(BwdArgs a, int32_t pass) {
   constexpr int SB = kSortThreads * IPT;
   __shared__ E stage[SB];
   __shared__ uint32_t cnt[kSortWaves][kSortRadixMax];  // per wave: digit counts, then counts of earlier waves
@@ -1447,7 +1446,7 @@ eb_status backward_update(const eb_tables *h, eb_tensor indices, eb_tensor offse
   }
   // 2. sort: digit counts, then one pass per digit
   if (e == hipSuccess) {
-    const unsigned hgrid = (unsigned)((sort_nblk + kHistBlocksPerGroup - 1) / kHistBlocksPerGroup);
+    const unsigned hgrid = (unsigned)sort_nblk;
     hipLaunchKernelGGL(a.sort_wide ? eb_bwd_sort_hist_kernel<uint64_t> : eb_bwd_sort_hist_kernel<uint32_t>,
                        dim3(hgrid), dim3(kHistThreads), 0, h->stream, a);
     e = hipGetLastError();
