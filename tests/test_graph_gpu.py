@@ -1,7 +1,8 @@
-"""The lookups under HIP graph capture: eb_forward, eb_forward_fm and
-eb_forward_seq allocate nothing and (outside checked mode) enqueue only
-kernels on the handle's stream, so a caller can capture them once and replay
-them.  Each test captures one call on the handle's stream, then replays it
+"""The lookups and the backward under HIP graph capture: eb_forward,
+eb_forward_fm, eb_forward_seq and the backward (given a workspace, or its
+no-allocation entry point) allocate nothing and (outside checked mode)
+enqueue only kernels on the handle's stream, so a caller can capture them
+once and replay them.  Each test captures one call on the handle's stream, then replays it
 several times, with eager work of the program and synchronisations between the
 replays and new index contents copied into the captured buffers, and checks
 every replay bit for bit against an eager call on the same inputs (the kernels
@@ -123,3 +124,66 @@ def test_sequence_lookup_replays(dev, name):
             return (torch.empty(w.seq_output_numel(), device=dev),)
 
         _replay_and_check(run_into, fresh, w, idx2, stream, f"seq {name}")
+
+
+def _clone_tables(tables):
+    from paper_2609_30656_amd.workload import Table
+    return [Table(t.rows.clone(), t.dim, t.dtype) for t in tables]
+
+
+@pytest.mark.parametrize("name,entry", [("c2", "workspace"), ("c3b", "workspace"), ("c2", "noalloc")])
+def test_backward_replays(dev, name, entry):
+    """The backward with row-wise Adagrad under capture: outside checked mode
+    eb_backward_update (given a workspace) and eb_backward_update_noalloc
+    enqueue only kernels, and its sort clears its own counters with a kernel.
+    Replays of a captured step, fed new indices and gradients through the
+    captured buffers, must leave the tables and the optimizer state bit for
+    bit where the same eager calls on a copy leave them."""
+    say(f"[graph] backward {name} {entry}")
+    w, idx2 = _batches(name, dev)
+    stream = torch.cuda.Stream(device=dev)
+    tabs_g, tabs_e = _clone_tables(w.tables), _clone_tables(w.tables)
+    R = sum(t.num_rows for t in w.tables)
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    st_g = torch.rand(R, generator=g, device=dev)
+    st_e = st_g.clone()
+    grads = [torch.randn((w.batch, w.sum_dim), generator=g, device=dev) for _ in range(5)]
+    idx_buf, grad_buf = w.indices.clone(), grads[0].clone()
+    with eb.eb_create_tables(tabs_g, stream) as hg, eb.eb_create_tables(tabs_e, stream) as he:
+        ws = torch.empty(eb.eb_backward_workspace_size(hg, w.num_indices), dtype=torch.uint8, device=dev)
+        ws_e = torch.empty_like(ws)
+
+        def step(h, idx, grad, st, workspace):
+            if entry == "noalloc":
+                eb.eb_backward_update_noalloc(h, idx, w.offsets, w.weights, w.pooling, grad, "rowwise_adagrad",
+                                              0.05, 1e-4, st)
+            else:
+                eb.eb_backward_update(h, idx, w.offsets, w.weights, w.pooling, grad, "rowwise_adagrad", 0.05,
+                                      1e-4, st, workspace=workspace)
+
+        # warm-up on the capture stream, matched by the same eager step on the copy
+        with torch.cuda.stream(stream):
+            step(hg, idx_buf, grad_buf, st_g, ws)
+            step(he, w.indices, grads[0], st_e, ws_e)
+        stream.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            step(hg, idx_buf, grad_buf, st_g, ws)
+        for rep, (src, grad) in enumerate(zip([w.indices, idx2, w.indices, idx2], grads[1:])):
+            idx_buf.copy_(src)
+            grad_buf.copy_(grad)
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            with torch.cuda.stream(stream):
+                step(he, src, grad, st_e, ws_e)
+            junk = torch.randn(1 << 20, device=dev).sum()  # eager work of the program between replays
+            torch.cuda.synchronize()
+            for t, (a, b) in enumerate(zip(tabs_g, tabs_e)):
+                assert torch.equal(a.rows.view(torch.uint8), b.rows.view(torch.uint8)), \
+                    f"backward {name} {entry}: replay {rep} table {t} differs"
+            assert torch.equal(st_g.view(torch.int32), st_e.view(torch.int32)), \
+                f"backward {name} {entry}: replay {rep} optimizer state differs"
+            assert torch.isfinite(junk)
+        del graph
