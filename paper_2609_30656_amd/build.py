@@ -12,6 +12,9 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 SOURCES = [os.path.join(CSRC, f) for f in ("eb_forward.hip", "eb_fm.hip", "eb_seq.hip", "eb_backward.hip") if os.path.exists(os.path.join(CSRC, f))]
+# the random-row gather rate measurement (a program of its own, not part of libeb.so)
+GATHER_SRC = os.path.join(CSRC, "gather_ceiling.hip")
+GATHER_BIN = os.path.join(PKG, "gather_ceiling")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libeb.so")
 
@@ -39,6 +42,20 @@ def build(verbose: bool = False, extra_flags=()) -> str:
     return LIB
 
 
+def build_gather_ceiling(verbose: bool = False) -> str:
+    """Compile the gather_ceiling measurement program next to libeb.so."""
+    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    flags = [f for f in HIPCC_FLAGS if f not in ("-shared", "-fPIC")]
+    tmp = GATHER_BIN + ".tmp"
+    cmd = [hipcc, *flags, GATHER_SRC, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, GATHER_BIN)
+    return GATHER_BIN
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_gather_ceiling(verbose=True))
     sys.exit(0)
