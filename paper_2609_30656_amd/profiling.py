@@ -5,10 +5,10 @@
 runs, one after another (each under its own time limit):
   1. a kernel trace of `bench.py` (--kernel-trace --stats): per-launch duration;
   2. three counter passes of `bench.py --copy-calibration`, one counter set
-     each: FETCH_SIZE, WRITE_SIZE, and TCC_HIT_sum + TCC_MISS_sum.  The 1 GiB
-     device-to-device copy at the end of each run reads the same counters, which
-     scales counter KiB to bytes (gfx950 issues 128-byte read requests that
-     FETCH_SIZE counts as 64 bytes).  The counts are L2<->fabric traffic, so
+     each: FETCH_SIZE, WRITE_SIZE, and TCC_HIT_sum + TCC_MISS_sum.  The three
+     1 GiB device-to-device copies at the end of each run (the run's last
+     copies) read the same counters, which scales counter KiB to bytes (gfx950
+     issues 128-byte read requests that FETCH_SIZE counts as 64 bytes).  The counts are L2<->fabric traffic, so
      Infinity Cache hits are included: an upper bound on HBM traffic;
 and writes profiles/<kernel>_<config>_<law>_{kernel_trace,pmc}.txt, each with
 the commands that made it and the hash of the kernel's sources, which
@@ -107,12 +107,34 @@ def _run(cmd, log, limit):
         raise SystemExit(f"[profiling] step failed with status {r.returncode}")
 
 
+def read_counters(path, kernel):
+    """Counter values of a rocprofv3 --pmc CSV: {counter: [value per launch of
+    `kernel`]} and {"copy:" + counter: [value per calibration copy]}.  The
+    calibration copies are the process's last CALIBRATION_COPIES device copies
+    (workload set-up may copy too: c5 builds its tables by copies)."""
+    acc = collections.defaultdict(list)
+    copies = collections.defaultdict(list)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            v = float(r["Counter_Value"])
+            if _match(r["Kernel_Name"], kernel):
+                acc[r["Counter_Name"]].append(v)
+            elif r["Kernel_Name"] == "__amd_rocclr_copyBuffer":
+                copies[r["Counter_Name"]].append((int(r["Dispatch_Id"]), v))
+    for name, lst in copies.items():
+        acc["copy:" + name] = [v for _, v in sorted(lst)[-CALIBRATION_COPIES:]]
+    return dict(acc)
+
+
 def _bench_line(log):
     with open(log) as f:
         for line in f:
             if line.startswith("{") and '"metric"' in line:
                 return json.loads(line)
     raise SystemExit(f"[profiling] no bench line in {log}")
+
+
+CALIBRATION_COPIES = 3  # bench.py --copy-calibration: three copies of 1 GiB, after everything else
 
 
 def _match(name, kernel):
@@ -179,13 +201,7 @@ def main(argv=None):
         cmds.append(" ".join(cmd[:cmd.index("--")]) + " -- python3 bench.py " +
                     " ".join(_bench_args(mode, cfg, law, 10, 2, True)[2:]))
         _run(cmd, os.path.join(work, f"pmc_{counters[0]}.log"), args.limit)
-        acc = collections.defaultdict(list)
-        for r in csv.DictReader(open(os.path.join(d, "pmc_counter_collection.csv"))):
-            v = float(r["Counter_Value"])
-            if _match(r["Kernel_Name"], kernel):
-                acc[r["Counter_Name"]].append(v)
-            elif r["Kernel_Name"] == "__amd_rocclr_copyBuffer" and v > 1e5:
-                acc["copy:" + r["Counter_Name"]].append(v)
+        acc = read_counters(os.path.join(d, "pmc_counter_collection.csv"), kernel)
         vals.update({k: (sum(v) / len(v), len(v)) for k, v in acc.items()})
 
     GiB = 1 << 30

@@ -53,3 +53,30 @@ def test_bench_refuses_more_than_one_gpu():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_counter_calibration_uses_the_last_copies(tmp_path):
+    # set-up copies (c5 builds its tables by copies) come before the lookup;
+    # only the run's last three copies, the 1 GiB calibration, scale the counters
+    path = tmp_path / "pmc_counter_collection.csv"
+    rows = []
+    d = 0
+
+    def add(kernel, value):
+        nonlocal d
+        d += 1
+        rows.append(f'{d},{d},"Agent 1",1,1,1,64,1,"{kernel}",256,0,0,8,0,16,"FETCH_SIZE",{value},0,1')
+
+    for _ in range(64):
+        add("__amd_rocclr_copyBuffer", 390000.0)  # table set-up
+    for _ in range(5):
+        add("void eb::(anonymous namespace)::eb_pool_kernel<2, 3, false, false>(eb::FwdArgs)", 1000.0)
+    for _ in range(3):
+        add("__amd_rocclr_copyBuffer", 524288.0)  # calibration
+    header = ('"Correlation_Id","Dispatch_Id","Agent_Id","Queue_Id","Process_Id","Thread_Id","Grid_Size",'
+              '"Kernel_Id","Kernel_Name","Workgroup_Size","LDS_Block_Size","Scratch_Size","VGPR_Count",'
+              '"Accum_VGPR_Count","SGPR_Count","Counter_Name","Counter_Value","Start_Timestamp","End_Timestamp"')
+    path.write_text(header + "\n" + "\n".join(rows) + "\n")
+    acc = profiling.read_counters(str(path), "eb_pool_kernel")
+    assert acc["FETCH_SIZE"] == [1000.0] * 5
+    assert acc["copy:FETCH_SIZE"] == [524288.0] * 3
