@@ -92,36 +92,107 @@ def run_and_check(w, dev, optimizer, lr=0.05, eps=1e-4, check_tables=None, label
         untouched[rows] = False
         raw = np.uint16 if tb.dtype == "f16" else np.uint32
         assert np.array_equal(got[untouched].view(raw), before[t][untouched].view(raw)), f"{label} t{t}: untouched rows"
+        if optimizer != "sgd":
+            assert np.array_equal(state1[base[t]:base[t + 1]][untouched], state0[base[t]:base[t + 1]][untouched])
         if rows.size == 0:
             continue
-        g64 = got[rows].astype(np.float64)
-        r64 = ref[rows].astype(np.float64)
-        dG = (n[:, None] + 8) * U * S
-        store = (2 * U * np.abs(r64)) if tb.dtype == "f32" else _ulp16(r64)
-        if optimizer == "sgd":
-            bound = lr * dG + store
-        else:
-            s_new = st_or[base[t] + rows].astype(np.float64)
-            D = tb.dim
-            ds = 2 * (np.abs(G) * dG).sum(axis=1) / D + (D + 8) * U * s_new
-            scale = lr / (np.sqrt(s_new) + eps)
-            # relative error of the step size lr / (sqrt(s) + eps) when the
-            # state is off by at most ds (valid for any ds; module docstring),
-            # plus its own roundings
-            sq, sq_lo = np.sqrt(s_new), np.sqrt(np.maximum(s_new - ds, 0.0))
-            with np.errstate(divide="ignore", invalid="ignore"):
-                rel = np.where(s_new > 0, ds / (sq + sq_lo) / (sq_lo + eps), 0.0)
-            rel = rel + 6 * U / (1 - 6 * U) * (1 + rel)
-            moved = np.any(G != 0, axis=1)  # a zero gradient moves nothing, whatever the step size
-            bound = scale[:, None] * dG + np.where(moved[:, None], np.abs(scale[:, None] * G) * rel[:, None], 0.0) \
-                + store
-            np.testing.assert_array_less(np.abs(state1[base[t] + rows] - s_new), ds + 2 * U * s_new + 1e-30)
-            assert np.array_equal(state1[base[t]:base[t + 1]][untouched], state0[base[t]:base[t + 1]][untouched])
-        err = np.abs(g64 - r64)
-        bound = bound / (1 - (n[:, None] + 16) * U)  # first order -> rigorous (module docstring)
-        bad = err > bound + 1e-30
-        assert not bad.any(), (f"{label} t{t}: {bad.sum()} elements beyond the bound; worst ratio "
-                               f"{np.max(err / np.maximum(bound, 1e-30)):.3g}")
+        _check_rows(f"{label} t{t}", tb.dtype, tb.dim, got[rows], ref[rows], G, S, n, optimizer, lr, eps,
+                    None if st_or is None else st_or[base[t] + rows],
+                    None if state1 is None else state1[base[t] + rows])
+
+
+def _check_rows(label, dtype, D, got, ref, G, S, n, optimizer, lr, eps, s_new, s_got):
+    """The bounds of the module docstring for the touched rows of one table:
+    got/ref their values after the GPU's and the oracle's step, G, S, n the
+    oracle's gradient, error scale and count, s_new/s_got the oracle's and the
+    GPU's new Adagrad state."""
+    g64 = got.astype(np.float64)
+    r64 = ref.astype(np.float64)
+    dG = (n[:, None] + 8) * U * S
+    store = (2 * U * np.abs(r64)) if dtype == "f32" else _ulp16(r64)
+    if optimizer == "sgd":
+        bound = lr * dG + store
+    else:
+        s_new = s_new.astype(np.float64)
+        ds = 2 * (np.abs(G) * dG).sum(axis=1) / D + (D + 8) * U * s_new
+        scale = lr / (np.sqrt(s_new) + eps)
+        # relative error of the step size lr / (sqrt(s) + eps) when the
+        # state is off by at most ds (valid for any ds; module docstring),
+        # plus its own roundings
+        sq, sq_lo = np.sqrt(s_new), np.sqrt(np.maximum(s_new - ds, 0.0))
+        with np.errstate(divide="ignore", invalid="ignore"):
+            rel = np.where(s_new > 0, ds / (sq + sq_lo) / (sq_lo + eps), 0.0)
+        rel = rel + 6 * U / (1 - 6 * U) * (1 + rel)
+        moved = np.any(G != 0, axis=1)  # a zero gradient moves nothing, whatever the step size
+        bound = scale[:, None] * dG + np.where(moved[:, None], np.abs(scale[:, None] * G) * rel[:, None], 0.0) \
+            + store
+        np.testing.assert_array_less(np.abs(s_got - s_new), ds + 2 * U * s_new + 1e-30)
+    err = np.abs(g64 - r64)
+    bound = bound / (1 - (n[:, None] + 16) * U)  # first order -> rigorous (module docstring)
+    bad = err > bound + 1e-30
+    assert not bad.any(), (f"{label}: {bad.sum()} elements beyond the bound; worst ratio "
+                           f"{np.max(err / np.maximum(bound, 1e-30)):.3g}")
+
+
+def run_and_check_touched(w, dev, optimizer, lr=0.05, eps=1e-4, label="", samples=200000):
+    """run_and_check for tables too large to copy whole: the oracle steps
+    compact tables holding only the rows the batch touches (the indices
+    renumbered to match; a row's update depends on its own occurrences only),
+    and the GPU's untouched rows are checked on a random sample."""
+    T = w.num_tables
+    grad = _grad(w, dev)
+    R = [t.num_rows for t in w.tables]
+    base = np.concatenate([[0], np.cumsum(R)])
+    off = w.offsets.cpu().numpy()
+    idx = w.indices.cpu().numpy()
+    touched, compact_idx, sample = [], np.empty_like(idx), []
+    rng = np.random.default_rng(3)
+    for t in range(T):
+        lo, hi = int(off[t * w.batch]), int(off[(t + 1) * w.batch])
+        rows = np.unique(idx[lo:hi])
+        touched.append(rows)
+        compact_idx[lo:hi] = np.searchsorted(rows, idx[lo:hi])
+        cand = rng.integers(0, R[t], min(samples, R[t]))
+        sample.append(np.setdiff1d(cand, rows))
+    state = None
+    if optimizer == "rowwise_adagrad":
+        gs = torch.Generator(device=dev)
+        gs.manual_seed(11)
+        state = torch.rand(sum(R), generator=gs, device=dev, dtype=torch.float32)
+
+    def take(t, rows):
+        return w.tables[t].rows.index_select(0, torch.from_numpy(rows).to(dev)).cpu().numpy()
+
+    def take_state(t, rows):
+        return state.index_select(0, torch.from_numpy(rows + base[t]).to(dev)).cpu().numpy()
+
+    before = [take(t, touched[t]) for t in range(T)]
+    before_s = [take(t, sample[t]) for t in range(T)]
+    st0 = None if state is None else [take_state(t, touched[t]) for t in range(T)]
+    st0_s = None if state is None else [take_state(t, sample[t]) for t in range(T)]
+    say(f"[bwd] {label}: {w.num_indices} lookups into {R} rows, {optimizer}; backward on the GPU")
+    with eb.eb_create_tables(w.tables) as h:
+        eb.eb_backward_update(h, w.indices, w.offsets, w.weights, w.pooling, grad, optimizer, lr, eps, state)
+        torch.cuda.synchronize()
+    say(f"[bwd] {label}: oracle on the touched rows")
+    tabs = [OracleTable(before[t].copy(), tb.dim, tb.dtype, len(touched[t])) for t, tb in enumerate(w.tables)]
+    st_or = None if state is None else np.concatenate(st0).astype(np.float32)
+    rep = ebo_backward_update(tabs, compact_idx, off, None if w.weights is None else w.weights.cpu().numpy(),
+                              w.pooling, grad.cpu().numpy(), optimizer, lr, eps, st_or, report=list(range(T)))
+    cbase = np.concatenate([[0], np.cumsum([len(r) for r in touched])])
+    for t, tb in enumerate(w.tables):
+        raw = np.uint16 if tb.dtype == "f16" else np.uint32
+        assert np.array_equal(take(t, sample[t]).view(raw), before_s[t].view(raw)), f"{label} t{t}: untouched rows"
+        if state is not None:
+            assert np.array_equal(take_state(t, sample[t]), st0_s[t]), f"{label} t{t}: untouched state"
+        rows, G, S, n = rep[t]
+        assert np.all(np.diff(rows) > 0) and (rows.size == 0 or rows[-1] < len(touched[t]))
+        if rows.size == 0:
+            continue
+        got = take(t, touched[t][rows])
+        _check_rows(f"{label} t{t}", tb.dtype, tb.dim, got, tabs[t].rows[rows], G, S, n, optimizer, lr, eps,
+                    None if st_or is None else st_or[cbase[t] + rows],
+                    None if state is None else take_state(t, touched[t][rows]))
 
 
 REDUCED = {
@@ -363,3 +434,60 @@ def test_backward_argument_errors(dev):
                               workspace=torch.empty((need + 3) // 4, dtype=torch.float32, device=dev))
         torch.cuda.synchronize()
         assert torch.all(tab[1:3] == -0.5) and torch.all(tab[0] == 0) and torch.all(tab[3:] == 0)
+
+
+def _sort_shape_workload(dev, row_counts, B, weighted, seed):
+    """fp32 D4 tables of the given row counts.  Each table's bags (lengths
+    U{0..300}) draw half their indices from 8 hot rows spread over the whole
+    range and half uniformly, so runs are long and short and every digit of
+    every sort pass varies."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    gd = torch.Generator(device=dev)
+    gd.manual_seed(seed)
+    tables, lens_all, idx_all = [], [], []
+    for R in row_counts:
+        tables.append(Table(torch.randn((R, 4), generator=gd, device=dev), 4, "f32"))
+        lens = torch.randint(0, 301, (B,), generator=g)
+        n = int(lens.sum())
+        hot = torch.randint(0, R, (8,), generator=g)
+        idx = torch.randint(0, R, (n,), generator=g)
+        pick = torch.rand(n, generator=g) < 0.5
+        idx[pick] = hot[torch.randint(0, 8, (int(pick.sum()),), generator=g)]
+        lens_all.append(lens)
+        idx_all.append(idx)
+    lens = torch.cat(lens_all)
+    off = torch.zeros(lens.numel() + 1, dtype=torch.int64)
+    torch.cumsum(lens, 0, out=off[1:])
+    idx = torch.cat(idx_all)
+    wts = torch.rand(idx.numel(), generator=g).to(dev) if weighted else None
+    return Workload("sort shape", tables, B, idx.to(dev), off.to(dev), wts, "sum", lens.to(dev))
+
+
+# (row counts, weighted): the sort's digits cover the rows of the largest
+# table (its row count included, the sentinel), in passes of up to 9 bits;
+# unweighted elements hold the row and the table-local bag id in 32 bits when
+# both fit, weighted ones the row and the position.
+SORT_SHAPES = {
+    "1 pass (9 bits)": ([300, 511], False),
+    "2 passes of 9 bits": ([512, 70000], False),
+    "3 passes of 9 bits, 32-bit elements": ([20_000_000, 1000], False),
+    "3 passes of 9 bits, 64-bit elements": ([20_000_000, 1000], True),
+    "4 passes of 7 bits": ([150_000_000, 3], False),
+}
+
+
+@pytest.mark.parametrize("shape", list(SORT_SHAPES))
+def test_sort_digit_shapes(dev, shape):
+    counts, weighted = SORT_SHAPES[shape]
+    w = _sort_shape_workload(dev, counts, 64, weighted, seed=len(shape))
+    run_and_check_touched(w, dev, "rowwise_adagrad", label=shape)
+
+
+@pytest.mark.parametrize("items", ["4", "8", "12", "16"])
+def test_sort_block_sizes(dev, monkeypatch, items):
+    # every elements-per-thread choice of the sort on a 3-pass sort whose
+    # tables span several blocks of each size
+    monkeypatch.setenv("EB_BWD_SORT_ITEMS", items)
+    w = _sort_shape_workload(dev, [20_000_000, 70000, 1000], 256, False, seed=9)
+    run_and_check_touched(w, dev, "rowwise_adagrad", label=f"{items} items per thread")
