@@ -285,10 +285,12 @@ __global__ __launch_bounds__(kBlock) void eb_bwd_keys_kernel(BwdArgs a) {
 // one of them holds the sum over every block before it, and publishes that sum
 // with its own counts added.  This is the decoupled look-back of single-pass
 // prefix scans (Merrill and Garland, 2016), as radix sorts with one pass per
-// digit use it.  The grid is no larger than the GPU holds at once, and each
-// workgroup takes blocks blockIdx.x, blockIdx.x + gridDim.x, ... in turn, so
-// the lowest unfinished block always belongs to a resident workgroup and
-// waits for nothing: no block waits for one that cannot run.  (A ticket
+// digit use it.  Workgroup b sorts block b, and a block waits only for
+// earlier blocks of its table.  The workgroups of one launch start in order
+// on each XCD, so when block u is the lowest unfinished one, every workgroup
+// ahead of it on its XCD has finished: u is running or can start, and it
+// waits for nothing unfinished.  So no block waits for one that cannot run,
+// however many of the launch's workgroups the GPU holds at once.  (A ticket
 // counter that orders workgroups as they start costs every workgroup an
 // atomic on one address, which serialised: about 37 ns each.)  Every wait is
 // bounded besides, so that a wait that never ended would raise kErrSortWait
@@ -541,8 +543,8 @@ __device__ __forceinline__ void sort_block(const BwdArgs &a, int32_t pass, int32
   }
 }
 
-// One pass: the sort blocks of workgroup blockIdx.x, each partitioned by
-// digit `pass` of the row.  Element k of a block (position start + k) is item
+// One pass: sort block blockIdx.x (and, were the grid smaller than the
+// blocks, blockIdx.x + gridDim.x, ...), partitioned by digit `pass` of the row.  Element k of a block (position start + k) is item
 // k / 64 % IPT of wave k / (64 * IPT), lane k % 64; the block's stable order
 // is k.
 template <typename E, int IPT>
@@ -1188,10 +1190,10 @@ hipError_t resident_grid(int device, int which, int64_t *grid, int32_t *cus) {
 }
 
 // Elements per thread of this call's sort (kernel `which`, sort blocks of
-// 512 * items positions, `grid` workgroups): the fewest rounds of resident
-// workgroups over the blocks; among those, the largest blocks that still
-// give every compute unit one (fewer blocks shorten the look-back and cost
-// less per block, but a block per unit keeps the GPU busy).
+// 512 * items positions, one workgroup per block): the fewest rounds of
+// resident workgroups over the blocks; among those, the largest blocks that
+// still give every compute unit one (fewer blocks shorten the look-back and
+// cost less per block, but a block per unit keeps the GPU busy).
 hipError_t choose_sort_items(const eb_tables *h, int64_t n, bool wide, int *which, int64_t *nblk_ub,
                              int64_t *grid) {
   int64_t best_rounds = -1;
@@ -1209,7 +1211,7 @@ hipError_t choose_sort_items(const eb_tables *h, int64_t n, bool wide, int *whic
       best_rounds = rounds;
       *which = k;
       *nblk_ub = blocks;
-      *grid = g < blocks ? g : blocks;
+      *grid = blocks;
     }
   }
   return best_rounds < 0 ? hipErrorInvalidValue : hipSuccess;
