@@ -209,13 +209,21 @@ __device__ __forceinline__ bool key_positions(const BwdArgs &a, const TableMeta 
       const int64_t p = c + u * kWave + lane;
       r[u] = (int64_t)__builtin_nontemporal_load(idx + (p < P1 ? p : P1 - 1));
     }
+    // bag of each position: the number of the run's later bags that start
+    // at or before it (each bag's offset read once for the four chunks)
+    int jv[kKeyChunks];
+#pragma unroll
+    for (int u = 0; u < kKeyChunks; ++u) jv[u] = 0;
+    for (int jj = 1; jj < nb; ++jj) {
+      const int64_t o = readlane64(my_off, jj);
+#pragma unroll
+      for (int u = 0; u < kKeyChunks; ++u) jv[u] += o <= c + u * kWave + lane ? 1 : 0;
+    }
 #pragma unroll
     for (int u = 0; u < kKeyChunks; ++u) {
       const int64_t p = c + u * kWave + lane;
       if (p < P1) {
-        int j = 0;
-        for (int jj = 1; jj < nb; ++jj)
-          if (readlane64(my_off, jj) <= p) j = jj;
+        const int j = jv[u];
         const bool ok = r[u] >= 0 && r[u] < m.num_rows;
         oob |= !ok;
         const uint32_t row = ok ? (uint32_t)r[u] : (uint32_t)m.num_rows;
