@@ -182,7 +182,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
+        print(f"bench.py: measures one GPU only; --gpus {args.gpus} is not supported "
               "(the pooled lookup on one GPU is the per-GPU share of a table-wise sharded job)", file=sys.stderr)
         sys.exit(2)
 
