@@ -33,17 +33,42 @@
  * rows, indices, offsets, weights, out) is DEVICE memory owned by the caller
  * and must stay valid until the work that uses it has finished on the
  * handle's stream.  The handle copies the table descriptors (not the rows)
- * into a small device array that it owns.
+ * into a device array that it owns, which also holds the long-bag queue
+ * (below).
  *
  * Streams and synchronisation.  The HIP stream is fixed when the handle is
- * created.  eb_forward only enqueues its kernel (one per storage type
- * present) on it and returns; `out` is valid once that stream has been
- * synchronised.  The other entry points behave the same way.  A handle is immutable after
- * creation, so forwards from several host threads may share it.  eb_forward,
+ * created.  eb_forward only enqueues its kernels (per storage type present,
+ * the lookup and the long-bag pass below) on it and returns; `out` is valid
+ * once that stream has been synchronised.  The other entry points behave the
+ * same way.  The handle's tables and settings are fixed at creation; its one
+ * piece of mutable device state, the long-bag queue, is used by a lookup and
+ * the pass right after it, which each call enqueues under a lock held by the
+ * handle, so forwards from several host threads may share it.  eb_forward,
  * eb_forward_fm and eb_forward_seq allocate nothing and, outside checked
  * mode, enqueue only kernel launches, so they may be captured into a HIP
  * graph on the handle's stream and replayed (the captured launches read
- * whatever the buffers hold at replay time).
+ * whatever the buffers hold at replay time; the long-bag pass leaves the
+ * queue's counters cleared for the next call, captured or not).  Replay such
+ * a graph on the handle's stream, or order it with that stream: two calls on
+ * one handle whose kernels run at the same time race on its queue.
+ *
+ * Long bags (Abstract, Sec. IV-A.3: jagged inputs with long-tailed bag
+ * lengths).  A bag of more than 1024 lookups would keep one wavefront busy
+ * long after the others, so the wavefront that holds it queues it instead, in
+ * segments of 2048 positions, and a second kernel (the long-bag pass) pools
+ * the segments on many workgroups: each stages a segment's indices (and
+ * weights) in LDS and splits it over four wavefronts; the segments' partial
+ * sums are added in segment order, so the result is deterministic (its
+ * summation order differs from the one-wavefront order, within the same
+ * error bound).  On MI355X a bag of a million lookups takes 0.13 ms so,
+ * against 30 ms on one wavefront.  The second kernel costs about 1.7 us per
+ * call even when no bag is long, so by default it runs only for batches of
+ * at least 2^23 lookups (numel(indices) >= 8388608), where that is under 1%
+ * of the lookup; EB_LONG_BAG (below) turns it on for every batch.  The queue
+ * lives in the handle: up to 16384 segments per call with one partial row of
+ * the widest table each (at most 64 MiB; 8 MiB for rows of 128 values); the
+ * bags whose segments do not fit are pooled by their own wavefront.  With no
+ * long bag the pass's workgroups find the queue empty and exit.
  *
  * Errors.  Every error the host can detect from the arguments is returned
  * before anything is enqueued, and `out` is left untouched.  The kernel never
@@ -73,13 +98,13 @@
  * EB_BWD_SORT_ITEMS=4|8|12|16 fixes the backward sort's blocks at 512
  * threads of that many elements (default: chosen per call from the number of
  * lookups and how many of the sort's workgroups the GPU holds at once).
- * EB_LONG_BAG=n (n > 0) makes the handle's lookups pool every bag of more
- * than n lookups with all four wavefronts of a workgroup (each a contiguous
- * quarter, partial sums added in a fixed order): for inputs with very long
- * bags.  Without it each bag is pooled by one wavefront, which is faster when
- * bags are short (the split path costs 7-10% on such inputs even unused).
- * Results do not depend on any of these, except that splitting a bag changes
- * the order of its sum (within the same error bound).
+ * EB_LONG_BAG=n (n > 0) runs the long-bag pass for batches of every size,
+ * for bags of more than n lookups (without it: n = 1024, for batches of at
+ * least 2^23 lookups); EB_LONG_BAG=0 turns the pass off (every bag is
+ * pooled by one wavefront, no second kernel, no queue).  EB_LONG_SEG=s (a
+ * power of two from 64 to 2048, default 2048) sets the positions per segment.
+ * Results do not depend on any of these, except that the long-bag pass
+ * changes the order of a long bag's sum (within the same error bound).
  */
 #ifndef EB_H_
 #define EB_H_

@@ -11,6 +11,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "eb.h"
 
 // Unweighted int8 row-wise pooling sums s*q and the biases separately (one
@@ -41,6 +43,32 @@ constexpr int64_t kTailGens = 4;  // default taper of the lookup's runs (sets of
 constexpr int kMaxBackwardDim = 256;
 // Handles with at most this many tables renumber workgroups XCD-contiguously.
 constexpr int32_t kRemapMaxTables = 32;
+
+// Long bags: the lookup leaves bags of more than kDefaultLongBag lookups
+// (EB_LONG_BAG at create time) to a second kernel, which pools them in
+// segments of up to kLongSegMax positions spread over its workgroups.
+constexpr int64_t kDefaultLongBag = 1024;
+// Without EB_LONG_BAG the pass runs for batches of at least this many lookups.
+constexpr int64_t kLongPassMinLookups = (int64_t)1 << 23;
+constexpr int32_t kDefaultLongSeg = 2048;          // positions per segment
+constexpr int32_t kLongSegMax = 2048;              // (a segment's indices are staged in LDS)
+constexpr int64_t kLqMaxEntries = 16384;           // segments queued per launch
+constexpr int64_t kLqMaxPartialFloats = 1 << 24;   // their partial rows: 64 MiB at most
+// counter words of LongQueue::ctrl
+enum : int { kLqTail = 0, kLqHead = 1, kLqFinished = 2 };
+
+// A handle's queue of long-bag segments (device memory).  Entry e names a
+// bag and the bag's first entry; the bag's K segments take K consecutive
+// entries, and arrived[first] counts the segments pooled so far.
+struct LongQueue {
+  uint32_t *ctrl;     // kLqTail: entries reserved; kLqHead: entries taken; kLqFinished: workgroups done
+  uint32_t *bag;      // [cap] bag id of each entry
+  uint32_t *first;    // [cap] first entry of the entry's bag
+  uint32_t *arrived;  // [cap] segments done, per first entry
+  float *part;        // [cap][part_ld] each segment's partial sum
+  int32_t cap;        // entries (0: no queue, long bags are not split)
+  int32_t part_ld;
+};
 
 // error bits raised by the kernel, reported in checked mode
 constexpr int kErrIndex = 1;
@@ -536,7 +564,14 @@ struct eb_tables {
   int32_t bags_per_wave;  // 0: chosen per call from the bag count
   int64_t tail_bags;      // lookup taper: bags per table in short runs at the end (-1: chosen per call)
   int32_t tail_run;       // bags per such run
-  int64_t long_bag_len;   // > 0: the lookup splits bags with more lookups over a workgroup's wavefronts
+  int64_t long_bag_len;   // > 0: bags with more lookups go to the long-bag pass (0: none do)
+  int32_t long_bag_forced;  // EB_LONG_BAG set: the pass runs for batches of any size
+  int32_t long_seg_log2;  // that pass pools them in segments of 2^long_seg_log2 positions
+  eb::LongQueue lq;       // its queue (inside the d_meta allocation)
+  // A lookup launch and its long-bag pass follow each other on the stream
+  // (the pass takes what the launch queued): calls from several host threads
+  // enqueue them under this lock.
+  std::mutex *enqueue;
   int32_t dtype_mask;     // bit d set: some table has storage type d
   int32_t single_log2;    // lanes-per-row log2 shared by every table of one type, else -1
   int32_t xcd_remap;      // see xcd_contiguous

@@ -23,13 +23,21 @@
 //   * a handle whose tables share one (storage type, LPR) kind launches a body
 //     specialised for it; otherwise one launch per storage type switches on
 //     each table's LPR;
-//   * optionally (EB_LONG_BAG at create time), bags longer than a threshold
-//     are pooled by all four wavefronts of their workgroup together.
+//   * bags longer than a threshold (1024 lookups unless EB_LONG_BAG says
+//     otherwise) are queued by the wavefront that holds them and pooled by a
+//     second kernel, cut into segments that run on many workgroups, each
+//     segment's indices staged in LDS and split over four wavefronts; the
+//     segments' partial sums are added in segment order.  By default this
+//     runs for batches of at least 2^23 lookups (below, the second kernel's
+//     launch would cost more than 1% of the lookup), and for any batch when
+//     EB_LONG_BAG is set.
 // Rows wider than 1 KiB take several 1 KiB column passes.  This file also
 // holds the C ABI's handle creation and the checks shared by the entry points
 // that pool.
 
 #include "eb_device.h"
+
+#include <new>
 
 namespace eb {
 namespace {
@@ -58,7 +66,9 @@ struct FwdArgs {
   int32_t head_waves;        // num_tables * head_groups
   int32_t num_waves;         // num_tables * groups_per_table
   int32_t xcd_remap;         // renumber workgroups XCD-contiguously
-  int64_t long_len;          // bags with more lookups are split over the workgroup's wavefronts
+  int64_t long_len;          // bags with more lookups are queued for the long-bag pass
+  int32_t seg_log2;          // that pass pools them in segments of 2^seg_log2 positions
+  LongQueue lq;              // the handle's queue (cap 0: no long-bag pass)
 };
 
 // Pool bags [g0, g0 + nb) of one table (batch rows b0 ..) over the 1 KiB column
@@ -104,9 +114,9 @@ __device__ __forceinline__ void wave_run(const FwdArgs &a, int32_t w, int32_t &t
 
 template <int DT, int LPR, bool W>
 __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, int32_t g0, int nb, int32_t b0,
-                                          int col_base, int64_t my_off) {
-  // (bags longer than a.long_len are pooled by pool_long_bags: skipped here)
-  // my_off: run_offsets(a, g0, nb)
+                                          int col_base, int64_t my_off, uint32_t queued) {
+  // my_off: run_offsets(a, g0, nb); bag j is skipped when bit j of `queued`
+  // is set (the long-bag pass pools it)
   using R = Reduce<DT, LPR>;
   constexpr int V = Vals<DT>::n;
   const int lane = threadIdx.x & (kWave - 1);
@@ -125,7 +135,7 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
       lo = lo < 0 ? 0 : (lo > a.num_indices ? a.num_indices : lo);
       hi = hi < lo ? lo : (hi > a.num_indices ? a.num_indices : hi);
     }
-    skip = hi - lo > a.long_len;
+    skip = (queued >> j) & 1u;
     if (skip) hi = lo;
   };
 
@@ -192,211 +202,117 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
   }
 }
 
-// Pool positions [lo, hi) of one table over the column window at col_base
-// into acc, reduced across the wave (the values the lanes for which
-// Reduce::stores() holds keep).
-template <int DT, int LPR, bool W>
-__device__ __forceinline__ void pool_range(const TableMeta &m, const FwdArgs &a, int64_t lo, int64_t hi, int col_base,
-                                           float (&acc)[Vals<DT>::n]) {
-  constexpr int V = Vals<DT>::n;
-  constexpr bool SPLIT = EB_INT8_SPLIT_BIAS && DT == kU8 && !W;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int colb = col_base + (lane % LPR) * 16;
-  const bool colok = colb < m.code_bytes;
-  float cb = 0.0f;
-#pragma unroll
-  for (int i = 0; i < V; ++i) acc[i] = 0.0f;
-  if (lo < hi) {
-    int64_t c = lo;
-    RawChunk cur = load_chunk<W>(a.indices, a.weights, a.idx64, c, hi);
-    while (true) {
-      const int64_t cn = c + kWave;
-      const bool more = cn < hi;
-      RawChunk nxt;
-      if (more) nxt = load_chunk<W>(a.indices, a.weights, a.idx64, cn, hi);
-      gather_chunk<DT, LPR, W, SPLIT>(m, a.ctx, resolve(cur, m.num_rows, a.idx64), acc, cb, colb, colok);
-      if (!more) break;
-      c = cn;
-      cur = nxt;
-    }
-  }
-  if constexpr (SPLIT) {
-#pragma unroll
-    for (int i = 0; i < V; ++i) acc[i] += cb;
-  }
-  Reduce<DT, LPR>::run(acc);
+// ----------------------------------------------------------------------------
+// Long bags.  One wavefront streaming a bag of many thousand lookups would
+// end the launch long after the others, so a wavefront queues its bags of
+// more than long_len lookups for a second kernel and skips them:
+//   * before its loop, the wavefront finds its long bags from the offsets it
+//     holds (one ballot; nothing more when there is none, the usual case),
+//     and for each reserves K = ceil(L / seg) consecutive entries of the
+//     handle's queue with one atomic add, writing the bag's id and first
+//     entry into them.  A bag whose entries do not fit the queue is pooled
+//     by the wavefront as usual;
+//   * the long-bag pass (eb_long_pass_kernel) runs after the lookup on the
+//     same stream.  Its workgroups of four wavefronts take one entry (a
+//     segment of seg positions) at a time from an atomic head: stage the
+//     segment's indices (and weights) in LDS with coalesced loads, let each
+//     wavefront pool a quarter of them with the lookup's row gather, and add
+//     the four partial vectors in LDS in wavefront order into the entry's
+//     partial row.  The workgroup whose arrival completes the bag adds its K
+//     partial rows in segment order (so the result does not depend on
+//     scheduling), divides by L for mean pooling and stores the bag.  The
+//     last workgroup out clears the queue's counters for the next call.
+// No workgroup waits for another.  Every value that decides the pass's
+// control flow around its barriers is made wave-uniform (readfirstlane): a
+// loop whose exit the compiler takes for divergent may be laid out so that
+// thread 0's work at the end of one round and at the start of the next sit
+// outside the loop the other threads re-enter, and they then read the shared
+// entry word before thread 0 has written it.
+
+constexpr int kLongBlocks = 256;          // workgroups of the long-bag pass (one per CU)
+constexpr uint32_t kNoBag = 0xFFFFFFFFu;   // an entry of a reservation that did not fit
+
+__device__ __forceinline__ uint32_t agent_load(const uint32_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void agent_store(uint32_t *p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t agent_add(uint32_t *p, uint32_t v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
-// One long bag (global id g, table m, batch row b, positions [lo, hi)), pooled
-// by all the workgroup's wavefronts: wave w takes the w-th contiguous quarter
-// of its positions; the partial vectors meet in LDS and wave 0 adds them in
-// wave order (so the result is deterministic) and stores the sum.  Every wave
-// of the workgroup calls this with the same arguments.
-template <int DT, int LPR, bool W>
-__device__ __forceinline__ void pool_long_bag(const TableMeta &m, const FwdArgs &a, int32_t b, int64_t lo, int64_t hi,
-                                              float (*part)[kPassBytes / Vals<DT>::esize]) {
-  using R = Reduce<DT, LPR>;
-  constexpr int V = Vals<DT>::n;
-  constexpr int WIN = kPassBytes / Vals<DT>::esize;
+// Queue the run's bags of more than a.long_len lookups (bags [g0, g0 + nb),
+// offsets my_off as run_offsets gives them).  Returns the mask of the bags
+// queued; their lengths are taken as pool_bags clamps them.
+__device__ __forceinline__ uint32_t queue_long_bags(const FwdArgs &a, int32_t g0, int nb, int64_t my_off) {
+  // no bag of the run can be long if the whole run is not (the usual case:
+  // two lane reads and a compare); broken offsets go on to the full test
+  const int64_t run_lo = readlane64(my_off, 0), run_hi = readlane64(my_off, nb);
+  if (run_lo >= 0 && run_hi >= run_lo && run_hi - run_lo <= a.long_len) return 0u;
   const int lane = threadIdx.x & (kWave - 1);
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int64_t L = hi - lo;
-  const int64_t piece = (L + kWavesPerBlock - 1) / kWavesPerBlock;
-  const int64_t plo = lo + piece * wave < hi ? lo + piece * wave : hi;
-  const int64_t phi = plo + piece < hi ? plo + piece : hi;
-  const int e0 = (lane % LPR) * V + R::first_value(lane);
-  const int passes = LPR == kWave ? m.passes : 1;
-  for (int p = 0; p < passes; ++p) {
-    float acc[V];
-    pool_range<DT, LPR, W>(m, a, plo, phi, p * kPassBytes, acc);
-    if (R::stores(lane)) {
-#pragma unroll
-      for (int i = 0; i < R::KEEP; ++i) part[wave][e0 + i] = acc[i];
+  const int src = lane + 1 < kWave ? lane + 1 : lane;
+  const uint32_t nlo = (uint32_t)__shfl((int)(uint32_t)my_off, src);
+  const uint32_t nhi = (uint32_t)__shfl((int)(uint32_t)((uint64_t)my_off >> 32), src);
+  const int64_t next = (int64_t)(((uint64_t)nhi << 32) | nlo);
+  const int64_t lo = my_off < 0 ? 0 : (my_off > a.num_indices ? a.num_indices : my_off);
+  const int64_t hi = next < lo ? lo : (next > a.num_indices ? a.num_indices : next);
+  const int64_t len = hi - lo;
+  uint64_t longm = __ballot(lane < nb && len > a.long_len);
+  uint32_t queued = 0;
+  while (longm) {
+    const int j = __builtin_ctzll(longm);
+    longm &= longm - 1;
+    const int64_t L = readlane64(len, j);
+    const uint32_t K = (uint32_t)((L + ((int64_t)1 << a.seg_log2) - 1) >> a.seg_log2);
+    uint32_t s0 = 0;
+    if (lane == 0) s0 = agent_add(a.lq.ctrl + kLqTail, K);
+    s0 = __builtin_amdgcn_readfirstlane(s0);
+    const uint64_t cap = (uint64_t)a.lq.cap;
+    const bool fits = (uint64_t)s0 + K <= cap;
+    for (uint32_t k = lane; k < K && (uint64_t)s0 + k < cap; k += kWave) {
+      a.lq.bag[s0 + k] = fits ? (uint32_t)(g0 + j) : kNoBag;
+      a.lq.first[s0 + k] = s0;
     }
-    __syncthreads();
-    if (wave == 0) {
-      const int rest = (m.code_bytes - p * kPassBytes) / Vals<DT>::esize;
-      const int n = rest < WIN ? rest : WIN;
-      float *dst = a.out + (int64_t)b * a.out_ld + m.out_col + p * WIN;
-      for (int e = lane; e < n; e += kWave) {
-        float v = part[0][e];
-#pragma unroll
-        for (int w = 1; w < kWavesPerBlock; ++w) v += part[w][e];
-        if (a.mean && L > 0) v = v / (float)L;
-        __builtin_nontemporal_store(v, dst + e);
-      }
-    }
-    __syncthreads();  // the next pass or bag reuses the buffers
+    if (fits) queued |= 1u << j;
   }
+  return queued;
 }
 
 template <int DT, int LPR, bool W>
 __device__ __forceinline__ void pool_all_passes(const TableMeta &m, const FwdArgs &a, int32_t g0, int nb,
-                                                int32_t b0, int64_t my_off) {
+                                                int32_t b0, int64_t my_off, uint32_t queued) {
   if constexpr (LPR == kWave) {
-    for (int p = 0; p < m.passes; ++p) pool_bags<DT, LPR, W>(m, a, g0, nb, b0, p * kPassBytes, my_off);
+    for (int p = 0; p < m.passes; ++p) pool_bags<DT, LPR, W>(m, a, g0, nb, b0, p * kPassBytes, my_off, queued);
   } else {
-    pool_bags<DT, LPR, W>(m, a, g0, nb, b0, 0, my_off);
+    pool_bags<DT, LPR, W>(m, a, g0, nb, b0, 0, my_off, queued);
   }
 }
 
 #define EB_LPR(LOG2)                                                          \
   case LOG2:                                                                  \
-    pool_all_passes<DT, (1 << (LOG2)), W>(m, a, g0, nb, b0, my_off);          \
+    pool_all_passes<DT, (1 << (LOG2)), W>(m, a, g0, nb, b0, my_off, queued);  \
     break;
 
-// The workgroup's bags [G0, G1) and the offsets at both ends (clamped into
-// [0, N]).  Loaded when the kernel starts, with the wavefront's own offsets,
-// and used only after its own bags are done, so the check costs no extra
-// memory round trip.
-struct BlockBags {
-  int64_t G0, G1;
-  int64_t o;  // lane 0: the offset at G0, lane 1: at G1 (a vector load, so it
-              // returns with the wavefront's own offsets and delays no scalar load)
-};
-
-__device__ __forceinline__ int64_t clamped_offset(const FwdArgs &a, int64_t g) {
-  const int64_t v = a.idx64 ? static_cast<const int64_t *>(a.offsets)[g]
-                            : (int64_t) static_cast<const int32_t *>(a.offsets)[g];
-  return v < 0 ? 0 : (v > a.num_indices ? a.num_indices : v);
-}
-
-// Wavefronts per workgroup of the lookup kernel.  The long-bag split shares
-// a workgroup's wavefronts; the plain kernels run one wavefront per
-// workgroup, so a wavefront done with short bags frees its slot for the next
-// one at once instead of waiting for a free slot on every SIMD (3-5% faster
-// with power-law bag lengths, the same elsewhere).
-__host__ __device__ constexpr int pool_waves(bool long_split) { return long_split ? kWavesPerBlock : 1; }
-
-__device__ __forceinline__ BlockBags block_bags(const FwdArgs &a, uint32_t blk) {
-  const int32_t w0 = (int32_t)blk * kWavesPerBlock;
-  const int32_t w1 = (w0 + kWavesPerBlock < a.num_waves ? w0 + kWavesPerBlock : a.num_waves) - 1;
-  auto bag = [&](int32_t w, bool end) -> int64_t {
-    int32_t t, b0, nb;
-    wave_run(a, w, t, b0, nb);
-    return (int64_t)t * a.batch + b0 + (end ? nb : 0);
-  };
-  BlockBags r;
-  r.G0 = bag(w0, false);
-  r.G1 = bag(w1, true);
-  const int lane = threadIdx.x & (kWave - 1);
-  r.o = lane < 2 ? clamped_offset(a, lane == 0 ? r.G0 : r.G1) : 0;
-  return r;
-}
-
-// Bags of the workgroup longer than a.long_len lookups are pooled, after the
-// wavefronts' own (shorter) bags, by all its wavefronts together
-// (pool_long_bag).  Every wavefront derives the same list from the offsets,
-// so all of them meet the same barriers; when the workgroup's bags hold no
-// more than a.long_len lookups in all (the usual case) no barrier is reached.
+// One wavefront per run of bags.  DT is the storage type the launch serves
+// (wavefronts of other tables skip their own bags).  LOG2 >= 0 fixes the
+// lanes per row for handles whose tables all share one kind; LOG2 < 0
+// switches on each table's lanes per row.  Specialising keeps the register
+// count (and so the occupancy) at what that kind needs.  The fp16 and
+// unweighted fp32 kernels that switch over every width are held to 8 waves
+// per SIMD (64 VGPRs), which they meet without spilling; the int8 one would
+// spill, so it keeps the compiler's choice.
 template <int DT, int LOG2, bool W>
-__device__ __forceinline__ void pool_block_long_bags(const FwdArgs &a, const BlockBags &bb,
-                                                     float (*part)[kPassBytes / Vals<DT>::esize]) {
-  const int lane = threadIdx.x & (kWave - 1);
-  const int64_t G0 = bb.G0, G1 = bb.G1;
-  auto off = [&](int64_t g) -> int64_t { return clamped_offset(a, g); };
-  if (readlane64(bb.o, 1) - readlane64(bb.o, 0) <= a.long_len) return;  // no bag can be long
-  for (int64_t gb = G0; gb < G1; gb += kWave) {
-    uint64_t mask;
-    {
-      const int64_t g = gb + lane;
-      int64_t lo = 0, hi = 0;
-      if (g < G1) {
-        lo = off(g);
-        hi = off(g + 1);
-        hi = hi < lo ? lo : hi;
-      }
-      mask = __ballot(g < G1 && hi - lo > a.long_len);
-    }
-    while (mask) {
-      const int j = __builtin_ctzll(mask);
-      mask &= mask - 1;
-      const int64_t gl = gb + j;
-      // re-read (uniform): nothing per lane stays live across the pooling
-      const int64_t blo = off(gl);
-      int64_t bhi = off(gl + 1);
-      bhi = bhi < blo ? blo : bhi;
-      const int32_t t = (int32_t)(gl / a.batch);
-      const int32_t b = (int32_t)(gl - (int64_t)t * a.batch);
-      const TableMeta m = a.meta[t];
-      if (m.kind / 8 != DT) continue;  // served by the launch for its storage type
-      if constexpr (LOG2 >= 0) {
-        pool_long_bag<DT, (1 << (LOG2 >= 0 ? LOG2 : 0)), W>(m, a, b, blo, bhi, part);
-      } else {
-        switch (m.kind % 8) {
-          case 0: pool_long_bag<DT, 1, W>(m, a, b, blo, bhi, part); break;
-          case 1: pool_long_bag<DT, 2, W>(m, a, b, blo, bhi, part); break;
-          case 2: pool_long_bag<DT, 4, W>(m, a, b, blo, bhi, part); break;
-          case 3: pool_long_bag<DT, 8, W>(m, a, b, blo, bhi, part); break;
-          case 4: pool_long_bag<DT, 16, W>(m, a, b, blo, bhi, part); break;
-          case 5: pool_long_bag<DT, 32, W>(m, a, b, blo, bhi, part); break;
-          case 6: pool_long_bag<DT, 64, W>(m, a, b, blo, bhi, part); break;
-          default: break;
-        }
-      }
-    }
-  }
-}
-
-// One wavefront per run of bags; with LONG, then the workgroup's long bags
-// together.  DT is the storage type the launch serves (wavefronts of other
-// tables skip their own bags).  LOG2 >= 0 fixes the lanes per row for handles
-// whose tables all share one kind; LOG2 < 0 switches on each table's lanes per
-// row.  Specialising keeps the register count (and so the occupancy) at what
-// that kind needs.  LONG is a specialisation of its own because the split
-// path's LDS and barriers slowed the common path by 7-10% on MI355X even when
-// no bag took it.  The fp16 kernel that switches over every width (without
-// the split) is held to 8 waves per SIMD (64 VGPRs), which it meets without
-// spilling; the int8 one and the split variants would spill, so they keep the
-// compiler's choice (the fp32 one needs 64 anyway).
-template <int DT, int LOG2, bool W, bool LONG>
-__global__ __launch_bounds__(kWave * pool_waves(LONG))
-__attribute__((amdgpu_waves_per_eu((LOG2 < 0 && DT == kF16 && !LONG) ? 8 : 1, 8)))
+__global__ __launch_bounds__(kWave)
+__attribute__((amdgpu_waves_per_eu((LOG2 < 0 && (DT == kF16 || (DT == kF32 && !W))) ? 8 : 1, 8)))
 void eb_pool_kernel(FwdArgs a) {
   const uint32_t blk = a.xcd_remap ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x;
-  BlockBags bb;
-  if constexpr (LONG) bb = block_bags(a, blk);
-  const int32_t wid = (int32_t)blk * pool_waves(LONG) + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int32_t wid = (int32_t)blk;
   if (wid < a.num_waves) {
     int32_t t, b0, nb;
     wave_run(a, wid, t, b0, nb);
@@ -405,8 +321,9 @@ void eb_pool_kernel(FwdArgs a) {
     const int64_t my_off = run_offsets(a, g0, nb);
     const TableMeta m = a.meta[t];
     if (m.kind / 8 == DT) {
+      const uint32_t queued = a.lq.cap > 0 ? queue_long_bags(a, g0, nb, my_off) : 0u;
       if constexpr (LOG2 >= 0) {
-        pool_all_passes<DT, (1 << (LOG2 >= 0 ? LOG2 : 0)), W>(m, a, g0, nb, b0, my_off);
+        pool_all_passes<DT, (1 << (LOG2 >= 0 ? LOG2 : 0)), W>(m, a, g0, nb, b0, my_off, queued);
       } else {
         switch (m.kind % 8) {
           EB_LPR(0) EB_LPR(1) EB_LPR(2) EB_LPR(3) EB_LPR(4) EB_LPR(5) EB_LPR(6)
@@ -416,41 +333,203 @@ void eb_pool_kernel(FwdArgs a) {
       }
     }
   }
-  if constexpr (LONG) {
-    // every wavefront of the workgroup, its own bags done or not
-    __shared__ float long_part[kWavesPerBlock][kPassBytes / Vals<DT>::esize];
-    pool_block_long_bags<DT, LOG2, W>(a, bb, long_part);
-  }
 }
 
 #undef EB_LPR
 
-typedef void (*KernelFn)(FwdArgs);
+// offsets[g], clamped into [0, N] (wave-uniform)
+__device__ __forceinline__ int64_t clamped_offset(const FwdArgs &a, int64_t g) {
+  const int64_t v = uniform64(a.idx64 ? static_cast<const int64_t *>(a.offsets)[g]
+                                      : (int64_t) static_cast<const int32_t *>(a.offsets)[g]);
+  return v < 0 ? 0 : (v > a.num_indices ? a.num_indices : v);
+}
 
-// kernel for (storage type, log2 lanes per row or -1, weighted, long-bag split)
-template <int DT, bool W, bool LONG>
-KernelFn pick_kernel(int log2) {
-  switch (log2) {
-    case 0: return eb_pool_kernel<DT, 0, W, LONG>;
-    case 1: return eb_pool_kernel<DT, 1, W, LONG>;
-    case 2: return eb_pool_kernel<DT, 2, W, LONG>;
-    case 3: return eb_pool_kernel<DT, 3, W, LONG>;
-    case 4: return eb_pool_kernel<DT, 4, W, LONG>;
-    case 5: return eb_pool_kernel<DT, 5, W, LONG>;
-    case 6: return eb_pool_kernel<DT, 6, W, LONG>;
-    default: return eb_pool_kernel<DT, -1, W, LONG>;
+// Bag g's index range, clamped as pool_bags clamps it (wave-uniform).
+__device__ __forceinline__ void long_bag_range(const FwdArgs &a, int64_t g, int64_t &lo, int64_t &hi) {
+  lo = clamped_offset(a, g);
+  hi = clamped_offset(a, g + 1);
+  hi = hi < lo ? lo : hi;
+}
+
+// Stage positions [plo, plo + n) of the index stream (and their weights) in
+// LDS, indices widened to 64 bits.
+template <bool W>
+__device__ __forceinline__ void stage_segment(const FwdArgs &a, int64_t plo, int n, int64_t *s_idx, float *s_w) {
+  for (int i = threadIdx.x; i < n; i += kBlock) {
+    s_idx[i] = a.idx64 ? static_cast<const int64_t *>(a.indices)[plo + i]
+                       : (int64_t) static_cast<const int32_t *>(a.indices)[plo + i];
+    if constexpr (W) s_w[i] = a.weights[plo + i];
+  }
+  __syncthreads();
+}
+
+// The workgroup pools the n staged positions of one segment of a table-m bag:
+// wavefront w takes the w-th contiguous quarter of the segment's 64-position
+// chunks.  Per 1 KiB column window, the wavefronts' reduced vectors meet in
+// s_part and their sum, in wavefront order, is written to dst (the row's
+// first m.dim values).
+template <int DT, int LPR, bool W>
+__device__ __forceinline__ void long_segment(const TableMeta &m, const FwdArgs &a, const int64_t *s_idx,
+                                             const float *s_w, int n, float *s_part, float *dst) {
+  using R = Reduce<DT, LPR>;
+  constexpr int V = Vals<DT>::n;
+  constexpr int WIN = kPassBytes / Vals<DT>::esize;  // values per column window
+  constexpr bool SPLIT = EB_INT8_SPLIT_BIAS && DT == kU8 && !W;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int chunks = (n + kWave - 1) / kWave;
+  const int per = (chunks + kWavesPerBlock - 1) / kWavesPerBlock;
+  const int c0 = wave * per < chunks ? wave * per : chunks;
+  const int c1 = c0 + per < chunks ? c0 + per : chunks;
+  const int passes = LPR == kWave ? m.passes : 1;
+  for (int p = 0; p < passes; ++p) {
+    const int colb = p * kPassBytes + (lane % LPR) * 16;
+    const bool colok = colb < m.code_bytes;
+    float acc[V];
+    float cb = 0.0f;
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] = 0.0f;
+    for (int c = c0; c < c1; ++c) {
+      RawChunk k;
+      k.n = n - c * kWave < kWave ? n - c * kWave : kWave;
+      const int at = c * kWave + (lane < k.n ? lane : 0);
+      const uint64_t v = (uint64_t)s_idx[at];
+      k.lo = (uint32_t)v;
+      k.hi = (uint32_t)(v >> 32);
+      k.w = W ? s_w[at] : 0.0f;
+      gather_chunk<DT, LPR, W, SPLIT>(m, a.ctx, resolve(k, m.num_rows, 1), acc, cb, colb, colok);
+    }
+    if constexpr (SPLIT) {
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] += cb;
+    }
+    R::run(acc);
+    if (R::stores(lane)) {
+      const int e = (lane % LPR) * V + R::first_value(lane);
+#pragma unroll
+      for (int i = 0; i < R::KEEP; ++i) s_part[wave * WIN + e + i] = acc[i];
+    }
+    __syncthreads();
+    const int rest = (m.code_bytes - p * kPassBytes) / Vals<DT>::esize;
+    const int cols = rest < WIN ? rest : WIN;
+    for (int c = threadIdx.x; c < cols; c += kBlock) {
+      float v = s_part[c];
+#pragma unroll
+      for (int w = 1; w < kWavesPerBlock; ++w) v += s_part[w * WIN + c];
+      dst[p * WIN + c] = v;
+    }
+    __syncthreads();  // s_part is reused by the next window
   }
 }
 
-template <bool LONG>
-KernelFn pick_kernel(int dt, int log2, bool weighted) {
-  if (dt == kF32) return weighted ? pick_kernel<kF32, true, LONG>(log2) : pick_kernel<kF32, false, LONG>(log2);
-  if (dt == kF16) return weighted ? pick_kernel<kF16, true, LONG>(log2) : pick_kernel<kF16, false, LONG>(log2);
-  return weighted ? pick_kernel<kU8, true, LONG>(log2) : pick_kernel<kU8, false, LONG>(log2);
+// The long-bag pass for the lookup's storage type DT (see above).
+template <int DT, bool W>
+__global__ __launch_bounds__(kBlock) void eb_long_pass_kernel(FwdArgs a) {
+  constexpr int WIN = kPassBytes / Vals<DT>::esize;
+  __shared__ int64_t s_idx[kLongSegMax];
+  __shared__ float s_w[W ? kLongSegMax : 1];
+  __shared__ float s_part[kWavesPerBlock * WIN];
+  __shared__ uint32_t s_word;
+  uint32_t *ctrl = a.lq.ctrl;
+  const uint32_t tail = __builtin_amdgcn_readfirstlane(agent_load(ctrl + kLqTail));
+  if (tail == 0) return;  // nothing queued (the usual case): nothing to clear either
+  const int tid = threadIdx.x;
+  const int64_t seg = (int64_t)1 << a.seg_log2;
+  const uint32_t cap = (uint32_t)a.lq.cap;
+  const uint32_t end = tail < cap ? tail : cap;
+  // one entry per round; `end` entries in all, so no workgroup takes more
+  for (uint32_t round = 0; round <= end; ++round) {
+    if (tid == 0) s_word = agent_add(ctrl + kLqHead, 1);
+    __syncthreads();
+    const uint32_t e = __builtin_amdgcn_readfirstlane(s_word);
+    __syncthreads();  // s_word is rewritten only after every thread has read it
+    if (e >= end) break;
+    const uint32_t gu = __builtin_amdgcn_readfirstlane(a.lq.bag[e]);
+    if (gu == kNoBag) continue;  // part of a reservation that did not fit
+    const uint32_t s0 = __builtin_amdgcn_readfirstlane(a.lq.first[e]);
+    int64_t lo, hi;
+    long_bag_range(a, gu, lo, hi);
+    const int64_t L = hi - lo;
+    const uint32_t K = (uint32_t)((L + seg - 1) >> a.seg_log2);
+    const int64_t plo = lo + (int64_t)(e - s0) * seg;
+    const int n = (int)((plo + seg < hi ? plo + seg : hi) - plo);
+    const int32_t t = (int32_t)(gu / (uint32_t)a.batch);
+    const int32_t b = (int32_t)(gu - (uint32_t)t * (uint32_t)a.batch);
+    const TableMeta m = a.meta[t];
+    stage_segment<W>(a, plo, n, s_idx, s_w);
+    float *part = a.lq.part + (size_t)e * a.lq.part_ld;
+    switch (m.kind % 8) {
+      case 0: long_segment<DT, 1, W>(m, a, s_idx, s_w, n, s_part, part); break;
+      case 1: long_segment<DT, 2, W>(m, a, s_idx, s_w, n, s_part, part); break;
+      case 2: long_segment<DT, 4, W>(m, a, s_idx, s_w, n, s_part, part); break;
+      case 3: long_segment<DT, 8, W>(m, a, s_idx, s_w, n, s_part, part); break;
+      case 4: long_segment<DT, 16, W>(m, a, s_idx, s_w, n, s_part, part); break;
+      case 5: long_segment<DT, 32, W>(m, a, s_idx, s_w, n, s_part, part); break;
+      case 6: long_segment<DT, 64, W>(m, a, s_idx, s_w, n, s_part, part); break;
+      default: break;
+    }
+    __threadfence();  // this segment's partial row is visible before it is counted
+    if (tid == 0) s_word = agent_add(a.lq.arrived + s0, 1);
+    __syncthreads();
+    const bool last = __builtin_amdgcn_readfirstlane(s_word) == K - 1;
+    __syncthreads();
+    if (last) {
+      __threadfence();  // the bag's other partial rows are visible here
+      const float *p0 = a.lq.part + (size_t)s0 * a.lq.part_ld;
+      float *dst = a.out + (int64_t)b * a.out_ld + m.out_col;
+      for (int c = tid; c < m.dim; c += kBlock) {
+        // the partial rows in segment order, eight loads in flight
+        float v = 0.0f;
+        for (uint32_t k = 0; k < K; k += 8) {
+          float x[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) x[u] = k + u < K ? p0[(size_t)(k + u) * a.lq.part_ld + c] : 0.0f;
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            if (k + u < K) v += x[u];
+        }
+        if (a.mean && L > 0) v = v / (float)L;
+        __builtin_nontemporal_store(v, dst + c);
+      }
+      if (tid == 0) agent_store(a.lq.arrived + s0, 0u);  // cleared for the next call
+    }
+  }
+  // the last workgroup out clears the counters (every workgroup has left the
+  // loop by then, so none reads them again)
+  if (tid == 0 && agent_add(ctrl + kLqFinished, 1) == gridDim.x - 1) {
+    agent_store(ctrl + kLqTail, 0u);
+    agent_store(ctrl + kLqHead, 0u);
+    agent_store(ctrl + kLqFinished, 0u);
+  }
 }
 
-KernelFn pick_kernel(int dt, int log2, bool weighted, bool split_long) {
-  return split_long ? pick_kernel<true>(dt, log2, weighted) : pick_kernel<false>(dt, log2, weighted);
+typedef void (*KernelFn)(FwdArgs);
+
+// kernel for (storage type, log2 lanes per row or -1, weighted)
+template <int DT, bool W>
+KernelFn pick_kernel(int log2) {
+  switch (log2) {
+    case 0: return eb_pool_kernel<DT, 0, W>;
+    case 1: return eb_pool_kernel<DT, 1, W>;
+    case 2: return eb_pool_kernel<DT, 2, W>;
+    case 3: return eb_pool_kernel<DT, 3, W>;
+    case 4: return eb_pool_kernel<DT, 4, W>;
+    case 5: return eb_pool_kernel<DT, 5, W>;
+    case 6: return eb_pool_kernel<DT, 6, W>;
+    default: return eb_pool_kernel<DT, -1, W>;
+  }
+}
+
+KernelFn pick_kernel(int dt, int log2, bool weighted) {
+  if (dt == kF32) return weighted ? pick_kernel<kF32, true>(log2) : pick_kernel<kF32, false>(log2);
+  if (dt == kF16) return weighted ? pick_kernel<kF16, true>(log2) : pick_kernel<kF16, false>(log2);
+  return weighted ? pick_kernel<kU8, true>(log2) : pick_kernel<kU8, false>(log2);
+}
+
+KernelFn pick_long_kernel(int dt, bool weighted) {
+  if (dt == kF32) return weighted ? eb_long_pass_kernel<kF32, true> : eb_long_pass_kernel<kF32, false>;
+  if (dt == kF16) return weighted ? eb_long_pass_kernel<kF16, true> : eb_long_pass_kernel<kF16, false>;
+  return weighted ? eb_long_pass_kernel<kU8, true> : eb_long_pass_kernel<kU8, false>;
 }
 
 }  // namespace
@@ -501,7 +580,15 @@ hipError_t launch_forward(const eb_tables *h, const eb_tensor &indices, const eb
   a.ctx.zero = h->d_zero;
   a.ctx.one = 1.0f;
   a.xcd_remap = h->xcd_remap;
-  a.long_len = h->long_bag_len > 0 ? h->long_bag_len : INT64_MAX;  // 0: no split
+  a.long_len = h->long_bag_len > 0 ? h->long_bag_len : INT64_MAX;  // 0: no long-bag pass
+  a.seg_log2 = h->long_seg_log2;
+  a.lq = h->lq;
+  // The pass costs one more kernel on the stream whether or not a bag needs
+  // it (on MI355X about 1.7 us: 8% of a 23 us lookup of a million lookups,
+  // under 1% from about eight million), so unless the handle asked for it
+  // (EB_LONG_BAG set) it runs only for batches that large.
+  const bool long_pass = h->lq.cap > 0 && (h->long_bag_forced || indices.numel >= kLongPassMinLookups);
+  if (!long_pass) a.lq.cap = 0;  // the lookup queues nothing: every bag is its wavefront's
   a.num_indices = indices.numel;
   a.out_ld = h->sum_dim;
   a.num_bags = (int32_t)sh.num_bags;
@@ -542,22 +629,25 @@ hipError_t launch_forward(const eb_tables *h, const eb_tensor &indices, const eb
   a.groups_per_table = a.head_groups + a.tail_groups;
   // Without the XCD renumbering the launch runs its wavefronts in id order,
   // so the tail runs of every table go last; with it, each XCD runs its own
-  // contiguous range of tables and a table's tail runs end that table.  The
-  // long-bag split needs a workgroup's runs contiguous, so keeps table order.
-  a.tail_last = (tail_bags > 0 && !h->xcd_remap && h->long_bag_len == 0 && head_groups > 0 && a.tail_groups > 0) ? 1 : 0;
+  // contiguous range of tables and a table's tail runs end that table.
+  a.tail_last = (tail_bags > 0 && !h->xcd_remap && head_groups > 0 && a.tail_groups > 0) ? 1 : 0;
   a.head_waves = (int32_t)(head_groups * h->num_tables);
   const int64_t num_waves = (int64_t)a.groups_per_table * h->num_tables;
   a.num_waves = (int32_t)num_waves;
 
   hipError_t e = hipSuccess;
-  // one launch per storage type present (one in the usual case)
+  std::lock_guard<std::mutex> lock(*h->enqueue);
+  // one launch per storage type present (one in the usual case), each
+  // followed by the long-bag pass over what it queued
   for (int dt = 0; dt < 3 && e == hipSuccess; ++dt) {
     if (!(h->dtype_mask & (1 << dt))) continue;
-    const int wpb = pool_waves(h->long_bag_len > 0);
-    const unsigned grid = (unsigned)((num_waves + wpb - 1) / wpb);
-    hipLaunchKernelGGL(pick_kernel(dt, h->single_log2, sh.weighted, h->long_bag_len > 0), dim3(grid),
-                       dim3(kWave * wpb), 0, h->stream, a);
+    hipLaunchKernelGGL(pick_kernel(dt, h->single_log2, sh.weighted), dim3((unsigned)num_waves), dim3(kWave), 0,
+                       h->stream, a);
     e = hipGetLastError();
+    if (e == hipSuccess && long_pass) {
+      hipLaunchKernelGGL(pick_long_kernel(dt, sh.weighted), dim3(kLongBlocks), dim3(kBlock), 0, h->stream, a);
+      e = hipGetLastError();
+    }
   }
   return e;
 }
@@ -728,9 +818,15 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   if (h->bwd_sort_items != 4 && h->bwd_sort_items != 8 && h->bwd_sort_items != 12 && h->bwd_sort_items != 16)
     h->bwd_sort_items = 0;
   const char *lb = getenv("EB_LONG_BAG");
-  h->long_bag_len = lb ? atoll(lb) : 0;
-  if (h->long_bag_len < 0) h->long_bag_len = 0;
-  if (h->long_bag_len > 0 && h->long_bag_len < kWavesPerBlock) h->long_bag_len = kWavesPerBlock;
+  h->long_bag_len = lb ? atoll(lb) : kDefaultLongBag;
+  if (h->long_bag_len < 0) h->long_bag_len = kDefaultLongBag;
+  h->long_bag_forced = lb && h->long_bag_len > 0;
+  // positions per long-bag segment: a power of two from 64 to kLongSegMax
+  const char *ls = getenv("EB_LONG_SEG");
+  int64_t seg = ls ? atoll(ls) : kDefaultLongSeg;
+  if (seg < kWave || seg > kLongSegMax) seg = kDefaultLongSeg;
+  h->long_seg_log2 = 0;
+  while ((2LL << h->long_seg_log2) <= seg) ++h->long_seg_log2;
   const char *tb = getenv("EB_TAIL_BAGS");
   h->tail_bags = tb ? atoll(tb) : -1;
   if (h->tail_bags < -1) h->tail_bags = -1;
@@ -742,20 +838,37 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   if (h->bags_per_wave < 0 || h->bags_per_wave > kMaxBagsPerWave) h->bags_per_wave = 0;
 
   const size_t meta_bytes = sizeof(TableMeta) * (size_t)num_tables;
-  // [descriptors][error word, padded to 256 B][zero row]
+  // [descriptors][error word, padded to 256 B][zero row][long-bag queue]
   const size_t err_off = (meta_bytes + 255) / 256 * 256;
   const size_t zero_off = err_off + 256;
+  const size_t lq_off = (zero_off + kZeroBytes + 255) / 256 * 256;
+  // the long-bag queue: 256 B of counters, then per entry a bag id, a first
+  // entry and an arrival count, then one partial row of the widest table per
+  // entry (kLqMaxPartialFloats floats at most)
+  const int32_t part_ld = (h->max_dim + 3) / 4 * 4;
+  int64_t lq_cap = h->long_bag_len > 0 ? kLqMaxPartialFloats / part_ld : 0;
+  lq_cap = lq_cap > kLqMaxEntries ? kLqMaxEntries : lq_cap;
+  const size_t lq_part_off = (256 + (size_t)lq_cap * 12 + 255) / 256 * 256;
+  const size_t lq_bytes = lq_cap > 0 ? lq_part_off + (size_t)lq_cap * part_ld * 4 : 0;
+  const size_t total = lq_off + lq_bytes;
   // a caller's cap on the handle's device memory: past it, fail as the
   // allocator would
   const char *cap = getenv("EB_DEVICE_ALLOC_LIMIT");
-  if (cap && cap[0] && strtoull(cap, nullptr, 10) < zero_off + kZeroBytes) {
+  if (cap && cap[0] && strtoull(cap, nullptr, 10) < total) {
+    free(meta);
+    free(h);
+    return EB_ERR_OOM;
+  }
+  h->enqueue = new (std::nothrow) std::mutex();
+  if (!h->enqueue) {
     free(meta);
     free(h);
     return EB_ERR_OOM;
   }
   void *dev = nullptr;
-  hipError_t e = hipMalloc(&dev, zero_off + kZeroBytes);
+  hipError_t e = hipMalloc(&dev, total);
   if (e != hipSuccess) {
+    delete h->enqueue;
     free(meta);
     free(h);
     return e == hipErrorOutOfMemory ? EB_ERR_OOM : EB_ERR_HIP;
@@ -763,9 +876,29 @@ eb_status eb_create_tables(const eb_table_desc *descs, int32_t num_tables, void 
   h->d_meta = static_cast<TableMeta *>(dev);
   h->d_err = reinterpret_cast<int *>(static_cast<char *>(dev) + err_off);
   h->d_zero = static_cast<unsigned char *>(dev) + zero_off;
+  h->lq = LongQueue{};
+  if (lq_cap > 0) {
+    char *q = static_cast<char *>(dev) + lq_off;
+    h->lq.ctrl = reinterpret_cast<uint32_t *>(q);
+    h->lq.bag = reinterpret_cast<uint32_t *>(q + 256);
+    h->lq.first = h->lq.bag + lq_cap;
+    h->lq.arrived = h->lq.first + lq_cap;
+    h->lq.part = reinterpret_cast<float *>(q + lq_part_off);
+    h->lq.cap = (int32_t)lq_cap;
+    h->lq.part_ld = part_ld;
+  } else {
+    h->long_bag_len = 0;  // no queue: no bag is left to the long-bag pass
+  }
   e = hipMemcpy(h->d_meta, meta, meta_bytes, hipMemcpyHostToDevice);
+  // the error word, the zero row, the queue's counters and arrival counts
+  // start at zero (its entries and partial rows are written before they are
+  // read); the copies and clears end before this call returns
   if (e == hipSuccess) e = hipMemset(static_cast<char *>(dev) + err_off, 0, 256 + kZeroBytes);
+  if (e == hipSuccess && lq_cap > 0) e = hipMemset(h->lq.ctrl, 0, 256);
+  if (e == hipSuccess && lq_cap > 0) e = hipMemset(h->lq.arrived, 0, (size_t)lq_cap * 4);
+  if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
   if (e != hipSuccess) {
+    delete h->enqueue;
     free(meta);
     (void)hipFree(dev);
     free(h);
@@ -801,6 +934,7 @@ eb_status eb_destroy(eb_tables *h) {
   if (st == EB_OK && hipStreamSynchronize(h->stream) != hipSuccess) st = EB_ERR_HIP;
   if (hipFree(h->d_meta) != hipSuccess) st = EB_ERR_HIP;
   free(h->h_meta);
+  delete h->enqueue;
   if (cur >= 0 && cur != h->device) (void)hipSetDevice(cur);
   free(h);
   return st;

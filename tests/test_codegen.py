@@ -42,3 +42,114 @@ def test_no_flat_memory_instructions(tmp_path):
         assert not bad, f"{o.name}: {len(bad)} flat memory instructions, e.g. {bad[:3]}"
     assert mem > 1000  # the disassembly really holds the kernels
     assert flat == 0
+
+
+# ---------------------------------------------------------------------------
+# Barriers and divergent loops.  A loop whose exit the compiler takes for
+# divergent is laid out as a loop that ends by narrowing exec: the lanes that
+# leave wait, masked off, while the others run the next round.  A workgroup
+# barrier inside such a loop then completes with some lanes of a wave still
+# in the previous round, and the others read what those lanes have not yet
+# written to LDS.  (A form of the long-bag pass whose loop control came from
+# LDS without readfirstlane livelocked this way: after a bag's last segment,
+# every thread but thread 0 re-entered the loop and read a stale entry word.)
+# Every kernel's loops around barriers must be controlled by wave-uniform
+# values; this checks the compiled code for it.
+
+SOURCES = ["eb_forward.hip", "eb_backward.hip", "eb_fm.hip", "eb_seq.hip"]
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+
+
+def _device_asm(src, out):
+    from paper_2609_30656_amd import build
+    flags = [f for f in build.HIPCC_FLAGS if f not in ("-shared", "-fPIC")]
+    return subprocess.Popen([HIPCC, *flags, "--cuda-device-only", "-S", "-I", build.INCLUDE, "-I", build.CSRC,
+                             os.path.join(build.CSRC, src), "-o", str(out)],
+                            stdout=subprocess.DEVNULL, stderr=subprocess.DEVNULL)
+
+
+def barriers_in_divergent_loops(asm):
+    """{kernel: (barriers, barriers inside a loop that exits by narrowing exec)}
+    from compiler assembly (-S), whose block comments name each block's loops."""
+    out = {}
+    lines = asm.split("\n")
+    i = 0
+    while i < len(lines):
+        m = re.match(r"^(_Z\S+):\s*;\s*@", lines[i])
+        if not m:
+            i += 1
+            continue
+        name, j = m.group(1), i + 1
+        while j < len(lines) and not lines[j].startswith(".Lfunc_end"):
+            j += 1
+        blocks = []  # [label, comment, instructions]
+        for line in lines[i + 1:j]:
+            bm = re.match(r"^(\.LBB\d+_\d+|; %bb\.\d+):\s*(;.*)?$", line)
+            if bm:
+                blocks.append([bm.group(1).replace(".L", ""), bm.group(2) or "", []])
+            elif blocks and re.match(r"^\s+;", line) and not blocks[-1][2]:
+                blocks[-1][1] += " " + line.strip()
+            elif blocks:
+                blocks[-1][2].append(line.strip())
+        parent_of, divergent, where = {}, set(), []
+        for label, comment, ins in blocks:
+            parents = set(re.findall(r"Parent Loop (BB\d+_\d+)", comment))
+            if "This Loop Header" in comment or "This Inner Loop Header" in comment:
+                inner = label
+                parent_of[label] = parents
+            else:
+                h = re.findall(r"in Loop: Header=(BB\d+_\d+)", comment)
+                inner = h[0] if h else None
+            if inner and any(s.startswith("s_andn2_b64 exec, exec") for s in ins):
+                divergent.add(inner)
+            where += [{inner} | parents if inner else parents for s in ins if s.startswith("s_barrier")]
+
+        def enclosing(loops):
+            seen, todo = set(loops), list(loops)
+            while todo:
+                for p in parent_of.get(todo.pop(), ()):
+                    if p not in seen:
+                        seen.add(p)
+                        todo.append(p)
+            return seen
+
+        out[name] = (len(where), sum(1 for w in where if enclosing(w) & divergent))
+        i = j
+    return out
+
+
+def test_no_barrier_in_a_divergent_loop(tmp_path):
+    if not os.path.exists(HIPCC):
+        pytest.skip("hipcc not found")
+    procs = {src: _device_asm(src, tmp_path / (src + ".s")) for src in SOURCES}
+    total = 0
+    for src, p in procs.items():
+        assert p.wait(timeout=600) == 0, f"{src}: hipcc failed"
+        found = barriers_in_divergent_loops((tmp_path / (src + ".s")).read_text())
+        assert found, f"{src}: no kernel found in the assembly"
+        for name, (nbar, bad) in found.items():
+            total += nbar
+            assert bad == 0, f"{src}: {name}: {bad} of {nbar} barriers inside a loop that exits by narrowing exec"
+    assert total > 50  # the long-bag pass, the sort and the keys kernel hold barriers in loops
+
+
+def test_divergent_loop_check_flags_a_barrier_in_one():
+    # the check itself, on a hand-made listing: loop BB0_1 ends by narrowing
+    # exec and holds a barrier
+    asm = "\n".join([
+        "_Zkern:                                 ; @_Zkern",
+        "; %bb.0:",
+        "\ts_mov_b64 s[0:1], 0",
+        ".LBB0_1:                                ; =>This Inner Loop Header: Depth=1",
+        "\ts_barrier",
+        "\tv_cmp_le_i32_e32 vcc, s2, v0",
+        "\ts_or_b64 s[0:1], vcc, s[0:1]",
+        "\ts_andn2_b64 exec, exec, s[0:1]",
+        "\ts_cbranch_execnz .LBB0_1",
+        "; %bb.2:",
+        "\ts_endpgm",
+        ".Lfunc_end0:",
+    ])
+    assert barriers_in_divergent_loops(asm) == {"_Zkern": (1, 1)}
+    uniform = asm.replace("\ts_andn2_b64 exec, exec, s[0:1]", "\ts_cmp_lg_u32 s3, 0")
+    assert barriers_in_divergent_loops(uniform) == {"_Zkern": (1, 0)}

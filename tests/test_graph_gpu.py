@@ -1,8 +1,10 @@
-"""The lookups and the backward under HIP graph capture: eb_forward,
-eb_forward_fm, eb_forward_seq and the backward (given a workspace, or its
-no-allocation entry point) allocate nothing and (outside checked mode)
-enqueue only kernels on the handle's stream, so a caller can capture them
-once and replay them.  Each test captures one call on the handle's stream, then replays it
+"""The lookups and the backward under HIP graph capture: eb_forward (the
+lookup and its long-bag pass), eb_forward_fm, eb_forward_seq and the
+backward (given a workspace, or its no-allocation entry point) allocate
+nothing and (outside checked mode) enqueue only kernels on the handle's
+stream, so a caller can capture them once and replay them (on the handle's
+stream, or ordered with it: the long-bag pass keeps a queue in the handle).
+Each test captures one call on the handle's stream, then replays it
 several times, with eager work of the program and synchronisations between the
 replays and new index contents copied into the captured buffers, and checks
 every replay bit for bit against an eager call on the same inputs (the kernels
@@ -68,7 +70,8 @@ def _replay_and_check(run_into, fresh_outputs, w, idx2, stream, label):
         torch.cuda.synchronize()
         for o in captured:
             o.fill_(float("nan"))  # the replay must write every element
-        graph.replay()
+        with torch.cuda.stream(stream):  # on the handle's stream, as its calls go
+            graph.replay()
         # eager work of the program between replays
         eager = fresh_outputs()
         with torch.cuda.stream(stream):
@@ -126,6 +129,26 @@ def test_sequence_lookup_replays(dev, name):
         _replay_and_check(run_into, fresh, w, idx2, stream, f"seq {name}")
 
 
+@pytest.mark.parametrize("name", ["c3b", "c5"])
+def test_forward_replays_with_long_bags(dev, monkeypatch, name):
+    # most bags left to the long-bag pass (a second kernel, with a queue and
+    # counters in the handle): each replay must find the counters cleared by
+    # the previous call, captured or eager
+    say(f"[graph] eb_forward {name}, long-bag pass")
+    monkeypatch.setenv("EB_LONG_BAG", "16")
+    monkeypatch.setenv("EB_LONG_SEG", "64")
+    w, idx2 = _batches(name, dev)
+    stream = torch.cuda.Stream(device=dev)
+    with eb.eb_create_tables(w.tables, stream) as h:
+        def run_into(idx, outs):
+            eb.eb_forward(h, idx, w.offsets, w.weights, w.pooling, outs[0])
+
+        def fresh():
+            return (torch.empty((w.batch, w.sum_dim), device=dev),)
+
+        _replay_and_check(run_into, fresh, w, idx2, stream, f"forward long {name}")
+
+
 def _clone_tables(tables):
     from paper_2609_30656_amd.workload import Table
     return [Table(t.rows.clone(), t.dim, t.dtype) for t in tables]
@@ -174,7 +197,8 @@ def test_backward_replays(dev, name, entry):
             idx_buf.copy_(src)
             grad_buf.copy_(grad)
             torch.cuda.synchronize()
-            graph.replay()
+            with torch.cuda.stream(stream):
+                graph.replay()
             torch.cuda.synchronize()
             with torch.cuda.stream(stream):
                 step(he, src, grad, st_e, ws_e)

@@ -210,9 +210,10 @@ def test_bags_per_wave(dev, monkeypatch, name, k):
 def test_tapered_runs(dev, monkeypatch, name, remap):
     # each table's last bags in short runs after its runs of k bags: with the
     # XCD renumbering the runs go table by table, without it every table's
-    # head runs come first; with the long-bag split a workgroup's runs stay
-    # contiguous.  Which wavefront pools a bag changes, the order of a bag's
-    # additions does not, so every mapping gives the untapered output's bits.
+    # head runs come first.  Which wavefront pools a bag changes, the order of
+    # a bag's additions does not, so every mapping gives the untapered
+    # output's bits (bags left to the long-bag pass are added in another
+    # order: the oracle's bar then).
     say(f"[parity] tapered runs {name} remap={remap}")
     monkeypatch.setenv("EB_XCD_REMAP", remap)
     w = make_workload(name, dev, **REDUCED[name])
@@ -225,6 +226,7 @@ def test_tapered_runs(dev, monkeypatch, name, remap):
              for k in ("3", "7") for tail in (1, 37, B - 1, B, 10 ** 9) for run in ("1", "2", "5")
              for long_len in ("0", "16")]
     for k, tail, run, long_len in cases:
+        say(f"[parity]   k={k} tail={tail} run={run} long={long_len}")
         monkeypatch.setenv("EB_BAGS_PER_WAVE", k)
         monkeypatch.setenv("EB_TAIL_BAGS", str(tail))
         monkeypatch.setenv("EB_TAIL_RUN", run)
@@ -233,19 +235,47 @@ def test_tapered_runs(dev, monkeypatch, name, remap):
         label = f"{name} remap={remap} k={k} tail={tail} run={run} long={long_len}"
         if long_len == "0":
             assert np.array_equal(got.view(np.uint32), base.view(np.uint32)), label
-        else:  # the split adds a long bag's four quarters: a different order
+        else:  # the long-bag pass adds a bag's quarters and segments: another order
             check(got, ref, asum, per_element_lengths(w), RTOL[w.tables[0].dtype], label)
 
 
-@pytest.mark.parametrize("long_len", ["4", "16", "64"])
+@pytest.mark.parametrize("long_len,seg", [("4", "2048"), ("16", "64"), ("64", "128")])
 @pytest.mark.parametrize("name", ["c1", "c2", "c3a", "c3b", "c4", "c5"])
-def test_long_bags_split_over_the_workgroup(dev, monkeypatch, name, long_len):
-    # bags longer than EB_LONG_BAG lookups are pooled by the workgroup's four
-    # wavefronts together; a low threshold sends many bags down that path
-    say(f"[parity] long-bag split at {long_len} {name}")
+def test_long_bag_pass(dev, monkeypatch, name, long_len, seg):
+    # bags longer than EB_LONG_BAG lookups are left by the lookup kernel to
+    # the long-bag pass, which pools them in segments of EB_LONG_SEG
+    # positions (four wavefronts each, indices staged in LDS) and adds the
+    # segments' partial rows in order; a low threshold sends most bags down
+    # that path, short segments cut them into several
+    say(f"[parity] long-bag pass at {long_len}, segments of {seg}, {name}")
     monkeypatch.setenv("EB_LONG_BAG", long_len)
+    monkeypatch.setenv("EB_LONG_SEG", seg)
     w = make_workload(name, dev, **REDUCED[name])
-    full_check(w, f"long>{long_len} {name}")
+    full_check(w, f"long>{long_len} seg {seg} {name}")
+
+
+def test_long_bag_queue_overflow(dev, monkeypatch):
+    # about 60 000 long bags of one segment each against a queue of 16 384
+    # entries: the bags whose entries do not fit are pooled by the wavefront
+    # that holds them, as without the pass.  Three calls on one handle, so
+    # each must find the queue's counters cleared by the one before
+    say("[parity] long-bag queue overflow")
+    monkeypatch.setenv("EB_LONG_BAG", "4")
+    monkeypatch.setenv("EB_LONG_SEG", "64")
+    w = make_workload("c5", dev, rows_cap=20000, batch=1024)
+    w2 = make_workload("c5", dev, rows_cap=20000, batch=96, batch_seed=1)
+    lens = w.lengths.cpu().numpy()
+    assert (np.ceil(lens[lens > 4] / 64)).sum() > 16384
+    rtol = RTOL[w.tables[0].dtype]
+    with eb.eb_create_tables(w.tables) as h:
+        for rep, wl in enumerate([w, w2, w]):
+            out = torch.full((wl.batch, wl.sum_dim), float("nan"), device=dev)
+            eb.eb_forward(h, wl.indices, wl.offsets, wl.weights, wl.pooling, out)
+            torch.cuda.synchronize()
+            tabs = oracle_tables(wl)
+            ref, asum = oracle_forward(wl, tables=tabs)
+            check(out.cpu().numpy(), ref, asum, per_element_lengths(wl), rtol, f"overflow call {rep}",
+                  split_scale(wl, tabs))
 
 
 # ----------------------------------------------------------------------------
@@ -398,28 +428,57 @@ def test_every_width_in_one_launch(dev, monkeypatch, mode, k):
 
 
 @pytest.mark.parametrize("mode", ["sum", "mean", "weighted"])
-def test_long_bag_split_every_width(dev, monkeypatch, mode):
-    say(f"[parity] long-bag split, every width, {mode}")
+def test_long_bag_pass_every_width(dev, monkeypatch, mode):
+    # every storage type and width (1 KiB column windows included) through
+    # the long-bag pass, bags of one to five segments of 64 positions
+    say(f"[parity] long-bag pass, every width, {mode}")
     monkeypatch.setenv("EB_LONG_BAG", "8")
+    monkeypatch.setenv("EB_LONG_SEG", "64")
     rng = np.random.default_rng(15)
     tables = [_table(dev, dt, 300 + 7 * i, D, seed=i) for i, (dt, D) in enumerate(WIDTHS)]
-    lens = [rng.integers(0, 40, 13) for _ in tables]
+    lens = [rng.integers(0, 300, 13) for _ in tables]
     for l in lens:
-        l[0], l[1], l[2], l[3] = 0, 1, 9, 8  # empty, one row, just long, just not long
+        l[0], l[1], l[2], l[3], l[4], l[5] = 0, 1, 9, 8, 64, 65  # empty, one row, just (not) long, segment ends
     w = _custom(dev, tables, lens, weighted=(mode == "weighted"), pooling="mean" if mode == "mean" else "sum")
-    full_check(w, f"long split widths {mode}")
+    full_check(w, f"long pass widths {mode}")
 
 
-@pytest.mark.parametrize("long_len", ["0", "4096"])
+@pytest.mark.parametrize("long_len", ["0", "default", "4096"])
 def test_one_very_long_bag(dev, monkeypatch, long_len):
-    # a bag of 300 000 lookups among short ones: one wavefront per bag (the
-    # default), or split over the workgroup above 4096 lookups
+    # a bag of 300 000 lookups among short ones: one wavefront per bag
+    # (EB_LONG_BAG=0, and the default for a batch of half a million lookups),
+    # or the long-bag pass for bags of more than 4096 lookups, in segments of
+    # 2048 positions
     say(f"[parity] one very long bag, EB_LONG_BAG={long_len}")
-    monkeypatch.setenv("EB_LONG_BAG", long_len)
+    if long_len == "default":
+        monkeypatch.delenv("EB_LONG_BAG", raising=False)
+    else:
+        monkeypatch.setenv("EB_LONG_BAG", long_len)
     tables = [_table(dev, "f32", 100000, 64), _table(dev, "f16", 50000, 128, seed=1)]
     lens = [np.array([3, 300000, 0, 7, 4097, 1]), np.array([4096, 2, 200000, 0, 5, 9])]
     w = _custom(dev, tables, lens)
-    full_check(w, "very long bag")
+    got = full_check(w, "very long bag")
+    if long_len == "default":  # below 2^23 lookups: no pass unless asked for
+        monkeypatch.setenv("EB_LONG_BAG", "0")
+        assert np.array_equal(got.view(np.uint32), run_gpu(w).cpu().numpy().view(np.uint32))
+
+
+def test_long_bag_pass_by_default(dev, monkeypatch):
+    # a batch of more than 2^23 lookups with bags of 1 000 000, 4097 and 1025
+    # lookups among bags of about twenty: without EB_LONG_BAG the pass runs
+    # (the result is bit for bit that of EB_LONG_BAG=1024), and matches the
+    # oracle
+    say("[parity] long-bag pass by default on a large batch")
+    monkeypatch.delenv("EB_LONG_BAG", raising=False)
+    rng = np.random.default_rng(21)
+    B = 380000
+    lens = rng.integers(10, 31, B)
+    lens[[5, 77, 1000, 299999]] = [1_000_000, 4097, 1025, 1024]
+    assert lens.sum() >= 1 << 23
+    w = _custom(dev, [_table(dev, "f32", 100000, 16)], [lens])
+    got = full_check(w, "pass by default")
+    monkeypatch.setenv("EB_LONG_BAG", "1024")
+    assert np.array_equal(got.view(np.uint32), run_gpu(w).cpu().numpy().view(np.uint32))
 
 
 def test_padded_row_strides(dev):
@@ -586,7 +645,7 @@ def test_create_reports_out_of_memory(dev, monkeypatch):
         monkeypatch.setenv("EB_DEVICE_ALLOC_LIMIT", cap)
         st, h = create()
         assert st == eb.EB_ERR_OOM and h is None, (cap, st, h)
-    monkeypatch.setenv("EB_DEVICE_ALLOC_LIMIT", str(1 << 20))
+    monkeypatch.setenv("EB_DEVICE_ALLOC_LIMIT", str(1 << 22))
     st, h = create()
     assert st == eb.EB_OK and h
     out = torch.full((1, 16), float("nan"), device=dev)
