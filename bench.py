@@ -41,6 +41,7 @@ counted) + index bytes + offset bytes + weight bytes + output bytes.
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -220,6 +221,18 @@ def main():
     else:
         algo = [b.backward_algorithmic_bytes() for b in batches]
     nlook = [b.num_indices for b in batches]
+    # the lookup's long-bag pass runs for batches of at least 2^23 lookups
+    # unless EB_LONG_BAG says otherwise (its launch is part of every timed
+    # step then, whether or not a bag is long)
+    lb = os.environ.get("EB_LONG_BAG")
+    m = re.match(r"\s*([+-]?\d+)", lb or "")
+    lb_val = int(m.group(1)) if m else 0  # read as the library reads it
+    long_len = 1024 if lb is None or lb_val < 0 else lb_val
+    long_pass = long_len > 0 and (lb is not None or min(nlook) >= 1 << 23)
+    also_in_step = []
+    if long_pass and args.mode in ("forward", "fm"):
+        longest = max(int(b.lengths.max()) for b in batches)
+        also_in_step = [f"eb_long_pass_kernel ({'pools the bags of more than %d lookups' % long_len if longest > long_len else 'no bag is longer than %d lookups: it finds its queue empty' % long_len})"]
     torch.cuda.synchronize()
 
     stream = torch.cuda.Stream(device=dev)  # default priority
@@ -502,6 +515,8 @@ def main():
             "traffic_gbs": None if traffic is None else round(traffic / kern_avg_s / 1e9, 1),
             "traffic_frac": None if traffic is None else round(traffic / kern_avg_s / 1e9 / PEAK_HBM_GBS, 4),
             "kernel_ms_avg": round(kern_avg_s * 1e3, 5),
+            # what one timed step enqueues besides the named kernel
+            "also_in_step": also_in_step,
             "timed_launches": args.steps,
             "kernel_ms_p10": round(w10, 5),
             "kernel_ms_median": round(w50, 5),
