@@ -221,14 +221,16 @@ def main():
     else:
         algo = [b.backward_algorithmic_bytes() for b in batches]
     nlook = [b.num_indices for b in batches]
-    # the lookup's long-bag pass runs for batches of at least 2^23 lookups
-    # unless EB_LONG_BAG says otherwise (its launch is part of every timed
-    # step then, whether or not a bag is long)
+    # the lookup's long-bag pass runs for batches of at least 2^23 lookups or
+    # of 64 lookups per bag on average, unless EB_LONG_BAG says otherwise
+    # (its launch is part of every timed step then, whether or not a bag is
+    # long)
     lb = os.environ.get("EB_LONG_BAG")
     m = re.match(r"\s*([+-]?\d+)", lb or "")
     lb_val = int(m.group(1)) if m else 0  # read as the library reads it
     long_len = 1024 if lb is None or lb_val < 0 else lb_val
-    long_pass = long_len > 0 and (lb is not None or min(nlook) >= 1 << 23)
+    long_pass = long_len > 0 and (lb is not None or min(nlook) >= 1 << 23 or
+                                  min(n / b.num_bags for n, b in zip(nlook, batches)) >= 64)
     also_in_step = []
     if long_pass and args.mode in ("forward", "fm"):
         longest = max(int(b.lengths.max()) for b in batches)

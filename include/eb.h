@@ -64,7 +64,9 @@
  * against 30 ms on one wavefront.  The second kernel costs about 1.7 us per
  * call even when no bag is long, so by default it runs only for batches of
  * at least 2^23 lookups (numel(indices) >= 8388608), where that is under 1%
- * of the lookup; EB_LONG_BAG (below) turns it on for every batch.  The queue
+ * of the lookup, and for batches of at least 64 lookups per bag on average
+ * (numel(indices) >= 64 * T * B), which are the ones that hold bags of
+ * thousands; EB_LONG_BAG (below) turns it on for every batch.  The queue
  * lives in the handle: up to 16384 segments per call with one partial row of
  * the widest table each (at most 64 MiB; 8 MiB for rows of 128 values); the
  * bags whose segments do not fit are pooled by their own wavefront.  With no
@@ -98,10 +100,10 @@
  * EB_BWD_SORT_ITEMS=4|8|12|16 fixes the backward sort's blocks at 512
  * threads of that many elements (default: chosen per call from the number of
  * lookups and how many of the sort's workgroups the GPU holds at once).
- * EB_LONG_BAG=n (n > 0) runs the long-bag pass for batches of every size,
- * for bags of more than n lookups (without it: n = 1024, for batches of at
- * least 2^23 lookups); EB_LONG_BAG=0 turns the pass off (every bag is
- * pooled by one wavefront, no second kernel, no queue).  EB_LONG_SEG=s (a
+ * EB_LONG_BAG=n (n > 0) runs the long-bag pass for every batch, for bags of
+ * more than n lookups (without it: n = 1024, for the batches above);
+ * EB_LONG_BAG=0 turns the pass off (every bag is pooled by one wavefront,
+ * no second kernel, no queue).  EB_LONG_SEG=s (a
  * power of two from 64 to 2048, default 2048) sets the positions per segment.
  * Results do not depend on any of these, except that the long-bag pass
  * changes the order of a long bag's sum (within the same error bound).

@@ -48,8 +48,10 @@ constexpr int32_t kRemapMaxTables = 32;
 // (EB_LONG_BAG at create time) to a second kernel, which pools them in
 // segments of up to kLongSegMax positions spread over its workgroups.
 constexpr int64_t kDefaultLongBag = 1024;
-// Without EB_LONG_BAG the pass runs for batches of at least this many lookups.
+// Without EB_LONG_BAG the pass runs for batches of at least this many
+// lookups, or of at least this many lookups per bag on average.
 constexpr int64_t kLongPassMinLookups = (int64_t)1 << 23;
+constexpr int64_t kLongPassMinMean = 64;
 constexpr int32_t kDefaultLongSeg = 2048;          // positions per segment
 constexpr int32_t kLongSegMax = 2048;              // (a segment's indices are staged in LDS)
 constexpr int64_t kLqMaxEntries = 16384;           // segments queued per launch

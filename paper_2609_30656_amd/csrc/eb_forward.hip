@@ -29,8 +29,8 @@
 //     segment's indices staged in LDS and split over four wavefronts; the
 //     segments' partial sums are added in segment order.  By default this
 //     runs for batches of at least 2^23 lookups (below, the second kernel's
-//     launch would cost more than 1% of the lookup), and for any batch when
-//     EB_LONG_BAG is set.
+//     launch would cost more than 1% of the lookup) or of 64 lookups per bag
+//     on average, and for any batch when EB_LONG_BAG is set.
 // Rows wider than 1 KiB take several 1 KiB column passes.  This file also
 // holds the C ABI's handle creation and the checks shared by the entry points
 // that pool.
@@ -584,10 +584,14 @@ hipError_t launch_forward(const eb_tables *h, const eb_tensor &indices, const eb
   a.seg_log2 = h->long_seg_log2;
   a.lq = h->lq;
   // The pass costs one more kernel on the stream whether or not a bag needs
-  // it (on MI355X about 1.7 us: 8% of a 23 us lookup of a million lookups,
-  // under 1% from about eight million), so unless the handle asked for it
-  // (EB_LONG_BAG set) it runs only for batches that large.
-  const bool long_pass = h->lq.cap > 0 && (h->long_bag_forced || indices.numel >= kLongPassMinLookups);
+  // it (on MI355X about 1.7 us: 8% of a 23 us lookup of a million lookups in
+  // bags of twenty, under 1% from about eight million lookups), so unless
+  // the handle asked for it (EB_LONG_BAG set) it runs for batches that large,
+  // and for batches whose bags hold kLongPassMinMean lookups or more on
+  // average: bag lengths are long-tailed, so those are the batches that hold
+  // bags of thousands.
+  const bool long_pass = h->lq.cap > 0 && (h->long_bag_forced || indices.numel >= kLongPassMinLookups ||
+                                           indices.numel >= kLongPassMinMean * sh.num_bags);
   if (!long_pass) a.lq.cap = 0;  // the lookup queues nothing: every bag is its wavefront's
   a.num_indices = indices.numel;
   a.out_ld = h->sum_dim;

@@ -446,9 +446,9 @@ def test_long_bag_pass_every_width(dev, monkeypatch, mode):
 @pytest.mark.parametrize("long_len", ["0", "default", "4096"])
 def test_one_very_long_bag(dev, monkeypatch, long_len):
     # a bag of 300 000 lookups among short ones: one wavefront per bag
-    # (EB_LONG_BAG=0, and the default for a batch of half a million lookups),
-    # or the long-bag pass for bags of more than 4096 lookups, in segments of
-    # 2048 positions
+    # (EB_LONG_BAG=0), or the long-bag pass for bags of more than 1024 (the
+    # default here: 42 000 lookups per bag on average) or 4096 lookups, in
+    # segments of 2048 positions
     say(f"[parity] one very long bag, EB_LONG_BAG={long_len}")
     if long_len == "default":
         monkeypatch.delenv("EB_LONG_BAG", raising=False)
@@ -458,27 +458,32 @@ def test_one_very_long_bag(dev, monkeypatch, long_len):
     lens = [np.array([3, 300000, 0, 7, 4097, 1]), np.array([4096, 2, 200000, 0, 5, 9])]
     w = _custom(dev, tables, lens)
     got = full_check(w, "very long bag")
-    if long_len == "default":  # below 2^23 lookups: no pass unless asked for
-        monkeypatch.setenv("EB_LONG_BAG", "0")
+    if long_len == "default":  # the pass ran, at the default threshold
+        monkeypatch.setenv("EB_LONG_BAG", "1024")
         assert np.array_equal(got.view(np.uint32), run_gpu(w).cpu().numpy().view(np.uint32))
 
 
 def test_long_bag_pass_by_default(dev, monkeypatch):
-    # a batch of more than 2^23 lookups with bags of 1 000 000, 4097 and 1025
-    # lookups among bags of about twenty: without EB_LONG_BAG the pass runs
-    # (the result is bit for bit that of EB_LONG_BAG=1024), and matches the
-    # oracle
-    say("[parity] long-bag pass by default on a large batch")
-    monkeypatch.delenv("EB_LONG_BAG", raising=False)
+    # without EB_LONG_BAG the pass runs for batches of at least 2^23 lookups
+    # (or of 64 lookups per bag on average): a batch of 8.4 M lookups with
+    # bags of 1 000 000, 4097 and 1025 lookups among bags of about twenty
+    # gives the bits of EB_LONG_BAG=1024 and matches the oracle; a batch of
+    # 400 000 lookups in bags of about twenty, one of 5000, gives the bits of
+    # EB_LONG_BAG=0 (no pass)
+    say("[parity] long-bag pass by default")
     rng = np.random.default_rng(21)
-    B = 380000
-    lens = rng.integers(10, 31, B)
-    lens[[5, 77, 1000, 299999]] = [1_000_000, 4097, 1025, 1024]
-    assert lens.sum() >= 1 << 23
-    w = _custom(dev, [_table(dev, "f32", 100000, 16)], [lens])
-    got = full_check(w, "pass by default")
-    monkeypatch.setenv("EB_LONG_BAG", "1024")
-    assert np.array_equal(got.view(np.uint32), run_gpu(w).cpu().numpy().view(np.uint32))
+    table = _table(dev, "f32", 100000, 16)
+    for B, long_lens, same_as in [(380000, [1_000_000, 4097, 1025, 1024], "1024"), (20000, [5000], "0")]:
+        monkeypatch.delenv("EB_LONG_BAG", raising=False)
+        lens = rng.integers(10, 31, B)
+        lens[:len(long_lens)] = long_lens
+        rng.shuffle(lens)
+        big = lens.sum() >= 1 << 23
+        assert big == (same_as == "1024") and lens.mean() < 64
+        w = _custom(dev, [table], [lens])
+        got = full_check(w, f"default, B={B}")
+        monkeypatch.setenv("EB_LONG_BAG", same_as)
+        assert np.array_equal(got.view(np.uint32), run_gpu(w).cpu().numpy().view(np.uint32)), B
 
 
 def test_padded_row_strides(dev):
