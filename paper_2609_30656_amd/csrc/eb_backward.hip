@@ -403,24 +403,33 @@ __device__ __forceinline__ void sort_block(const BwdArgs &a, int32_t pass, int32
   const uint64_t below_me = (1ull << lane) - 1ull;
 #pragma unroll
   for (int i0 = 0; i0 < IPT; i0 += 4) {
-    uint32_t lead[4], old[4];
+    uint32_t lead[4], old[4], plo[4], phi[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int i = i0 + u;
-      dg[i] = (uint32_t)(e[i] >> shift) & dmask;
-      // a lane keeps the lanes whose bit q equals its own: the ballot of bit
-      // q, complemented where the lane's bit is 0 (m: the bit copied into
-      // every bit of a word)
-      uint32_t plo = ~0u, phi = ~0u;
-      for (int q = 0; q < bits; ++q) {
-        const uint32_t m = (uint32_t)((int32_t)(dg[i] << (31 - q)) >> 31);
+      dg[i0 + u] = (uint32_t)(e[i0 + u] >> shift) & dmask;
+      plo[u] = ~0u;
+      phi[u] = ~0u;
+    }
+    // a lane keeps the lanes whose bit q equals its own: the ballot of bit
+    // q, complemented where the lane's bit is 0 (m: the bit copied into
+    // every bit of a word, one signed bit-field extract).  Bit by bit for
+    // the four items at once, so their four chains of dependent operations
+    // interleave.
+    for (int q = 0; q < bits; ++q) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)dg[i0 + u], (uint32_t)q, 1u);
         const uint64_t bal = __ballot(m != 0u);
         // p & ~(ballot ^ m) as one three-input bitwise operation per half
         // (truth table 0x90: inputs p, ballot, m)
-        plo = __builtin_amdgcn_bitop3_b32(plo, (uint32_t)bal, m, 0x90);
-        phi = __builtin_amdgcn_bitop3_b32(phi, (uint32_t)(bal >> 32), m, 0x90);
+        plo[u] = __builtin_amdgcn_bitop3_b32(plo[u], (uint32_t)bal, m, 0x90);
+        phi[u] = __builtin_amdgcn_bitop3_b32(phi[u], (uint32_t)(bal >> 32), m, 0x90);
       }
-      const uint64_t peers = ((uint64_t)phi << 32) | plo;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u;
+      const uint64_t peers = ((uint64_t)phi[u] << 32) | plo[u];
       const uint64_t below = peers & below_me;
       rk[i] = (uint32_t)__builtin_popcountll(below);
       lead[u] = (uint32_t)__builtin_ctzll(peers);
