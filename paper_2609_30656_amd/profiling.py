@@ -184,8 +184,14 @@ def main(argv=None):
                 lines += [f"algorithmic_bytes_per_launch = {algo:.0f}",
                           f"algorithmic_GBps_at_average = {algo / avg:.1f}"]
     lines.append("# kernels of the profiled process by total time (workload generation included):")
-    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"]))[:8]:
+    top = sorted(rows, key=lambda r: -float(r["TotalDurationNs"]))
+    for r in top[:8]:
         lines.append(f"#   {r['Calls']:>5} calls  avg {float(r['AverageNs']) / 1e3:10.2f} us  {r['Name'][:100]}")
+    rest = [r for r in top[8:] if "eb::" in r["Name"]]
+    if rest:
+        lines.append("# the library's other kernels in the same process:")
+        for r in rest:
+            lines.append(f"#   {r['Calls']:>5} calls  avg {float(r['AverageNs']) / 1e3:10.2f} us  {r['Name'][:100]}")
     os.makedirs(PROFILES, exist_ok=True)
     with open(summary_path(mode, cfg, law, "kernel_trace"), "w") as f:
         f.write("\n".join(lines) + "\n")
