@@ -61,8 +61,9 @@
  * sums are added in segment order, so the result is deterministic (its
  * summation order differs from the one-wavefront order, within the same
  * error bound).  On MI355X a bag of a million lookups takes 0.13 ms so,
- * against 30 ms on one wavefront.  The second kernel costs about 1.7 us per
- * call even when no bag is long, so by default it runs only for batches of
+ * against 30 ms on one wavefront.  The second kernel costs a few
+ * microseconds per call even when no bag is long (1.7-6 us on MI355X), so
+ * by default it runs only for batches of
  * at least 2^23 lookups (numel(indices) >= 8388608), where that is under 1%
  * of the lookup, and for batches of at least 64 lookups per bag on average
  * (numel(indices) >= 64 * T * B), which are the ones that hold bags of

@@ -584,7 +584,7 @@ hipError_t launch_forward(const eb_tables *h, const eb_tensor &indices, const eb
   a.seg_log2 = h->long_seg_log2;
   a.lq = h->lq;
   // The pass costs one more kernel on the stream whether or not a bag needs
-  // it (on MI355X about 1.7 us: 8% of a 23 us lookup of a million lookups in
+  // it (on MI355X 1.7-6 us: 8% of a 23 us lookup of a million lookups in
   // bags of twenty, under 1% from about eight million lookups), so unless
   // the handle asked for it (EB_LONG_BAG set) it runs for batches that large,
   // and for batches whose bags hold kLongPassMinMean lookups or more on
