@@ -685,6 +685,50 @@ def test_checked_mode_reports_bad_data(dev, monkeypatch):
     assert ulp_distance(out.cpu().numpy(), ref).max() <= 1
 
 
+def test_checked_mode_through_the_long_bag_pass(dev, monkeypatch):
+    # bags of 40 lookups with EB_LONG_BAG=8, so every bag goes through the
+    # pass (segments of 64 positions): an index outside the table inside a
+    # long bag, and offsets that break the partition, are reported by
+    # checked mode; a good call after them pools correctly
+    say("[parity] checked mode through the long-bag pass")
+    monkeypatch.setenv("EB_CHECK", "1")
+    monkeypatch.setenv("EB_LONG_BAG", "8")
+    monkeypatch.setenv("EB_LONG_SEG", "64")
+    tb = _table(dev, "f32", 1000, 16)
+    w = _custom(dev, [tb], [np.array([40, 40, 40])], seed=9)
+    idx, off = w.indices, w.offsets
+    out = torch.empty((3, 16), device=dev)
+    with eb.eb_create_tables([tb]) as h:
+        for where, bad in ((45, 1000), (100, -3)):
+            b = idx.clone()
+            b[where] = bad
+            with pytest.raises(eb.EBError) as e:
+                eb.eb_forward(h, b, off, None, "sum", out)
+            assert e.value.status == eb.EB_ERR_INDEX_OOB
+        for bad_off in ([0, 40, 30, 120], [0, 40, 80, 130]):
+            with pytest.raises(eb.EBError) as e:
+                eb.eb_forward(h, idx, torch.tensor(bad_off, device=dev), None, "sum", out)
+            assert e.value.status == eb.EB_ERR_OFFSETS
+        eb.eb_forward(h, idx, off, None, "sum", out)
+    tabs = oracle_tables(w)
+    ref, asum = oracle_forward(w, tables=tabs)
+    check(out.cpu().numpy(), ref, asum, per_element_lengths(w), RTOL["f32"], "checked long pass",
+          split_scale(w, tabs))
+
+
+@pytest.mark.parametrize("index_dtype", [torch.int32, torch.int64])
+def test_long_bag_pass_index_types(dev, monkeypatch, index_dtype):
+    # the pass stages 32- and 64-bit indices alike (widened to 64 bits in LDS)
+    say(f"[parity] long-bag pass, {index_dtype} indices")
+    monkeypatch.setenv("EB_LONG_BAG", "32")
+    monkeypatch.setenv("EB_LONG_SEG", "64")
+    rng = np.random.default_rng(33)
+    tables = [_table(dev, "f16", 3000, 128), _table(dev, "int8_rowwise", 2000, 64, seed=1)]
+    lens = [rng.integers(0, 400, 40) for _ in tables]
+    w = _custom(dev, tables, lens, weighted=True, index_dtype=index_dtype)
+    full_check(w, f"long pass {index_dtype}")
+
+
 def test_native_library_is_the_one_loaded(dev):
     lib = eb.load_library()
     assert os.path.samefile(lib._name, eb.LIB_PATH)
