@@ -207,8 +207,9 @@ __device__ __forceinline__ void pool_bags(const TableMeta &m, const FwdArgs &a, 
 // end the launch long after the others, so a wavefront queues its bags of
 // more than long_len lookups for a second kernel and skips them:
 //   * before its loop, the wavefront finds its long bags from the offsets it
-//     holds (one ballot; nothing more when there is none, the usual case),
-//     and for each reserves K = ceil(L / seg) consecutive entries of the
+//     holds (the whole run's length from two lane reads, which settles the
+//     usual case; for a longer run, one ballot over its bags' lengths), and
+//     for each reserves K = ceil(L / seg) consecutive entries of the
 //     handle's queue with one atomic add, writing the bag's id and first
 //     entry into them.  A bag whose entries do not fit the queue is pooled
 //     by the wavefront as usual;
