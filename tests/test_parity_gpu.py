@@ -729,6 +729,38 @@ def test_long_bag_pass_index_types(dev, monkeypatch, index_dtype):
     full_check(w, f"long pass {index_dtype}")
 
 
+@pytest.mark.parametrize("case", range(12))
+def test_long_bag_pass_random_settings(dev, monkeypatch, case):
+    # seeded random mixes through the pass: two to four tables of any storage
+    # type and width, long-tailed bag lengths up to a few thousand, every
+    # pooling mode and index width, thresholds from 4 to 512 and segments
+    # from 64 to 2048 positions
+    rng = np.random.default_rng(700 + case)
+    dtypes = ["f32", "f16", "int8_rowwise", "int8_rowwise_split"]
+    nt = int(rng.integers(2, 5))
+    tables = []
+    for t in range(nt):
+        dt = dtypes[int(rng.integers(0, 4))]
+        mult = {"f32": 4, "f16": 8, "int8_rowwise": 16, "int8_rowwise_split": 16}[dt]
+        D = mult * int(rng.integers(1, 33))
+        tables.append(_table(dev, dt, int(rng.integers(50, 5000)), D, seed=case * 10 + t))
+    B = int(rng.integers(1, 60))
+    lens = [np.minimum(rng.lognormal(3.0, 1.6, B).astype(np.int64), 6000) for _ in tables]
+    mode = ["sum", "mean", "weighted"][case % 3]
+    long_len = str(int(rng.choice([4, 16, 64, 200, 512])))
+    seg = str(int(rng.choice([64, 128, 512, 2048])))
+    idt = torch.int32 if case % 4 == 1 else torch.int64
+    say(f"[parity] long-bag pass random case {case}: {nt} tables, B={B}, {mode}, long>{long_len}, seg {seg}, "
+        f"{idt}, longest {max(int(l.max()) for l in lens)}")
+    monkeypatch.setenv("EB_LONG_BAG", long_len)
+    monkeypatch.setenv("EB_LONG_SEG", seg)
+    w = _custom(dev, tables, lens, weighted=(mode == "weighted"), pooling="mean" if mode == "mean" else "sum",
+                index_dtype=idt, seed=case)
+    got = full_check(w, f"random case {case}")
+    # deterministic: the same call again gives the same bits
+    assert np.array_equal(got.view(np.uint32), run_gpu(w).cpu().numpy().view(np.uint32)), case
+
+
 def test_native_library_is_the_one_loaded(dev):
     lib = eb.load_library()
     assert os.path.samefile(lib._name, eb.LIB_PATH)
