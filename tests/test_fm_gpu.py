@@ -125,6 +125,18 @@ def test_reduced_configs(dev, name):
         assert torch.equal(fm.view(torch.int32), torch.zeros_like(fm).view(torch.int32))
 
 
+@pytest.mark.parametrize("name", ["c3a", "c5"])
+def test_with_the_long_bag_pass(dev, monkeypatch, name):
+    # most bags pooled by the long-bag pass (EB_LONG_BAG=16, segments of 64):
+    # eb_forward_fm's pooled output is still eb_forward's, bit for bit, and
+    # the term holds the oracle's bound
+    say(f"[fm] long-bag pass {name}")
+    monkeypatch.setenv("EB_LONG_BAG", "16")
+    monkeypatch.setenv("EB_LONG_SEG", "64")
+    w = make_workload(name, dev, **REDUCED[name])
+    full_fm_check(w, f"long-bag pass {name}")
+
+
 @pytest.mark.parametrize("name", ["c2", "c5"])
 def test_int32_indices(dev, name):
     say(f"[fm] int32 {name}")

@@ -541,13 +541,19 @@ def test_side_stream(dev):
 # argument errors through the ABI (host-side: nothing is enqueued)
 
 
-def test_threads_share_a_handle(dev):
-    # The handle is immutable after creation, so host threads may call the
-    # lookup on it at once (ctypes releases the GIL during the call).  Each
-    # thread writes its own output; every result equals a single-threaded call.
+@pytest.mark.parametrize("long_len", ["0", "16"])
+def test_threads_share_a_handle(dev, monkeypatch, long_len):
+    # Host threads may call the lookup on one handle at once (ctypes releases
+    # the GIL during the call): its tables and settings are fixed, and with
+    # the long-bag pass (EB_LONG_BAG=16: most bags queued) each call enqueues
+    # its lookup and pass under the handle's lock, so no pass takes another
+    # call's queue.  Each thread writes its own output; every result equals a
+    # single-threaded call.
     import threading
 
-    say("[parity] four host threads on one handle")
+    monkeypatch.setenv("EB_LONG_BAG", long_len)
+    monkeypatch.setenv("EB_LONG_SEG", "64")
+    say(f"[parity] four host threads on one handle, EB_LONG_BAG={long_len}")
     w = make_workload("c2", dev, **REDUCED["c2"])
     ws = [w] + [make_workload("c2", dev, batch_seed=s, tables=w.tables, **REDUCED["c2"]) for s in (1, 2, 3)]
     with eb.eb_create_tables(w.tables) as h:
