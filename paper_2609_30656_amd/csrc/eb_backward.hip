@@ -1445,10 +1445,20 @@ eb_status backward_update(const eb_tables *h, eb_tensor indices, eb_tensor offse
   // the keys kernel clears the digit counts and this call's part of the
   // look-back status
   a.zero_words = (int64_t)((L.hist_bytes + 8 * (size_t)L.passes * sort_nblk * ((size_t)1 << L.bits) + 15) / 16);
+  // Bags per keys wavefront: the lookup's rule (about sqrt(bags / resident
+  // wavefronts)), but at least enough to fit all wavefronts in about one
+  // set of resident ones, up to 8.  A keys wavefront spends most of its time
+  // waiting for its offsets and first index chunk, so a small batch gains
+  // from fewer, longer wavefronts: on MI355X c2's step 0.117 -> 0.114 ms
+  // (2 -> 7 bags), c3a's 0.368 -> 0.365 (4 -> 8); past 8 (c4 at 32 rather
+  // than 10) it lost 1%.
   int64_t k = 1;
   {
     const int64_t per_slot = num_bags / kResidentWaves;
     while ((k + 1) * (k + 1) <= per_slot) ++k;
+    int64_t fill = (num_bags + kResidentWaves - 1) / kResidentWaves;
+    fill = fill > 8 ? 8 : fill;
+    k = k < fill ? fill : k;
     k = k > kMaxBagsPerWave ? kMaxBagsPerWave : k;
   }
   a.bags_per_wave = (int32_t)k;
