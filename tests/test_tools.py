@@ -1,7 +1,7 @@
 """Host-side tools, on the CPU: the profile summaries' source hash (comments do
 not count, code does), the counter traffic that bench.py reports only while a
-summary matches the current kernel source, and bench.py's refusal of more
-than one GPU."""
+summary matches the current kernel source, that every committed summary does,
+and bench.py's refusal of more than one GPU."""
 import os
 import subprocess
 import sys
@@ -80,3 +80,22 @@ def test_counter_calibration_uses_the_last_copies(tmp_path):
     acc = profiling.read_counters(str(path), "eb_pool_kernel")
     assert acc["FETCH_SIZE"] == [1000.0] * 5
     assert acc["copy:FETCH_SIZE"] == [524288.0] * 3
+
+
+def test_committed_summaries_match_the_current_sources():
+    # every summary under profiles/ that names a kernel source hash was taken
+    # on the kernel as it is now: a kernel change without new summaries fails
+    checked, stale = 0, []
+    for name in sorted(os.listdir(profiling.PROFILES)):
+        path = os.path.join(profiling.PROFILES, name)
+        with open(path) as f:
+            hashes = [ln.split("=", 1)[1].split()[0] for ln in f if ln.startswith("kernel_source_sha256_16")]
+        if not hashes:
+            continue
+        modes = [m for m, (k, _) in profiling.KERNELS.items() if name.startswith(k + "_")]
+        assert len(modes) == 1, name
+        checked += 1
+        if hashes[0] != profiling.kernel_source_hash(modes[0]):
+            stale.append(name)
+    assert checked > 0
+    assert not stale, f"summaries taken on other kernel code: {stale}"
