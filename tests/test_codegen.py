@@ -1,5 +1,7 @@
-"""The built library's gfx950 code, on the CPU: no kernel reaches memory
-through flat (generic address space) instructions.  A flat access also counts
+"""The built library's gfx950 code, on the CPU: no barrier sits in a loop
+that exits by narrowing exec, no kernel spills vector registers to scratch,
+and no kernel reaches memory through flat (generic address space)
+instructions.  A flat access also counts
 against the LDS counter, so a wait for a cross-lane shuffle would wait for
 it too; every table row, optimizer state and partial sum is addressed in the
 global address space instead.  The code objects are unbundled from libeb.so
@@ -118,14 +120,24 @@ def barriers_in_divergent_loops(asm):
     return out
 
 
-def test_no_barrier_in_a_divergent_loop(tmp_path):
+@pytest.fixture(scope="module")
+def device_asm(tmp_path_factory):
+    """{source: compiler assembly (-S) of its gfx950 device code}, compiled once."""
     if not os.path.exists(HIPCC):
         pytest.skip("hipcc not found")
-    procs = {src: _device_asm(src, tmp_path / (src + ".s")) for src in SOURCES}
-    total = 0
+    d = tmp_path_factory.mktemp("asm")
+    procs = {src: _device_asm(src, d / (src + ".s")) for src in SOURCES}
+    out = {}
     for src, p in procs.items():
         assert p.wait(timeout=600) == 0, f"{src}: hipcc failed"
-        found = barriers_in_divergent_loops((tmp_path / (src + ".s")).read_text())
+        out[src] = (d / (src + ".s")).read_text()
+    return out
+
+
+def test_no_barrier_in_a_divergent_loop(device_asm):
+    total = 0
+    for src, text in device_asm.items():
+        found = barriers_in_divergent_loops(text)
         assert found, f"{src}: no kernel found in the assembly"
         for name, (nbar, bad) in found.items():
             total += nbar
@@ -153,3 +165,43 @@ def test_divergent_loop_check_flags_a_barrier_in_one():
     assert barriers_in_divergent_loops(asm) == {"_Zkern": (1, 1)}
     uniform = asm.replace("\ts_andn2_b64 exec, exec, s[0:1]", "\ts_cmp_lg_u32 s3, 0")
     assert barriers_in_divergent_loops(uniform) == {"_Zkern": (1, 0)}
+
+
+# ---------------------------------------------------------------------------
+# Register spills.  A kernel that spills vector registers keeps values in
+# scratch memory: one more round trip inside loops that are meant to be bound
+# by the row loads alone.  Every kernel is sized (batch depth, the occupancy
+# each asks the compiler for) to fit its vector registers; this keeps it so.
+# (Scalar registers that overflow go to lanes of vector registers, not to
+# memory, so they are reported but allowed.)
+
+def kernel_spills(asm):
+    """{kernel: (vgpr_count, vgpr_spill_count, sgpr_spill_count, scratch bytes
+    per lane)} from the code object metadata in compiler assembly."""
+    out = {}
+    for block in asm.split("  - .agpr_count:")[1:]:
+        f = {k: re.search(r"\." + k + r":\s+(\S+)", block) for k in
+             ("name", "vgpr_count", "vgpr_spill_count", "sgpr_spill_count", "private_segment_fixed_size")}
+        if all(f.values()):
+            out[f["name"].group(1)] = tuple(int(f[k].group(1)) for k in
+                                            ("vgpr_count", "vgpr_spill_count", "sgpr_spill_count",
+                                             "private_segment_fixed_size"))
+    return out
+
+
+def test_no_kernel_spills_vector_registers(device_asm):
+    total = 0
+    for src, text in device_asm.items():
+        found = kernel_spills(text)
+        assert found, f"{src}: no kernel metadata in the assembly"
+        total += len(found)
+        spilling = {k: v for k, v in found.items() if v[1] or v[3]}
+        assert not spilling, f"{src}: kernels with vector spills or scratch (vgprs, vgpr spills, sgpr spills, " \
+                             f"scratch bytes): {spilling}"
+    assert total > 50
+
+
+def test_spill_check_reads_the_metadata():
+    block = ("  - .agpr_count:     0\n    .name:           _Zk\n    .private_segment_fixed_size: 16\n"
+             "    .sgpr_spill_count: 0\n    .vgpr_count:     72\n    .vgpr_spill_count: 3\n")
+    assert kernel_spills("amdhsa.kernels:\n" + block) == {"_Zk": (72, 3, 0, 16)}
